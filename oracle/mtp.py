@@ -1,0 +1,110 @@
+"""Recurrent MTP draft head of the oracle (float64).
+
+Test infrastructure: imported only by the tests, the smoke check and the
+benchmark's CPU-baseline leg.
+
+The head (App. "Models and Draft Heads") drafts one position at a time from
+the hidden state and the token embedding of the position before it: the two
+are normalised by separate RMSNorms, concatenated (hidden first), projected
+2H -> H by a bias-free linear layer and passed through one decoder layer that
+keeps a KV cache of its own, one entry per position.  Embedding and output
+head are the backbone's.  Reading where the paper is silent: one final
+RMSNorm precedes the shared LM head, and the hidden carried along the chain
+is the decoder layer's output before that norm.
+
+Cycle restart (App. "Train--Inference Inconsistency under Teacher Forcing",
+Eqs. tf-restart and tf-restart-kv): behind the boundary every cache entry is
+computed from a target feature; the chain's own features enter the cache only
+through the current cycle's writes, which the next cycle discards, also when
+every draft was accepted.
+
+Indexing used here.  Let h_t be the target's last-layer hidden at position t
+(it predicts token x_{t+1}).  Cache slot s of the head holds the entry of the
+pair (h_s, x_{s+1}), rotated at position s + 1.  With m committed target
+positions before a step, the head's committed length is also m.  After the
+step accepted n drafts and drew the final token f, the extend rows are
+(h_m, d_1) .. (h_{m+n-1}, d_n), (h_{m+n}, f) at slots m .. m+n; the last row's
+output g_1 gives q_1 and the first new draft; chain step i feeds
+(g_{i-1}, d'_{i-1}) at slot m+n+i-1.  The committed length becomes m+n+1.
+
+Parity beyond the pass-through special cases in the tests is unpinned: the
+paper describes the head's composition in prose only.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from .numerics import Rounding, rmsnorm, softmax, inverse_cdf
+from .model import layer_forward, lm_head
+
+
+def _f64(a):
+    return np.asarray(a, dtype=np.float64)
+
+
+def mtp_apply(shape, Wm, W, h: np.ndarray, toks: np.ndarray, pos: np.ndarray,
+              cache_k: np.ndarray, cache_v: np.ndarray, rnd: Rounding):
+    """The head over R consecutive rows of one sequence.
+
+    h [R, H] conditioning hiddens, toks [R] tokens, pos [R] rotary positions,
+    cache [s, n_kv, d] entries the rows attend before their own.
+    Returns (g [R, H] layer outputs, logits [R, V], k [R,n_kv,d], v [R,n_kv,d])."""
+    a = rmsnorm(h, Wm["norm_h"], shape.rms_eps)
+    e = rmsnorm(_f64(W["embed"])[np.asarray(toks)], Wm["norm_e"], shape.rms_eps)
+    x = rnd(np.concatenate([a, e], axis=-1)) @ _f64(Wm["w_proj"]).T
+    g, k, v = layer_forward(shape, Wm["layer"], x[None], np.asarray(pos)[None],
+                            [cache_k], [cache_v], rnd)
+    head = {"final_norm": Wm["final_norm"], "lm_head": W["lm_head"]}
+    return g[0], lm_head(shape, head, g[0], rnd), k[0], v[0]
+
+
+def _draw(z: np.ndarray, u: float, mode: str, temperature: float) -> int:
+    z32 = z.astype(np.float32)
+    if mode == "greedy":
+        return int(np.argmax(z32))
+    return inverse_cdf(softmax(z32.astype(np.float64) / temperature), u)[0]
+
+
+def mtp_draft(shape, Wm, W, cache_k, cache_v, mtp_lens, hidden, n_accept, out_tokens,
+              u_draft, k: int, mode: str, temperature: float, rnd: Rounding):
+    """Draft the next block of every sequence.
+
+    cache_k[b] / cache_v[b] [>= mtp_lens[b], n_kv, d]: the head's cache;
+    hidden [B, k+1, H] target hiddens of the last verification; n_accept [B];
+    out_tokens [B, k+1] (accepted drafts then the final token); u_draft [B, k].
+    Returns dict(drafts [B, k], draft_logits [B, k, V], new_lens [B],
+    ext_k / ext_v: per sequence the committed extend entries [n_b+1, n_kv, d],
+    chain_k / chain_v: per sequence the transient chain entries [k-1, n_kv, d])."""
+    B = len(mtp_lens)
+    V = np.asarray(W["lm_head"]).shape[0]
+    drafts = np.zeros((B, k), dtype=np.int64)
+    dlog = np.zeros((B, k, V))
+    new_lens = np.zeros(B, dtype=np.int64)
+    ext_k, ext_v, ch_k, ch_v = [], [], [], []
+    for b in range(B):
+        m = int(mtp_lens[b])
+        R = int(n_accept[b]) + 1
+        kc, vc = _f64(cache_k[b][:m]), _f64(cache_v[b][:m])
+        g, logits, kn, vn = mtp_apply(shape, Wm, W, _f64(hidden[b, :R]), out_tokens[b, :R],
+                                      m + 1 + np.arange(R), kc, vc, rnd)
+        ext_k.append(kn)
+        ext_v.append(vn)
+        kc, vc = np.concatenate([kc, kn]), np.concatenate([vc, vn])
+        g_prev, z = g[-1], logits[-1]
+        ck, cv = [], []
+        for i in range(k):
+            dlog[b, i] = z
+            drafts[b, i] = _draw(z, u_draft[b, i], mode, temperature)
+            if i + 1 < k:
+                slot = m + R + i
+                g1, l1, k1, v1 = mtp_apply(shape, Wm, W, g_prev[None], [drafts[b, i]],
+                                           [slot + 1], kc, vc, rnd)
+                kc, vc = np.concatenate([kc, k1]), np.concatenate([vc, v1])
+                ck.append(k1[0])
+                cv.append(v1[0])
+                g_prev, z = g1[0], l1[0]
+        ch_k.append(np.array(ck))
+        ch_v.append(np.array(cv))
+        new_lens[b] = m + R
+    return dict(drafts=drafts, draft_logits=dlog, new_lens=new_lens,
+                ext_k=ext_k, ext_v=ext_v, chain_k=ch_k, chain_v=ch_v)

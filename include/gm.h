@@ -1,0 +1,226 @@
+/*
+ * gm.h -- C ABI of the batched speculative-decoding step (MI355X / gfx950).
+ *
+ * One step of speculative rollout generation for a batch of B sequences
+ * (GrowMTP, Sec. 2.2): the target verifies a block of k+1 positions per
+ * sequence in one forward (gm_verify_forward, gm_verify_attention), accepts a
+ * prefix of the k drafts and draws one more token (gm_spec_accept), commits
+ * the accepted KV entries and rolls back the rest (gm_kv_commit), and the MTP
+ * draft head proposes the next block (gm_mtp_draft).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers are DEVICE pointers unless a comment says "host".  Every buffer
+ *   is owned by the caller; no call keeps a pointer after it returns and no
+ *   call allocates or frees device memory.  Scratch memory is passed in as a
+ *   workspace whose size gm_workspace_size() reports.
+ * - Every call enqueues its kernels on `stream` (a hipStream_t; NULL is the
+ *   null stream) and returns without waiting for them.
+ * - Shapes and arguments are validated on the host before anything is
+ *   launched; a failed check returns a negative gm_status, launches nothing
+ *   and leaves a message for gm_last_error().  Faults that only the device
+ *   can see (a token id outside the vocabulary, a block-table entry outside
+ *   the page pool) are reported through the optional `dev_err` word: the
+ *   kernel ORs a GM_DEVERR_* bit into it and skips the offending access.
+ * - Outputs are bit-deterministic for fixed inputs (no reduction depends on
+ *   the order of atomics).
+ * - Token ids are int32.  Logits, uniforms and hidden states are float32.
+ *   Weights and KV entries use the model dtype: GM_F32 (float) or GM_BF16
+ *   (bfloat16 stored as uint16).  Norm weights use the model dtype too.
+ * - Block layout: block position i of sequence b (0 <= i <= k) is absolute
+ *   position m_b + i, where m_b = seq_lens[b] is the committed length; the
+ *   block is [t_m, d_1 .. d_k]: the pending token (drawn by the last cycle,
+ *   not yet in the cache) followed by the k drafts.
+ */
+#ifndef GM_H
+#define GM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GM_OK = 0,
+  GM_ERR_INVALID_ARG = -1,   /* null pointer, bad size or shape */
+  GM_ERR_UNSUPPORTED = -2,   /* a valid configuration this build does not implement */
+  GM_ERR_CAPACITY = -3,      /* the KV page table cannot hold the positions the call writes */
+  GM_ERR_WORKSPACE = -4,     /* workspace missing or smaller than gm_workspace_size() */
+  GM_ERR_DEVICE = -5         /* a HIP runtime call failed */
+} gm_status;
+
+enum { GM_DEVERR_TOKEN = 1, GM_DEVERR_PAGE = 2 };
+
+typedef enum { GM_F32 = 0, GM_BF16 = 1 } gm_dtype;
+typedef enum { GM_GREEDY = 0, GM_SAMPLE = 1 } gm_accept_mode;
+typedef enum {
+  GM_OP_VERIFY_FORWARD = 0,
+  GM_OP_VERIFY_ATTENTION = 1,
+  GM_OP_SPEC_ACCEPT = 2,
+  GM_OP_MTP_DRAFT = 3
+} gm_op;
+
+/* Decoder shape: pre-norm RMSNorm / RoPE (rotate-half, angle pos * base^(-2i/d))
+ * / grouped-query attention / SwiGLU, the layer of the paper's backbones
+ * (App. "Models and Draft Heads").  Limits of this build: head_dim 128 for
+ * GM_BF16 (64 or 128 for GM_F32), n_heads a multiple of n_kv_heads with
+ * (n_heads / n_kv_heads) * (k + 1) <= 64, hidden and ffn multiples of 64,
+ * GM_BF16 needs vocab, hidden, ffn and n_heads * head_dim multiples of 128. */
+typedef struct {
+  int n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab;
+  float rope_base;       /* 10000 */
+  float rms_eps;         /* 1e-6 */
+  int dtype;             /* gm_dtype */
+  int qk_norm;           /* 1: per-head RMSNorm of q and k before RoPE (Qwen3) */
+  int tie_embed;         /* informational: lm_head may alias embed */
+} gm_model_config;
+
+/* One decoder layer.  Linear weights are row-major [out, in] (y = W x). */
+typedef struct {
+  const void *attn_norm;  /* [H] */
+  const void *w_qkv;      /* [(n_heads + 2 n_kv_heads) head_dim, H]: the rows of W_q, then W_k, then W_v */
+  const void *q_norm;     /* [head_dim], or NULL when qk_norm == 0 */
+  const void *k_norm;     /* [head_dim], or NULL when qk_norm == 0 */
+  const void *w_o;        /* [H, n_heads head_dim] */
+  const void *ffn_norm;   /* [H] */
+  const void *w_gate_up;  /* [2 ffn, H]: the rows of W_gate, then W_up */
+  const void *w_down;     /* [H, ffn] */
+} gm_layer_weights;
+
+typedef struct {
+  const void *embed;                /* [vocab, H] */
+  const void *final_norm;           /* [H] */
+  const void *lm_head;              /* [vocab, H] */
+  const gm_layer_weights *layers;   /* host array [n_layers] */
+} gm_model_weights;
+
+/* The recurrent MTP draft head (App. "Models and Draft Heads"): RMSNorm_h of
+ * the conditioning hidden and RMSNorm_e of the token embedding, concatenated
+ * hidden first, a bias-free projection 2H -> H, one decoder layer with a KV
+ * cache of its own, a final RMSNorm and the backbone's LM head. */
+typedef struct {
+  const void *norm_h;      /* [H] */
+  const void *norm_e;      /* [H] */
+  const void *w_proj;      /* [H, 2H]: columns 0..H-1 act on RMSNorm_h(h), H..2H-1 on RMSNorm_e(E[t]) */
+  const void *final_norm;  /* [H] */
+  gm_layer_weights layer;
+} gm_mtp_weights;
+
+/* Paged KV cache.  Each layer owns two page pools, K and V, each
+ * [num_pages][n_kv_heads][page_size * head_dim] elements of the model dtype.
+ * Position t of sequence b lives in page block_table[b][t / page_size] at
+ * offset t % page_size.  Inside the block of one (page, kv head) the tokens
+ * come in tiles of 16 (tile j holds offsets 16j .. 16j+15) of 16 * head_dim
+ * elements, and inside a tile (token s = 0..15, channel c = 0..head_dim-1):
+ *   K element at  (c / 32) * 512 + ((c % 32) / 8) * 128 + s * 8 + c % 8
+ *   V element at  (c / 32) * 512 + (s / 4) * 128 + (c % 16) * 8 + ((c / 16) % 2) * 4 + s % 4
+ * so that one 64-lane load of 16 bytes per lane reads 1 KiB of the tile in
+ * the order the matrix-core operands take it.  page_size is a multiple of 16. */
+typedef struct {
+  void *const *k_pages;        /* host array [n_layers] of device bases */
+  void *const *v_pages;        /* host array [n_layers] of device bases */
+  int n_layers;
+  int page_size;
+  int num_pages;
+  int max_pages_per_seq;
+  const int32_t *block_table;  /* [B][max_pages_per_seq] */
+  int32_t *seq_lens;           /* [B] committed lengths m_b */
+  int max_ctx;                 /* host: an upper bound on every seq_lens[b] */
+} gm_kv_cache;
+
+/* Bytes of workspace the given call needs (0 on invalid arguments).
+ * `max_ctx` is the bound that the call's gm_kv_cache carries. */
+size_t gm_workspace_size(int op, const gm_model_config *cfg, int B, int k, int max_ctx);
+
+/* Verification forward (Sec. 3.1, Eq. verification-context; App.
+ * "Draft-Path Reconstruction": one target forward over the draft path).
+ * tokens [B][k+1] is the block [t_m, d_1..d_k].  Writes the K/V entries of
+ * the block at positions m_b .. m_b+k of every layer (seq_lens is not
+ * changed: gm_kv_commit decides what stays), logits [B][k+1][vocab] float32
+ * (row i is the target's distribution for the token after block position i)
+ * and hidden [B][k+1][H] float32, the last layer's output before the final
+ * RMSNorm (the feature the MTP head consumes).
+ * Errors: GM_ERR_CAPACITY if max_ctx + k + 1 > max_pages_per_seq * page_size. */
+gm_status gm_verify_forward(const gm_model_config *cfg, const gm_model_weights *w,
+                            const gm_kv_cache *cache, int B, int k, const int32_t *tokens,
+                            float *logits, float *hidden, void *ws, size_t ws_bytes,
+                            int32_t *dev_err, void *stream);
+
+/* Verify attention of one layer: the query at block position i of sequence b
+ * attends causally to cache positions 0 .. m_b + i (the committed prefix and
+ * block positions 0..i, which must already be in the cache), scale
+ * 1/sqrt(head_dim), query head h reading KV head h / (n_heads / n_kv_heads).
+ * q and out are [B][k+1][n_heads][head_dim] in the model dtype; q is after
+ * RoPE. */
+gm_status gm_verify_attention(const gm_model_config *cfg, const gm_kv_cache *cache, int layer,
+                              int B, int k, const void *q, void *out, void *ws, size_t ws_bytes,
+                              int32_t *dev_err, void *stream);
+
+/* Accept rule (Sec. 2.2, Eq. accept-rule).  p_i = softmax(target_logits[b][i] / T),
+ * q_i = softmax(draft_logits[b][i] / T).
+ * GM_SAMPLE: scanning i = 0..k-1, draft d_i is accepted iff u_accept[b][i] <
+ *   p_i(d_i) / q_i(d_i) (ratio rounded to float32); the scan stops at the
+ *   first rejection.  With n accepted, the final token is an inverse-CDF draw
+ *   with u_final[b] (smallest id x with sum_{y<=x} w(y) > u * sum w) from
+ *   w = max(0, p_n - q_n) if n < k (from p_n if that mass is 0), or from
+ *   w = p_k (bonus token) if n = k.
+ * GM_GREEDY: d_i is accepted iff it is the argmax of target_logits[b][i]
+ *   (lowest id on ties); the final token is the argmax of row n.
+ *   draft_logits, u_accept and u_final may be NULL.
+ * Outputs: n_accept [B] in [0, k]; out_tokens [B][k+1] = d_0..d_{n-1}, final, -1 pad.
+ * The logits rows are read in place; no probability matrix is written. */
+gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature,
+                         const float *target_logits, const float *draft_logits,
+                         const int32_t *draft_tokens, const float *u_accept, const float *u_final,
+                         int32_t *n_accept, int32_t *out_tokens, void *ws, size_t ws_bytes,
+                         void *stream);
+
+/* Commit / rollback (Sec. 2.2; App. "Train--Inference Inconsistency under
+ * Teacher Forcing", Eq. tf-restart-kv): block positions 0..n_b stay, the rest
+ * are rolled back by index only (no KV bytes move): seq_lens[b] += n_b + 1.
+ * committed_slots [B][k+1] (may be NULL) receives the physical slot
+ * (page * page_size + offset) of each committed block position, -1 for rolled
+ * back ones. */
+gm_status gm_kv_commit(const gm_kv_cache *cache, int B, int k, const int32_t *n_accept,
+                       int32_t *committed_slots, void *stream);
+
+/* MTP draft of the next block (Sec. 2.2; App. "Models and Draft Heads";
+ * Eqs. tf-restart, tf-restart-kv).  mtp_cache is a one-layer cache whose
+ * seq_lens hold the head's committed length, equal to the target's committed
+ * length before the last verification.  Slot s of the head's cache holds the
+ * entry of the pair (h_s, x_{s+1}) rotated at position s+1, where h_s is the
+ * target hidden at position s.  Extend: the n_b+1 rows (verify_hidden[b][i],
+ * out_tokens[b][i]), i = 0..n_b, are written at slots m_b..m_b+n_b and the
+ * head's length becomes m_b+n_b+1 (the entries behind the boundary come from
+ * target features).  The output of row n_b gives q_1; chain step j feeds
+ * (layer output of step j-1, draft j-1) at slot m_b+n_b+j; those entries lie
+ * past the committed length and are overwritten by the next extend.
+ * Drafts are argmax (GM_GREEDY) or inverse-CDF draws with u_draft[b][j]
+ * (GM_SAMPLE) from softmax(z / T).  Outputs: drafts [B][k],
+ * draft_logits [B][k][vocab] float32.  Errors: GM_ERR_CAPACITY if
+ * max_ctx + 2k + 1 > max_pages_per_seq * page_size of the head's cache. */
+gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weights *mtp,
+                       const gm_model_weights *shared, const gm_kv_cache *mtp_cache, int B, int k,
+                       int mode, float temperature, const float *verify_hidden,
+                       const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft,
+                       int32_t *drafts, float *draft_logits, void *ws, size_t ws_bytes,
+                       int32_t *dev_err, void *stream);
+
+/* Thread-local message describing the last non-OK status of this thread. */
+const char *gm_last_error(void);
+
+/* Kernel timing.  While tracing is on, every kernel the library launches
+ * whose name matches `filter` (all kernels when NULL) is bracketed by a pair
+ * of HIP events on its stream.  gm_trace_stop() waits for the recorded events
+ * and sums their durations per kernel name. */
+gm_status gm_trace_start(const char *filter);
+gm_status gm_trace_stop(void);
+int gm_trace_count(void);
+gm_status gm_trace_get(int i, const char **name, int *launches, double *total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GM_H */

@@ -1,0 +1,245 @@
+// C ABI of libgm: argument validation, workspace carving and kernel launches.
+// Every entry point validates on the host, then enqueues on the caller's
+// stream and returns without synchronising.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "forward.h"
+#include "launch.h"
+
+using namespace gm;
+
+namespace {
+thread_local std::string g_err;
+
+gm_status fail(gm_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+gm_status check_launch(const char *what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(GM_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+  return GM_OK;
+}
+
+constexpr int kMaxK = 15;
+
+// ---------------------------------------------------------------- workspace plans
+struct AcceptPlan {
+  size_t tstat, dstat, sel, wsum, psum, total;
+};
+AcceptPlan plan_accept(int B, int k, int V) {
+  Carve c;
+  AcceptPlan p;
+  const int nch = stat_chunks(V), nsc = scan_chunks(V);
+  p.tstat = c.take(sizeof(RowStat) * (size_t)B * (k + 1) * nch);
+  p.dstat = c.take(sizeof(RowStat) * (size_t)B * (k > 0 ? k : 1) * nch);
+  p.sel = c.take(sizeof(RowSel) * (size_t)B);
+  p.wsum = c.take(sizeof(double) * (size_t)B * nsc);
+  p.psum = c.take(sizeof(double) * (size_t)B * nsc);
+  p.total = c.off;
+  return p;
+}
+
+gm_status check_config(const gm_model_config *cfg, int B, int k) {
+  if (!cfg) return fail(GM_ERR_INVALID_ARG, "null model config");
+  if (B < 0) return fail(GM_ERR_INVALID_ARG, "B = %d < 0", B);
+  if (k < 0 || k > kMaxK) return fail(GM_ERR_UNSUPPORTED, "draft length k = %d outside [0, %d]", k, kMaxK);
+  if (cfg->n_layers < 1 || cfg->hidden < 1 || cfg->n_heads < 1 || cfg->n_kv_heads < 1 || cfg->head_dim < 1 ||
+      cfg->ffn < 1 || cfg->vocab < 1)
+    return fail(GM_ERR_INVALID_ARG, "non-positive model dimension");
+  if (cfg->n_heads % cfg->n_kv_heads) return fail(GM_ERR_INVALID_ARG, "n_heads %% n_kv_heads != 0");
+  if (cfg->dtype != GM_F32 && cfg->dtype != GM_BF16) return fail(GM_ERR_INVALID_ARG, "unknown dtype %d", cfg->dtype);
+  const int G = cfg->n_heads / cfg->n_kv_heads;
+  if (G * (k + 1) > kAttnMaxRows)
+    return fail(GM_ERR_UNSUPPORTED, "(n_heads / n_kv_heads) * (k + 1) = %d exceeds %d", G * (k + 1), kAttnMaxRows);
+  if (cfg->hidden % 64 || cfg->ffn % 64) return fail(GM_ERR_UNSUPPORTED, "hidden and ffn must be multiples of 64");
+  if (!(cfg->rms_eps >= 0.f) || !(cfg->rope_base > 0.f)) return fail(GM_ERR_INVALID_ARG, "bad rms_eps or rope_base");
+  if (cfg->dtype == GM_BF16) {
+    if (cfg->head_dim != 128) return fail(GM_ERR_UNSUPPORTED, "bf16 path needs head_dim 128, got %d", cfg->head_dim);
+    if (cfg->vocab % 128 || cfg->hidden % 128 || cfg->ffn % 128 || (cfg->n_heads * cfg->head_dim) % 128)
+      return fail(GM_ERR_UNSUPPORTED, "bf16 path needs vocab, hidden, ffn and n_heads*head_dim multiples of 128");
+  } else {
+    if (cfg->head_dim != 64 && cfg->head_dim != 128)
+      return fail(GM_ERR_UNSUPPORTED, "f32 path needs head_dim 64 or 128, got %d", cfg->head_dim);
+  }
+  return GM_OK;
+}
+
+gm_status check_layer(const gm_model_config *cfg, const gm_layer_weights *L, const char *what) {
+  if (!L->attn_norm || !L->w_qkv || !L->w_o || !L->ffn_norm || !L->w_gate_up || !L->w_down)
+    return fail(GM_ERR_INVALID_ARG, "%s: null layer weight", what);
+  if (cfg->qk_norm && (!L->q_norm || !L->k_norm)) return fail(GM_ERR_INVALID_ARG, "%s: qk_norm set but q_norm/k_norm null", what);
+  return GM_OK;
+}
+
+gm_status check_cache(const gm_model_config *cfg, const gm_kv_cache *c, int n_layers, int k_extra,
+                      const char *what) {
+  if (!c) return fail(GM_ERR_INVALID_ARG, "%s: null cache", what);
+  if (c->n_layers != n_layers) return fail(GM_ERR_INVALID_ARG, "%s: cache has %d layers, need %d", what, c->n_layers, n_layers);
+  if (!c->k_pages || !c->v_pages || !c->block_table || !c->seq_lens)
+    return fail(GM_ERR_INVALID_ARG, "%s: null cache pointer", what);
+  for (int l = 0; l < n_layers; ++l)
+    if (!c->k_pages[l] || !c->v_pages[l]) return fail(GM_ERR_INVALID_ARG, "%s: null page pool of layer %d", what, l);
+  if (c->page_size < 16 || c->page_size % 16) return fail(GM_ERR_UNSUPPORTED, "%s: page_size %d is not a multiple of 16", what, c->page_size);
+  if (c->num_pages < 1 || c->max_pages_per_seq < 1) return fail(GM_ERR_INVALID_ARG, "%s: empty page pool", what);
+  if (c->max_ctx < 0) return fail(GM_ERR_INVALID_ARG, "%s: max_ctx < 0", what);
+  if ((long)c->max_ctx + k_extra > (long)c->max_pages_per_seq * c->page_size)
+    return fail(GM_ERR_CAPACITY, "%s: max_ctx %d + %d positions exceed %d pages of %d", what, c->max_ctx, k_extra,
+                c->max_pages_per_seq, c->page_size);
+  (void)cfg;
+  return GM_OK;
+}
+
+gm_status check_ws(void *ws, size_t have, size_t need) {
+  if (need > have) return fail(GM_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", have, need);
+  if (need && !ws) return fail(GM_ERR_WORKSPACE, "null workspace");
+  if (((uintptr_t)ws) & 255) return fail(GM_ERR_WORKSPACE, "workspace not 256-byte aligned");
+  return GM_OK;
+}
+}  // namespace
+
+extern "C" const char *gm_last_error(void) { return g_err.c_str(); }
+
+extern "C" size_t gm_workspace_size(int op, const gm_model_config *cfg, int B, int k, int max_ctx) {
+  if (B < 0 || k < 0 || k > kMaxK || max_ctx < 0) return 0;
+  switch (op) {
+    case GM_OP_SPEC_ACCEPT:
+      if (!cfg || cfg->vocab < 1) return 0;
+      return plan_accept(B, k, cfg->vocab).total;
+    case GM_OP_VERIFY_FORWARD:
+      if (check_config(cfg, B, k) != GM_OK) return 0;
+      return plan_forward(*cfg, B, k, max_ctx).total;
+    case GM_OP_VERIFY_ATTENTION:
+      if (check_config(cfg, B, k) != GM_OK) return 0;
+      return plan_attention(*cfg, B, k + 1, max_ctx).total;
+    case GM_OP_MTP_DRAFT:
+      if (check_config(cfg, B, k) != GM_OK) return 0;
+      return plan_mtp(*cfg, B, k, max_ctx).total;
+    default:
+      return 0;
+  }
+}
+
+// ---------------------------------------------------------------- gm_spec_accept
+extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature, const float *target_logits,
+                                    const float *draft_logits, const int32_t *draft_tokens, const float *u_accept,
+                                    const float *u_final, int32_t *n_accept, int32_t *out_tokens, void *ws,
+                                    size_t ws_bytes, void *stream) {
+  if (B < 0 || k < 0 || k > kMaxK || V < 1) return fail(GM_ERR_INVALID_ARG, "bad B=%d k=%d V=%d", B, k, V);
+  if (mode != GM_GREEDY && mode != GM_SAMPLE) return fail(GM_ERR_INVALID_ARG, "unknown accept mode %d", mode);
+  if (!(temperature > 0.f)) return fail(GM_ERR_INVALID_ARG, "temperature must be > 0");
+  if (B == 0) return GM_OK;
+  if (!target_logits || !n_accept || !out_tokens) return fail(GM_ERR_INVALID_ARG, "null target_logits / outputs");
+  if (k > 0 && !draft_tokens) return fail(GM_ERR_INVALID_ARG, "null draft_tokens");
+  if (mode == GM_SAMPLE) {
+    if (!u_final) return fail(GM_ERR_INVALID_ARG, "sample mode needs u_final");
+    if (k > 0 && (!draft_logits || !u_accept)) return fail(GM_ERR_INVALID_ARG, "sample mode needs draft_logits and u_accept");
+  }
+  const AcceptPlan p = plan_accept(B, k, V);
+  gm_status st = check_ws(ws, ws_bytes, p.total);
+  if (st != GM_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  char *w = (char *)ws;
+  RowStat *tstat = (RowStat *)(w + p.tstat), *dstat = (RowStat *)(w + p.dstat);
+  RowSel *sel = (RowSel *)(w + p.sel);
+  const float inv_t = 1.0f / temperature;
+  launch_row_stats(target_logits, V, B * (k + 1), V, inv_t, tstat, s);
+  if (mode == GM_SAMPLE && k > 0) launch_row_stats(draft_logits, V, B * k, V, inv_t, dstat, s);
+  launch_accept_decide(B, k, V, mode, inv_t, target_logits, draft_logits, tstat, dstat, draft_tokens, u_accept,
+                       u_final, n_accept, out_tokens, sel, s);
+  if (mode == GM_SAMPLE) launch_residual_draw(B, V, inv_t, sel, (double *)(w + p.wsum), (double *)(w + p.psum), s);
+  return check_launch("gm_spec_accept");
+}
+
+// ---------------------------------------------------------------- gm_kv_commit
+extern "C" gm_status gm_kv_commit(const gm_kv_cache *cache, int B, int k, const int32_t *n_accept,
+                                  int32_t *committed_slots, void *stream) {
+  if (!cache || !cache->block_table || !cache->seq_lens) return fail(GM_ERR_INVALID_ARG, "null cache");
+  if (B < 0 || k < 0 || k > kMaxK) return fail(GM_ERR_INVALID_ARG, "bad B=%d k=%d", B, k);
+  if (cache->page_size < 1 || cache->max_pages_per_seq < 1) return fail(GM_ERR_INVALID_ARG, "bad page geometry");
+  if (B == 0) return GM_OK;
+  if (!n_accept) return fail(GM_ERR_INVALID_ARG, "null n_accept");
+  launch_kv_commit(B, k, cache->page_size, cache->max_pages_per_seq, cache->block_table, cache->seq_lens, n_accept,
+                   committed_slots, (hipStream_t)stream);
+  return check_launch("gm_kv_commit");
+}
+
+// ---------------------------------------------------------------- gm_verify_attention
+extern "C" gm_status gm_verify_attention(const gm_model_config *cfg, const gm_kv_cache *cache, int layer, int B,
+                                         int k, const void *q, void *out, void *ws, size_t ws_bytes,
+                                         int32_t *dev_err, void *stream) {
+  gm_status st = check_config(cfg, B, k);
+  if (st != GM_OK) return st;
+  if (!cache) return fail(GM_ERR_INVALID_ARG, "null cache");
+  if (layer < 0 || layer >= cache->n_layers) return fail(GM_ERR_INVALID_ARG, "layer %d outside [0, %d)", layer, cache->n_layers);
+  st = check_cache(cfg, cache, cache->n_layers, k + 1, "gm_verify_attention");
+  if (st != GM_OK) return st;
+  if (B == 0) return GM_OK;
+  if (!q || !out) return fail(GM_ERR_INVALID_ARG, "null q / out");
+  const AttnPlan p = plan_attention(*cfg, B, k + 1, cache->max_ctx);
+  st = check_ws(ws, ws_bytes, p.total);
+  if (st != GM_OK) return st;
+  AttnArgs a = attn_args(*cfg, *cache, layer, B, k + 1, cache->seq_lens, 0, nullptr);
+  a.q = q;
+  a.out = out;
+  a.dev_err = dev_err;
+  run_attention(a, p, (char *)ws, (hipStream_t)stream);
+  return check_launch("gm_verify_attention");
+}
+
+// ---------------------------------------------------------------- gm_verify_forward
+extern "C" gm_status gm_verify_forward(const gm_model_config *cfg, const gm_model_weights *w, const gm_kv_cache *cache,
+                                       int B, int k, const int32_t *tokens, float *logits, float *hidden, void *ws,
+                                       size_t ws_bytes, int32_t *dev_err, void *stream) {
+  gm_status st = check_config(cfg, B, k);
+  if (st != GM_OK) return st;
+  if (!w || !w->embed || !w->final_norm || !w->lm_head || !w->layers) return fail(GM_ERR_INVALID_ARG, "null model weights");
+  for (int l = 0; l < cfg->n_layers; ++l)
+    if ((st = check_layer(cfg, &w->layers[l], "gm_verify_forward")) != GM_OK) return st;
+  st = check_cache(cfg, cache, cfg->n_layers, k + 1, "gm_verify_forward");
+  if (st != GM_OK) return st;
+  if (B == 0) return GM_OK;
+  if (!tokens || !logits || !hidden) return fail(GM_ERR_INVALID_ARG, "null tokens / logits / hidden");
+  const ForwardPlan p = plan_forward(*cfg, B, k, cache->max_ctx);
+  st = check_ws(ws, ws_bytes, p.total);
+  if (st != GM_OK) return st;
+  run_verify_forward(*cfg, *w, *cache, B, k, tokens, logits, hidden, p, (char *)ws, dev_err, (hipStream_t)stream);
+  return check_launch("gm_verify_forward");
+}
+
+// ---------------------------------------------------------------- gm_mtp_draft
+extern "C" gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weights *mtp, const gm_model_weights *shared,
+                                  const gm_kv_cache *mtp_cache, int B, int k, int mode, float temperature,
+                                  const float *verify_hidden, const int32_t *n_accept, const int32_t *out_tokens,
+                                  const float *u_draft, int32_t *drafts, float *draft_logits, void *ws,
+                                  size_t ws_bytes, int32_t *dev_err, void *stream) {
+  gm_status st = check_config(cfg, B, k);
+  if (st != GM_OK) return st;
+  if (k < 1) return fail(GM_ERR_INVALID_ARG, "gm_mtp_draft needs k >= 1");
+  if (mode != GM_GREEDY && mode != GM_SAMPLE) return fail(GM_ERR_INVALID_ARG, "unknown draft mode %d", mode);
+  if (!(temperature > 0.f)) return fail(GM_ERR_INVALID_ARG, "temperature must be > 0");
+  if (!mtp || !mtp->norm_h || !mtp->norm_e || !mtp->w_proj || !mtp->final_norm) return fail(GM_ERR_INVALID_ARG, "null MTP weights");
+  if ((st = check_layer(cfg, &mtp->layer, "gm_mtp_draft")) != GM_OK) return st;
+  if (!shared || !shared->embed || !shared->lm_head) return fail(GM_ERR_INVALID_ARG, "null shared embedding / LM head");
+  st = check_cache(cfg, mtp_cache, 1, 2 * k + 1, "gm_mtp_draft");
+  if (st != GM_OK) return st;
+  if (B == 0) return GM_OK;
+  if (!verify_hidden || !n_accept || !out_tokens || !drafts || !draft_logits)
+    return fail(GM_ERR_INVALID_ARG, "null MTP input / output");
+  if (mode == GM_SAMPLE && !u_draft) return fail(GM_ERR_INVALID_ARG, "sample mode needs u_draft");
+  const MtpPlan p = plan_mtp(*cfg, B, k, mtp_cache->max_ctx);
+  st = check_ws(ws, ws_bytes, p.total);
+  if (st != GM_OK) return st;
+  run_mtp_draft(*cfg, *mtp, *shared, *mtp_cache, B, k, mode, 1.0f / temperature, verify_hidden, n_accept, out_tokens,
+                u_draft, drafts, draft_logits, p, (char *)ws, dev_err, (hipStream_t)stream);
+  return check_launch("gm_mtp_draft");
+}

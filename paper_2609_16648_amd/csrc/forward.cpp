@@ -1,0 +1,192 @@
+// Orchestration of the verify forward (Sec. 3.1, Eq. verification-context)
+// and of the MTP draft (App. "Models and Draft Heads"; Eqs. tf-restart,
+// tf-restart-kv) as sequences of kernel launches on one stream.
+#include "forward.h"
+
+namespace gm {
+
+namespace {
+size_t esize(int dtype) { return dtype == GM_BF16 ? 2 : 4; }
+int qkv_width(const gm_model_config &c) { return (c.n_heads + 2 * c.n_kv_heads) * c.head_dim; }
+
+RopeArgs rope_args(const gm_model_config &cfg, const gm_kv_cache &c, int layer, int M, int R, const float *qkv,
+                   void *q_out, const int32_t *base, int base_off, const int32_t *blk_len, int pos_off,
+                   const gm_layer_weights &L, int32_t *dev_err) {
+  RopeArgs a{};
+  a.dtype = cfg.dtype;
+  a.M = M;
+  a.R = R;
+  a.n_heads = cfg.n_heads;
+  a.n_kv = cfg.n_kv_heads;
+  a.head_dim = cfg.head_dim;
+  a.qkv = qkv;
+  a.q_out = q_out;
+  a.k_pages = c.k_pages[layer];
+  a.v_pages = c.v_pages[layer];
+  a.block_table = c.block_table;
+  a.page_size = c.page_size;
+  a.max_pages = c.max_pages_per_seq;
+  a.num_pages = c.num_pages;
+  a.base_lens = base;
+  a.base_off = base_off;
+  a.blk_len = blk_len;
+  a.blk_len_add = blk_len ? 1 : 0;
+  a.pos_off = pos_off;
+  a.rope_base = cfg.rope_base;
+  a.eps = cfg.rms_eps;
+  a.q_norm = cfg.qk_norm ? L.q_norm : nullptr;
+  a.k_norm = cfg.qk_norm ? L.k_norm : nullptr;
+  a.dev_err = dev_err;
+  return a;
+}
+}  // namespace
+
+// ---------------------------------------------------------------- verify forward
+ForwardPlan plan_forward(const gm_model_config &cfg, int B, int k, int max_ctx) {
+  ForwardPlan p{};
+  const size_t M = (size_t)B * (k + 1), e = esize(cfg.dtype);
+  const size_t qd = (size_t)cfg.n_heads * cfg.head_dim;
+  Carve c;
+  p.nbuf = c.take(M * cfg.hidden * e);
+  p.act = c.take(M * cfg.ffn * e);
+  p.qkv = c.take(M * qkv_width(cfg) * sizeof(float));
+  p.q = c.take(M * qd * e);
+  p.attn = c.take(M * qd * e);
+  p.attn_plan = plan_attention(cfg, B, k + 1, max_ctx);
+  p.attn_ws = c.take(p.attn_plan.total);
+  p.total = c.off;
+  return p;
+}
+
+// One target forward over the block of every sequence.  The residual stream
+// lives in `hidden` (float32); it is the last layer's output at the end.
+void run_verify_forward(const gm_model_config &cfg, const gm_model_weights &w, const gm_kv_cache &c, int B, int k,
+                        const int32_t *tokens, float *logits, float *hidden, const ForwardPlan &p, char *ws,
+                        int32_t *dev_err, hipStream_t s) {
+  const int R = k + 1, M = B * R, H = cfg.hidden, F = cfg.ffn, V = cfg.vocab, dt = cfg.dtype;
+  const int qd = cfg.n_heads * cfg.head_dim;
+  void *nbuf = ws + p.nbuf, *act = ws + p.act, *q = ws + p.q, *attn = ws + p.attn;
+  float *qkv = (float *)(ws + p.qkv);
+  float *x = hidden;
+  launch_embed(dt, M, H, V, tokens, w.embed, x, dev_err, s);
+  for (int l = 0; l < cfg.n_layers; ++l) {
+    const gm_layer_weights &L = w.layers[l];
+    launch_rmsnorm(dt, M, H, cfg.rms_eps, x, L.attn_norm, nbuf, s);
+    launch_gemm("gemm_qkv", dt, EPI_STORE_F32, M, qkv_width(cfg), H, nbuf, H, L.w_qkv, qkv, qkv_width(cfg), s);
+    launch_rope_append(rope_args(cfg, c, l, M, R, qkv, q, c.seq_lens, 0, nullptr, 0, L, dev_err), s);
+    AttnArgs a = attn_args(cfg, c, l, B, R, c.seq_lens, 0, nullptr);
+    a.q = q;
+    a.out = attn;
+    a.dev_err = dev_err;
+    run_attention(a, p.attn_plan, ws + p.attn_ws, s);
+    launch_gemm("gemm_o", dt, EPI_ADD_F32, M, H, qd, attn, qd, L.w_o, x, H, s);
+    launch_rmsnorm(dt, M, H, cfg.rms_eps, x, L.ffn_norm, nbuf, s);
+    launch_gemm("gemm_gate_up", dt, EPI_SWIGLU, M, F, H, nbuf, H, L.w_gate_up, act, F, s);
+    launch_gemm("gemm_down", dt, EPI_ADD_F32, M, H, F, act, F, L.w_down, x, H, s);
+  }
+  launch_rmsnorm(dt, M, H, cfg.rms_eps, x, w.final_norm, nbuf, s);
+  launch_gemm("gemm_lm_head", dt, EPI_STORE_F32, M, V, H, nbuf, H, w.lm_head, logits, V, s);
+}
+
+// ---------------------------------------------------------------- MTP draft
+MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx) {
+  MtpPlan p{};
+  const size_t R = k + 1, Me = (size_t)B * R, e = esize(cfg.dtype), H = cfg.hidden;
+  const size_t qd = (size_t)cfg.n_heads * cfg.head_dim;
+  Carve c;
+  p.u = c.take(Me * 2 * H * e);
+  p.x = c.take(Me * H * sizeof(float));
+  p.xg = c.take((size_t)B * H * sizeof(float));
+  p.nbuf = c.take(Me * H * e);
+  p.act = c.take((size_t)B * cfg.ffn * e);
+  p.qkv = c.take(Me * qkv_width(cfg) * sizeof(float));
+  p.q = c.take(Me * qd * e);
+  p.attn = c.take(Me * qd * e);
+  p.attn_g = c.take((size_t)B * qd * e);
+  p.attn_ext = plan_attention(cfg, B, (int)R, max_ctx);
+  p.attn_chain = plan_attention(cfg, B, 1, max_ctx + 2 * k);
+  p.attn_ws = c.take(p.attn_ext.total > p.attn_chain.total ? p.attn_ext.total : p.attn_chain.total);
+  const int V = cfg.vocab;
+  p.stat = c.take(sizeof(RowStat) * (size_t)B * stat_chunks(V));
+  p.sel = c.take(sizeof(RowSel) * (size_t)B);
+  p.wsum = c.take(sizeof(double) * (size_t)B * scan_chunks(V));
+  p.psum = c.take(sizeof(double) * (size_t)B * scan_chunks(V));
+  p.total = c.off;
+  return p;
+}
+
+// Extend the head's cache with the n_b + 1 rows of target features behind the
+// new boundary, then run the chain of k drafts.  Only the K/V projection of
+// the first n_b extend rows is needed; the rest of the layer runs on the last
+// row of each sequence (and on the single row of every chain step).
+void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const gm_model_weights &shared,
+                   const gm_kv_cache &c, int B, int k, int mode, float inv_t, const float *verify_hidden,
+                   const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft, int32_t *drafts,
+                   float *draft_logits, const MtpPlan &p, char *ws, int32_t *dev_err, hipStream_t s) {
+  const int R = k + 1, Me = B * R, H = cfg.hidden, F = cfg.ffn, V = cfg.vocab, dt = cfg.dtype;
+  const int qd = cfg.n_heads * cfg.head_dim, qw = qkv_width(cfg);
+  const size_t e = esize(dt);
+  const gm_layer_weights &L = mtp.layer;
+  void *u = ws + p.u, *nbuf = ws + p.nbuf, *act = ws + p.act, *q = ws + p.q, *attn = ws + p.attn,
+       *attn_g = ws + p.attn_g;
+  float *x = (float *)(ws + p.x), *xg = (float *)(ws + p.xg), *qkv = (float *)(ws + p.qkv);
+  RowStat *stat = (RowStat *)(ws + p.stat);
+  RowSel *sel = (RowSel *)(ws + p.sel);
+  double *wsum = (double *)(ws + p.wsum), *psum = (double *)(ws + p.psum);
+  int32_t *lens = c.seq_lens;
+
+  // the layer tail on one row per sequence (x1 [B][H] float32 in place), then the
+  // shared LM head into draft_logits[:, j, :] and the draw of drafts[:, j]
+  auto tail_and_draw = [&](float *x1, int j) {
+    launch_gemm("mtp_gemm_o", dt, EPI_ADD_F32, B, H, qd, attn_g, qd, L.w_o, x1, H, s);
+    launch_rmsnorm(dt, B, H, cfg.rms_eps, x1, L.ffn_norm, nbuf, s);
+    launch_gemm("mtp_gemm_gate_up", dt, EPI_SWIGLU, B, F, H, nbuf, H, L.w_gate_up, act, F, s);
+    launch_gemm("mtp_gemm_down", dt, EPI_ADD_F32, B, H, F, act, F, L.w_down, x1, H, s);
+    launch_rmsnorm(dt, B, H, cfg.rms_eps, x1, mtp.final_norm, nbuf, s);
+    float *zl = draft_logits + (long)j * V;
+    launch_gemm("mtp_gemm_lm_head", dt, EPI_STORE_F32, B, V, H, nbuf, H, shared.lm_head, zl, (long)k * V, s);
+    launch_row_stats(zl, (long)k * V, B, V, inv_t, stat, s);
+    launch_draft_select(B, V, mode, inv_t, zl, (long)k * V, stat, u_draft ? u_draft + j : nullptr, k, drafts + j, k,
+                        sel, s);
+    if (mode == GM_SAMPLE) launch_residual_draw(B, V, inv_t, sel, wsum, psum, s);
+  };
+
+  // ---- extend: rows (h_{m+i}, x_{m+i+1}), i = 0..n_b, at slots m_b + i
+  launch_mtp_input(dt, Me, H, V, cfg.rms_eps, verify_hidden, out_tokens, 1, shared.embed, mtp.norm_h, mtp.norm_e, u,
+                   dev_err, s);
+  launch_gemm("mtp_gemm_proj", dt, EPI_STORE_F32, Me, H, 2 * H, u, 2 * H, mtp.w_proj, x, H, s);
+  launch_rmsnorm(dt, Me, H, cfg.rms_eps, x, L.attn_norm, nbuf, s);
+  launch_gemm("mtp_gemm_qkv", dt, EPI_STORE_F32, Me, qw, H, nbuf, H, L.w_qkv, qkv, qw, s);
+  launch_rope_append(rope_args(cfg, c, 0, Me, R, qkv, q, lens, 0, n_accept, 1, L, dev_err), s);
+  {
+    AttnArgs a = attn_args(cfg, c, 0, B, R, lens, 0, n_accept);
+    a.blk_len_add = 1;
+    a.q = q;
+    a.out = attn;
+    a.dev_err = dev_err;
+    run_attention(a, p.attn_ext, ws + p.attn_ws, s);
+  }
+  launch_gather_rows(B, R, qd, e, attn, n_accept, attn_g, s);
+  launch_gather_rows(B, R, H, sizeof(float), x, n_accept, xg, s);
+  // the head's committed length moves to the new boundary m_b + n_b + 1
+  launch_kv_commit(B, k, c.page_size, c.max_pages_per_seq, c.block_table, lens, n_accept, nullptr, s);
+  tail_and_draw(xg, 0);
+
+  // ---- chain: step j feeds (g_{j-1}, d_{j-1}) at slot boundary + j - 1
+  for (int j = 1; j < k; ++j) {
+    launch_mtp_input(dt, B, H, V, cfg.rms_eps, xg, drafts + (j - 1), k, shared.embed, mtp.norm_h, mtp.norm_e, u,
+                     dev_err, s);
+    launch_gemm("mtp_gemm_proj", dt, EPI_STORE_F32, B, H, 2 * H, u, 2 * H, mtp.w_proj, xg, H, s);
+    launch_rmsnorm(dt, B, H, cfg.rms_eps, xg, L.attn_norm, nbuf, s);
+    launch_gemm("mtp_gemm_qkv", dt, EPI_STORE_F32, B, qw, H, nbuf, H, L.w_qkv, qkv, qw, s);
+    launch_rope_append(rope_args(cfg, c, 0, B, 1, qkv, q, lens, j - 1, nullptr, 1, L, dev_err), s);
+    AttnArgs a = attn_args(cfg, c, 0, B, 1, lens, j - 1, nullptr);
+    a.q = q;
+    a.out = attn_g;
+    a.dev_err = dev_err;
+    run_attention(a, p.attn_chain, ws + p.attn_ws, s);
+    tail_and_draw(xg, j);
+  }
+}
+
+}  // namespace gm

@@ -1,0 +1,105 @@
+// Internal interfaces of the verify forward, verify attention and MTP draft.
+#pragma once
+
+#include "../../include/gm.h"
+#include "launch.h"
+
+namespace gm {
+
+constexpr int kAttnMaxRows = 64;   // (n_heads / n_kv_heads) * block rows per KV head
+
+struct Carve {
+  size_t off = 0;
+  size_t take(size_t n) {
+    size_t o = off;
+    off += (n + 255) & ~size_t(255);
+    return o;
+  }
+};
+
+// ---------------------------------------------------------------- attention
+struct AttnPlan {
+  int splits;          // context splits per (sequence, kv head)
+  int split_tokens;    // tokens per split (multiple of 16)
+  int rows_pad;        // 16-row tiles * 16
+  size_t part_o, part_ml, total;
+};
+AttnPlan plan_attention(const gm_model_config &cfg, int B, int R, int max_ctx);
+
+struct AttnArgs {
+  int dtype, B, R, n_heads, n_kv, head_dim;
+  int page_size, max_pages, num_pages;
+  const void *k_pages, *v_pages;
+  const int32_t *block_table;
+  const int32_t *base_lens;   // block start of sequence b: base_lens[b] + base_off
+  int base_off;
+  const int32_t *blk_len;     // rows of the block that are valid (< R), or null: all R
+  int blk_len_add;            // valid rows = blk_len[b] + blk_len_add
+  const void *q;              // [B][R][n_heads][head_dim] model dtype, after RoPE
+  void *out;                  // [B][R][n_heads][head_dim] model dtype
+  int32_t *dev_err;
+  float scale;                // 1 / sqrt(head_dim)
+};
+AttnArgs attn_args(const gm_model_config &cfg, const gm_kv_cache &c, int layer, int B, int R,
+                   const int32_t *base_lens, int base_off, const int32_t *blk_len);
+void run_attention(const AttnArgs &a, const AttnPlan &p, char *ws, hipStream_t s);
+
+// ---------------------------------------------------------------- GEMM  Y[M,N] = X[M,K] W[N,K]^T
+enum GemmEpi {
+  EPI_STORE_F32 = 0,   // Y (float) = acc
+  EPI_ADD_F32 = 1,     // Y (float) += acc
+  EPI_STORE_ACT = 2,   // Y (model dtype) = acc
+  EPI_SWIGLU = 3       // W = [W_gate; W_up] (2N rows); Y (model dtype)[m][n] = silu(gate) * up
+};
+void launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, const void *X, int ldx,
+                 const void *W, void *Y, long ldy, hipStream_t s);
+
+// ---------------------------------------------------------------- row kernels
+void launch_embed(int dtype, int M, int H, int V, const int32_t *tokens, const void *E, float *x,
+                  int32_t *dev_err, hipStream_t s);
+void launch_rmsnorm(int dtype, int M, int H, float eps, const float *x, const void *w, void *out,
+                    hipStream_t s);
+struct RopeArgs {
+  int dtype, M, R, n_heads, n_kv, head_dim;
+  const float *qkv;            // [M][(n_heads + 2 n_kv) head_dim]
+  void *q_out;                 // [M][n_heads][head_dim]
+  void *k_pages, *v_pages;
+  const int32_t *block_table;
+  int page_size, max_pages, num_pages;
+  const int32_t *base_lens;
+  int base_off;
+  const int32_t *blk_len;
+  int blk_len_add;
+  int pos_off;                 // rotary position = slot + pos_off
+  float rope_base, eps;
+  const void *q_norm, *k_norm; // or null
+  int32_t *dev_err;
+};
+void launch_rope_append(const RopeArgs &a, hipStream_t s);
+void launch_mtp_input(int dtype, int M, int H, int V, float eps, const float *h, const int32_t *tok,
+                      int tok_stride, const void *E, const void *norm_h, const void *norm_e, void *out,
+                      int32_t *dev_err, hipStream_t s);
+void launch_gather_rows(int M_out, int R, int C, size_t elem, const void *src, const int32_t *sel, void *dst,
+                        hipStream_t s);
+
+// ---------------------------------------------------------------- orchestration
+struct ForwardPlan {
+  size_t nbuf, act, qkv, q, attn, attn_ws, total;
+  AttnPlan attn_plan;
+};
+ForwardPlan plan_forward(const gm_model_config &cfg, int B, int k, int max_ctx);
+void run_verify_forward(const gm_model_config &cfg, const gm_model_weights &w, const gm_kv_cache &c, int B, int k,
+                        const int32_t *tokens, float *logits, float *hidden, const ForwardPlan &p, char *ws,
+                        int32_t *dev_err, hipStream_t s);
+
+struct MtpPlan {
+  size_t u, x, xg, nbuf, act, qkv, q, attn, attn_g, attn_ws, stat, sel, wsum, psum, total;
+  AttnPlan attn_ext, attn_chain;
+};
+MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx);
+void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const gm_model_weights &shared,
+                   const gm_kv_cache &c, int B, int k, int mode, float inv_t, const float *verify_hidden,
+                   const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft, int32_t *drafts,
+                   float *draft_logits, const MtpPlan &p, char *ws, int32_t *dev_err, hipStream_t s);
+
+}  // namespace gm

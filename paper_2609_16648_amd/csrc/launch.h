@@ -1,0 +1,63 @@
+// Host-side launchers of the gfx950 kernels (internal to libgm).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace gm {
+
+// ---------------------------------------------------------------- tracing
+// RAII bracket of one kernel launch by a pair of HIP events while tracing is on.
+struct TraceScope {
+  TraceScope(const char *name, hipStream_t s);
+  ~TraceScope();
+  int slot;
+  hipStream_t stream;
+};
+
+// ---------------------------------------------------------------- vocabulary pass
+struct RowStat {        // softmax statistics of one chunk of one row of logits
+  float max;            // max of z / T over the chunk
+  int argmax;           // lowest id attaining it
+  double sum;           // sum of exp(z / T - max) over the chunk
+};
+
+struct RowSel {         // one inverse-CDF draw per sequence
+  const float *p_row;   // logits of p (never null)
+  const float *q_row;   // logits of q, or null: draw from p
+  double mp, sp;        // max and normaliser of p
+  double mq, sq;        // max and normaliser of q
+  double u;             // the uniform
+  int32_t *dst;         // where the drawn id goes
+  int active;           // 0: nothing to draw for this sequence
+  int pad;
+};
+
+constexpr int kStatThreads = 256;
+constexpr int kStatVec = 16;                                   // float4 per thread
+constexpr int kStatChunk = kStatThreads * kStatVec * 4;       // 16384 ids per chunk
+constexpr int kScanThreads = 256;
+constexpr int kScanPer = 16;                                   // ids per thread
+constexpr int kScanChunk = kScanThreads * kScanPer;           // 4096 ids per chunk
+
+inline int stat_chunks(int V) { return (V + kStatChunk - 1) / kStatChunk; }
+inline int scan_chunks(int V) { return (V + kScanChunk - 1) / kScanChunk; }
+
+void launch_row_stats(const float *logits, long row_stride, int n_rows, int V, float inv_t,
+                      RowStat *out, hipStream_t s);
+void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const float *tlog,
+                          const float *dlog, const RowStat *tstat, const RowStat *dstat,
+                          const int32_t *drafts, const float *u_accept, const float *u_final,
+                          int32_t *n_accept, int32_t *out_tokens, RowSel *sel, hipStream_t s);
+void launch_draft_select(int B, int V, int mode, float inv_t, const float *dlog, long row_stride,
+                         const RowStat *stat, const float *u, int u_stride, int32_t *dst,
+                         int dst_stride, RowSel *sel, hipStream_t s);
+void launch_residual_draw(int B, int V, float inv_t, const RowSel *sel, double *wsum,
+                          double *psum, hipStream_t s);
+
+// ---------------------------------------------------------------- KV index
+void launch_kv_commit(int B, int k, int page_size, int max_pages, const int32_t *block_table,
+                      int32_t *seq_lens, const int32_t *n_accept, int32_t *slots, hipStream_t s);
+
+}  // namespace gm

@@ -1,0 +1,207 @@
+// Row-wise kernels of the forward and the draft head: embedding gather,
+// RMSNorm, the MTP input (two RMSNorms and the concatenation), RoPE with the
+// KV append into the paged cache, and row gathers.
+//
+// Precision: row statistics in float32; the rotary angle pos * base^(-2i/d)
+// and its sine / cosine in float64 (positions reach 32K, where a float32
+// angle is off by ~2e-3 rad); outputs rounded once to the model dtype.
+#include "common.h"
+#include "forward.h"
+
+namespace gm {
+
+namespace {
+template <typename T>
+__global__ __launch_bounds__(256) void embed_kernel(int H, int V, const int32_t *__restrict__ tok,
+                                                    const T *__restrict__ E, float *__restrict__ x,
+                                                    int32_t *dev_err) {
+  const int r = blockIdx.x;
+  const int t = tok[r];
+  float *xr = x + (long)r * H;
+  if (t < 0 || t >= V) {
+    if (threadIdx.x == 0) raise_dev_err(dev_err, GM_DEVERR_TOKEN);
+    for (int c = threadIdx.x; c < H; c += blockDim.x) xr[c] = 0.f;
+    return;
+  }
+  const T *er = E + (long)t * H;
+  for (int c = threadIdx.x; c < H; c += blockDim.x) xr[c] = Elem<T>::load(er, c);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(int H, float eps, const float *__restrict__ x,
+                                                      const T *__restrict__ w, T *__restrict__ out) {
+  __shared__ float red[16];
+  const int r = blockIdx.x;
+  const float *xr = x + (long)r * H;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < H; c += blockDim.x) ss += xr[c] * xr[c];
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)H + eps);
+  T *o = out + (long)r * H;
+  for (int c = threadIdx.x; c < H; c += blockDim.x) Elem<T>::store(o, c, xr[c] * inv * Elem<T>::load(w, c));
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void mtp_input_kernel(int H, int V, float eps, const float *__restrict__ h,
+                                                        const int32_t *__restrict__ tok, int tok_stride,
+                                                        const T *__restrict__ E, const T *__restrict__ nh,
+                                                        const T *__restrict__ ne, T *__restrict__ out,
+                                                        int32_t *dev_err) {
+  __shared__ float red[16];
+  const int r = blockIdx.x;
+  const int t = tok[(long)r * tok_stride];
+  T *o = out + (long)r * 2 * H;
+  if (t < 0 || t >= V) {     // -1 pads a row with no token
+    if (t >= V && threadIdx.x == 0) raise_dev_err(dev_err, GM_DEVERR_TOKEN);
+    for (int c = threadIdx.x; c < 2 * H; c += blockDim.x) Elem<T>::store(o, c, 0.f);
+    return;
+  }
+  const float *hr = h + (long)r * H;
+  const T *er = E + (long)t * H;
+  float sh = 0.f, se = 0.f;
+  for (int c = threadIdx.x; c < H; c += blockDim.x) {
+    const float a = hr[c], e = Elem<T>::load(er, c);
+    sh += a * a;
+    se += e * e;
+  }
+  sh = block_sum(sh, red);
+  se = block_sum(se, red);
+  const float ih = 1.0f / sqrtf(sh / (float)H + eps), ie = 1.0f / sqrtf(se / (float)H + eps);
+  for (int c = threadIdx.x; c < H; c += blockDim.x) {
+    Elem<T>::store(o, c, hr[c] * ih * Elem<T>::load(nh, c));
+    Elem<T>::store(o, H + c, Elem<T>::load(er, c) * ie * Elem<T>::load(ne, c));
+  }
+}
+
+// one block per row; wave w handles heads w, w+4, ...; lane c < d/2 handles the pair (c, c + d/2)
+template <typename T>
+__global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
+  const int row = blockIdx.x, b = row / a.R, i = row % a.R;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int D = a.head_dim, half = D / 2;
+  const int nh = a.n_heads + 2 * a.n_kv;
+  int blen = a.R;
+  if (a.blk_len) {
+    blen = a.blk_len[b] + a.blk_len_add;
+    blen = blen < 0 ? 0 : (blen > a.R ? a.R : blen);
+  }
+  const int slot = a.base_lens[b] + a.base_off + i;
+  const double pos = (double)(slot + a.pos_off);
+  const bool write_kv = i < blen;
+  long kv_base = -1;
+  int s_in = 0;
+  if (write_kv) {
+    const int pi = slot / a.page_size;
+    const int page = pi < a.max_pages ? a.block_table[(long)b * a.max_pages + pi] : -1;
+    if (page < 0 || page >= a.num_pages) {
+      if (threadIdx.x == 0) raise_dev_err(a.dev_err, GM_DEVERR_PAGE);
+    } else {
+      const int off = slot % a.page_size;
+      kv_base = (((long)page * a.n_kv) * a.page_size + (off & ~15)) * D;   // + head * page_size * D
+      s_in = off & 15;
+    }
+  }
+  const float *src_row = a.qkv + (long)row * nh * D;
+  const T *qn = (const T *)a.q_norm, *kn = (const T *)a.k_norm;
+  for (int hh = w; hh < nh; hh += 4) {
+    const float *src = src_row + hh * D;
+    const int kind = hh < a.n_heads ? 0 : (hh < a.n_heads + a.n_kv ? 1 : 2);
+    const bool act = lane < half;
+    float x1 = act ? src[lane] : 0.f, x2 = act ? src[lane + half] : 0.f;
+    if (kind < 2 && qn) {
+      const T *nw = kind == 0 ? qn : kn;
+      const float ss = wave_sum(x1 * x1 + x2 * x2);
+      const float inv = 1.0f / sqrtf(ss / (float)D + a.eps);
+      if (act) {
+        x1 = x1 * inv * Elem<T>::load(nw, lane);
+        x2 = x2 * inv * Elem<T>::load(nw, lane + half);
+      }
+    }
+    if (!act) continue;
+    float y1 = x1, y2 = x2;
+    if (kind < 2) {
+      const double ang = pos * pow((double)a.rope_base, -2.0 * lane / D);
+      double sn, cs;
+      sincos(ang, &sn, &cs);
+      y1 = (float)((double)x1 * cs - (double)x2 * sn);
+      y2 = (float)((double)x2 * cs + (double)x1 * sn);
+    }
+    if (kind == 0) {
+      T *q = (T *)a.q_out + ((long)row * a.n_heads + hh) * D;
+      Elem<T>::store(q, lane, y1);
+      Elem<T>::store(q, lane + half, y2);
+    } else if (kv_base >= 0) {
+      const int head = kind == 1 ? hh - a.n_heads : hh - a.n_heads - a.n_kv;
+      const long base = kv_base + (long)head * a.page_size * D;
+      if (kind == 1) {
+        T *kp = (T *)a.k_pages + base;
+        Elem<T>::store(kp, k_tile_off(s_in, lane), y1);
+        Elem<T>::store(kp, k_tile_off(s_in, lane + half), y2);
+      } else {
+        T *vp = (T *)a.v_pages + base;
+        Elem<T>::store(vp, v_tile_off(s_in, lane), y1);
+        Elem<T>::store(vp, v_tile_off(s_in, lane + half), y2);
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void gather_rows_kernel(int R, int C16, const uint4 *__restrict__ src,
+                                                          const int32_t *__restrict__ sel, uint4 *__restrict__ dst) {
+  const int b = blockIdx.x;
+  int i = sel[b];
+  i = i < 0 ? 0 : (i >= R ? R - 1 : i);
+  const uint4 *s = src + ((long)b * R + i) * C16;
+  uint4 *d = dst + (long)b * C16;
+  for (int c = threadIdx.x; c < C16; c += blockDim.x) d[c] = s[c];
+}
+}  // namespace
+
+void launch_embed(int dtype, int M, int H, int V, const int32_t *tokens, const void *E, float *x, int32_t *dev_err,
+                  hipStream_t s) {
+  if (M <= 0) return;
+  TraceScope ts("embed", s);
+  if (dtype == GM_BF16)
+    hipLaunchKernelGGL(embed_kernel<bf16>, dim3(M), dim3(256), 0, s, H, V, tokens, (const bf16 *)E, x, dev_err);
+  else
+    hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, H, V, tokens, (const float *)E, x, dev_err);
+}
+
+void launch_rmsnorm(int dtype, int M, int H, float eps, const float *x, const void *w, void *out, hipStream_t s) {
+  if (M <= 0) return;
+  TraceScope ts("rmsnorm", s);
+  if (dtype == GM_BF16)
+    hipLaunchKernelGGL(rmsnorm_kernel<bf16>, dim3(M), dim3(256), 0, s, H, eps, x, (const bf16 *)w, (bf16 *)out);
+  else
+    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(M), dim3(256), 0, s, H, eps, x, (const float *)w, (float *)out);
+}
+
+void launch_rope_append(const RopeArgs &a, hipStream_t s) {
+  if (a.M <= 0) return;
+  TraceScope ts("rope_append", s);
+  if (a.dtype == GM_BF16) hipLaunchKernelGGL(rope_append_kernel<bf16>, dim3(a.M), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(rope_append_kernel<float>, dim3(a.M), dim3(256), 0, s, a);
+}
+
+void launch_mtp_input(int dtype, int M, int H, int V, float eps, const float *h, const int32_t *tok, int tok_stride,
+                      const void *E, const void *norm_h, const void *norm_e, void *out, int32_t *dev_err,
+                      hipStream_t s) {
+  if (M <= 0) return;
+  TraceScope ts("mtp_input", s);
+  if (dtype == GM_BF16)
+    hipLaunchKernelGGL(mtp_input_kernel<bf16>, dim3(M), dim3(256), 0, s, H, V, eps, h, tok, tok_stride,
+                       (const bf16 *)E, (const bf16 *)norm_h, (const bf16 *)norm_e, (bf16 *)out, dev_err);
+  else
+    hipLaunchKernelGGL(mtp_input_kernel<float>, dim3(M), dim3(256), 0, s, H, V, eps, h, tok, tok_stride,
+                       (const float *)E, (const float *)norm_h, (const float *)norm_e, (float *)out, dev_err);
+}
+
+void launch_gather_rows(int M_out, int R, int C, size_t elem, const void *src, const int32_t *sel, void *dst,
+                        hipStream_t s) {
+  if (M_out <= 0) return;
+  TraceScope ts("gather_rows", s);
+  const int C16 = (int)((size_t)C * elem / 16);
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(M_out), dim3(256), 0, s, R, C16, (const uint4 *)src, sel, (uint4 *)dst);
+}
+
+}  // namespace gm

@@ -1,0 +1,381 @@
+// Vocabulary-pass kernels: softmax statistics, the accept rule (Sec. 2.2,
+// Eq. accept-rule), the residual / bonus draw and the draft-head draw.
+//
+// Logits rows are read in place; no probability matrix is written.
+//  1. row_stats: per (row, chunk of 16384 ids) the max of z/T, the lowest id
+//     attaining it and sum exp(z/T - max) accumulated in float64.
+//  2. accept_decide (one thread per sequence): combines the chunk statistics,
+//     evaluates p_i(d_i) / q_i(d_i) in float64 from the two gathered logits,
+//     rounds the ratio to float32, compares it with u and stops at the first
+//     rejection; greedy mode compares d_i with the row argmax instead.  It
+//     prepares one draw per sequence (residual max(0, p - q) at the first
+//     rejection, p_{k+1} after a full accept).
+//  3. residual_chunk + residual_scan: an inverse-CDF draw in ascending id
+//     order evaluated in float64 (p, q and the running sum), first as chunk
+//     masses, then a scan inside the chunk that holds u * Z.
+#include <float.h>
+
+#include "common.h"
+#include "launch.h"
+
+namespace gm {
+
+// ------------------------------------------------------------------ 1. row statistics
+__global__ __launch_bounds__(kStatThreads) void row_stats_kernel(const float *__restrict__ logits,
+                                                                 long row_stride, int V, float inv_t,
+                                                                 int n_chunks, RowStat *__restrict__ out) {
+  __shared__ float sm_max[kStatThreads / kWave];
+  __shared__ int sm_arg[kStatThreads / kWave];
+  __shared__ double sm_sum[kStatThreads / kWave];
+  const int r = blockIdx.x, c = blockIdx.y, tid = threadIdx.x;
+  const float *row = logits + (long)r * row_stride;
+  const int lo = c * kStatChunk;
+  const int hi = min(V, lo + kStatChunk);
+  const bool vec = ((V & 3) == 0) && ((row_stride & 3) == 0);
+
+  float v[kStatVec][4];
+#pragma unroll
+  for (int j = 0; j < kStatVec; ++j) {
+    const int e = lo + 4 * (tid + kStatThreads * j);
+    if (vec && e + 3 < hi) {
+      const float4 f = *reinterpret_cast<const float4 *>(row + e);
+      v[j][0] = f.x * inv_t; v[j][1] = f.y * inv_t; v[j][2] = f.z * inv_t; v[j][3] = f.w * inv_t;
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[j][q] = (e + q < hi) ? row[e + q] * inv_t : -INFINITY;
+    }
+  }
+  // max and lowest arg-max: ids are visited in ascending order within a thread
+  float m = -INFINITY;
+  int am = 0x7fffffff;
+#pragma unroll
+  for (int j = 0; j < kStatVec; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (v[j][q] > m) { m = v[j][q]; am = lo + 4 * (tid + kStatThreads * j) + q; }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float om = __shfl_xor(m, o, kWave);
+    const int oa = __shfl_xor(am, o, kWave);
+    if (om > m || (om == m && oa < am)) { m = om; am = oa; }
+  }
+  const int lane = tid & 63, wid = tid >> 6;
+  if (lane == 0) { sm_max[wid] = m; sm_arg[wid] = am; }
+  __syncthreads();
+  m = sm_max[0];
+  am = sm_arg[0];
+#pragma unroll
+  for (int w = 1; w < kStatThreads / kWave; ++w)
+    if (sm_max[w] > m || (sm_max[w] == m && sm_arg[w] < am)) { m = sm_max[w]; am = sm_arg[w]; }
+
+  double s = 0.0;
+#pragma unroll
+  for (int j = 0; j < kStatVec; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) s += (double)expf(v[j][q] - m);
+  s = wave_sum(s);
+  if (lane == 0) sm_sum[wid] = s;
+  __syncthreads();
+  if (tid == 0) {
+    double t = 0.0;
+    for (int w = 0; w < kStatThreads / kWave; ++w) t += sm_sum[w];
+    RowStat o;
+    o.max = m;
+    o.argmax = am;
+    o.sum = t;
+    out[(long)r * n_chunks + c] = o;
+  }
+}
+
+void launch_row_stats(const float *logits, long row_stride, int n_rows, int V, float inv_t,
+                      RowStat *out, hipStream_t s) {
+  if (n_rows <= 0) return;
+  TraceScope ts("row_stats", s);
+  dim3 grid(n_rows, stat_chunks(V));
+  hipLaunchKernelGGL(row_stats_kernel, grid, dim3(kStatThreads), 0, s, logits, row_stride, V, inv_t,
+                     stat_chunks(V), out);
+}
+
+// max, normaliser and lowest arg-max of a whole row from its chunk statistics
+__device__ __forceinline__ void combine_stats(const RowStat *st, int nch, double &M, double &S, int &am) {
+  float m = -INFINITY;
+  int a = 0;
+  for (int c = 0; c < nch; ++c)
+    if (st[c].max > m) { m = st[c].max; a = st[c].argmax; }
+  double s = 0.0;
+  for (int c = 0; c < nch; ++c) s += st[c].sum * exp((double)st[c].max - (double)m);
+  M = (double)m;
+  S = s;
+  am = a;
+}
+
+// ------------------------------------------------------------------ 2. accept decision
+__global__ void accept_decide_kernel(int B, int k, int V, int mode, float inv_t,
+                                     const float *__restrict__ tlog, const float *__restrict__ dlog,
+                                     const RowStat *__restrict__ tstat, const RowStat *__restrict__ dstat,
+                                     int nch, const int32_t *__restrict__ drafts,
+                                     const float *__restrict__ u_acc, const float *__restrict__ u_fin,
+                                     int32_t *__restrict__ n_out, int32_t *__restrict__ out_tokens,
+                                     RowSel *__restrict__ sel) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int k1 = k + 1;
+  int n = 0;
+  RowSel rs;
+  rs.active = 0;
+  rs.q_row = nullptr;
+  rs.mq = 0.0;
+  rs.sq = 1.0;
+  rs.pad = 0;
+  if (mode == GM_GREEDY) {
+    double M, S;
+    int am = 0;
+    for (; n < k; ++n) {
+      combine_stats(tstat + (long)(b * k1 + n) * nch, nch, M, S, am);
+      if (drafts[b * k + n] != am) break;
+    }
+    if (n == k) combine_stats(tstat + (long)(b * k1 + k) * nch, nch, M, S, am);
+    out_tokens[b * k1 + n] = am;
+  } else {
+    for (; n < k; ++n) {
+      const int d = drafts[b * k + n];
+      if (d < 0 || d >= V) break;
+      double Mt, St, Mq, Sq;
+      int am;
+      combine_stats(tstat + (long)(b * k1 + n) * nch, nch, Mt, St, am);
+      combine_stats(dstat + (long)(b * k + n) * nch, nch, Mq, Sq, am);
+      const double zt = (double)(tlog[(long)(b * k1 + n) * V + d] * inv_t);
+      const double zq = (double)(dlog[(long)(b * k + n) * V + d] * inv_t);
+      const double p = exp(zt - Mt) / St;
+      const double q = exp(zq - Mq) / Sq;
+      const float ratio = q > 0.0 ? (float)(p / q) : INFINITY;
+      if (!(u_acc[b * k + n] < ratio)) break;
+    }
+    int am;
+    rs.p_row = tlog + (long)(b * k1 + n) * V;
+    combine_stats(tstat + (long)(b * k1 + n) * nch, nch, rs.mp, rs.sp, am);
+    if (n < k) {
+      rs.q_row = dlog + (long)(b * k + n) * V;
+      combine_stats(dstat + (long)(b * k + n) * nch, nch, rs.mq, rs.sq, am);
+    }
+    rs.u = (double)u_fin[b];
+    rs.dst = out_tokens + b * k1 + n;
+    rs.active = 1;
+  }
+  for (int i = 0; i < n; ++i) out_tokens[b * k1 + i] = drafts[b * k + i];
+  for (int i = n + 1; i < k1; ++i) out_tokens[b * k1 + i] = -1;
+  n_out[b] = n;
+  sel[b] = rs;
+}
+
+void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const float *tlog,
+                          const float *dlog, const RowStat *tstat, const RowStat *dstat,
+                          const int32_t *drafts, const float *u_accept, const float *u_final,
+                          int32_t *n_accept, int32_t *out_tokens, RowSel *sel, hipStream_t s) {
+  TraceScope ts("accept_decide", s);
+  hipLaunchKernelGGL(accept_decide_kernel, dim3((B + 63) / 64), dim3(64), 0, s, B, k, V, mode, inv_t,
+                     tlog, dlog, tstat, dstat, stat_chunks(V), drafts, u_accept, u_final, n_accept,
+                     out_tokens, sel);
+}
+
+// one draw per sequence from softmax(z / T) of a draft-logits row (greedy: its argmax)
+__global__ void draft_select_kernel(int B, int V, int mode, const float *__restrict__ dlog,
+                                    long row_stride, const RowStat *__restrict__ stat, int nch,
+                                    const float *__restrict__ u, int u_stride, int32_t *__restrict__ dst,
+                                    int dst_stride, RowSel *__restrict__ sel) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  RowSel rs;
+  int am;
+  combine_stats(stat + (long)b * nch, nch, rs.mp, rs.sp, am);
+  rs.p_row = dlog + (long)b * row_stride;
+  rs.q_row = nullptr;
+  rs.mq = 0.0;
+  rs.sq = 1.0;
+  rs.pad = 0;
+  rs.dst = dst + (long)b * dst_stride;
+  if (mode == GM_GREEDY) {
+    *rs.dst = am;
+    rs.active = 0;
+    rs.u = 0.0;
+  } else {
+    rs.u = (double)u[(long)b * u_stride];
+    rs.active = 1;
+  }
+  sel[b] = rs;
+}
+
+void launch_draft_select(int B, int V, int mode, float inv_t, const float *dlog, long row_stride,
+                         const RowStat *stat, const float *u, int u_stride, int32_t *dst,
+                         int dst_stride, RowSel *sel, hipStream_t s) {
+  (void)inv_t;
+  TraceScope ts("draft_select", s);
+  hipLaunchKernelGGL(draft_select_kernel, dim3((B + 63) / 64), dim3(64), 0, s, B, V, mode, dlog,
+                     row_stride, stat, stat_chunks(V), u, u_stride, dst, dst_stride, sel);
+}
+
+// ------------------------------------------------------------------ 3. inverse-CDF draw
+// weight of id x: max(0, p(x) - q(x)) with q, p(x) without; every quantity in float64
+__device__ __forceinline__ double draw_weight(const RowSel &s, int x, float inv_t, bool use_p) {
+  const double p = exp((double)(s.p_row[x] * inv_t) - s.mp) / s.sp;
+  if (use_p || s.q_row == nullptr) return p;
+  const double q = exp((double)(s.q_row[x] * inv_t) - s.mq) / s.sq;
+  return fmax(p - q, 0.0);
+}
+
+// per-thread sums over kScanPer consecutive ids, then a serial sum over the
+// threads in ascending order (thread 0), so both kernels associate identically
+__global__ __launch_bounds__(kScanThreads) void residual_chunk_kernel(int V, float inv_t,
+                                                                      const RowSel *__restrict__ sel,
+                                                                      int nch, double *__restrict__ wsum,
+                                                                      double *__restrict__ psum) {
+  __shared__ double sw[kScanThreads], sp[kScanThreads];
+  const int b = blockIdx.x, c = blockIdx.y, tid = threadIdx.x;
+  const RowSel s = sel[b];
+  if (!s.active) return;
+  const int x0 = c * kScanChunk + tid * kScanPer;
+  double w = 0.0, p = 0.0;
+  for (int j = 0; j < kScanPer; ++j) {
+    const int x = x0 + j;
+    if (x < V) {
+      const double px = exp((double)(s.p_row[x] * inv_t) - s.mp) / s.sp;
+      const double qx = s.q_row ? exp((double)(s.q_row[x] * inv_t) - s.mq) / s.sq : 0.0;
+      w += s.q_row ? fmax(px - qx, 0.0) : px;
+      p += px;
+    }
+  }
+  sw[tid] = w;
+  sp[tid] = p;
+  __syncthreads();
+  if (tid == 0) {
+    double tw = 0.0, tp = 0.0;
+    for (int i = 0; i < kScanThreads; ++i) { tw += sw[i]; tp += sp[i]; }
+    wsum[(long)b * nch + c] = tw;
+    psum[(long)b * nch + c] = tp;
+  }
+}
+
+__global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, float inv_t,
+                                                                     const RowSel *__restrict__ sel, int nch,
+                                                                     const double *__restrict__ wsum,
+                                                                     const double *__restrict__ psum) {
+  __shared__ double st[kScanThreads];
+  __shared__ double sh_t, sh_base;
+  __shared__ int sh_chunk, sh_thread, sh_use_p, sh_found;
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const RowSel s = sel[b];
+  if (!s.active) return;
+  if (tid == 0) {
+    const double *W = wsum + (long)b * nch;
+    double Z = 0.0;
+    for (int c = 0; c < nch; ++c) Z += W[c];
+    int use_p = 0;
+    if (!(Z > 0.0)) {          // no residual mass: draw from p
+      use_p = 1;
+      W = psum + (long)b * nch;
+      Z = 0.0;
+      for (int c = 0; c < nch; ++c) Z += W[c];
+    }
+    const double t = s.u * Z;
+    double run = 0.0;
+    int cs = -1;
+    for (int c = 0; c < nch; ++c) {
+      if (run + W[c] > t) { cs = c; break; }
+      run += W[c];
+    }
+    if (cs < 0) {              // rounding put u * Z past the end: last chunk with mass
+      run = 0.0;
+      for (int c = 0; c < nch; ++c)
+        if (W[c] > 0.0) cs = c;
+      if (cs < 0) cs = 0;
+      for (int c = 0; c < cs; ++c) run += W[c];
+    }
+    sh_t = t;
+    sh_base = run;
+    sh_chunk = cs;
+    sh_use_p = use_p;
+  }
+  __syncthreads();
+  const int cs = sh_chunk;
+  const bool use_p = sh_use_p != 0;
+  const int x0 = cs * kScanChunk + tid * kScanPer;
+  double w = 0.0;
+  for (int j = 0; j < kScanPer; ++j)
+    if (x0 + j < V) w += draw_weight(s, x0 + j, inv_t, use_p);
+  st[tid] = w;
+  __syncthreads();
+  if (tid == 0) {
+    double acc = sh_base;
+    int th = -1, last_nz = -1;
+    for (int i = 0; i < kScanThreads; ++i) {
+      if (st[i] > 0.0) last_nz = i;
+      if (th < 0 && acc + st[i] > sh_t) th = i;
+      if (th < 0) acc += st[i];
+    }
+    sh_found = th >= 0;
+    if (th < 0) th = last_nz < 0 ? 0 : last_nz;
+    sh_thread = th;
+    sh_base = acc;
+  }
+  __syncthreads();
+  if (tid == sh_thread) {
+    double acc = sh_base;
+    int x_last = -1, x_hit = -1;
+    for (int j = 0; j < kScanPer; ++j) {
+      const int x = x0 + j;
+      if (x >= V) break;
+      const double wx = draw_weight(s, x, inv_t, use_p);
+      if (wx > 0.0) x_last = x;
+      acc += wx;
+      if (sh_found && x_hit < 0 && acc > sh_t) x_hit = x;
+    }
+    *s.dst = x_hit >= 0 ? x_hit : (x_last >= 0 ? x_last : (x0 < V ? x0 : V - 1));
+  }
+}
+
+void launch_residual_draw(int B, int V, float inv_t, const RowSel *sel, double *wsum, double *psum,
+                          hipStream_t s) {
+  const int nch = scan_chunks(V);
+  {
+    TraceScope ts("residual_chunk", s);
+    hipLaunchKernelGGL(residual_chunk_kernel, dim3(B, nch), dim3(kScanThreads), 0, s, V, inv_t, sel, nch,
+                       wsum, psum);
+  }
+  {
+    TraceScope ts("residual_scan", s);
+    hipLaunchKernelGGL(residual_scan_kernel, dim3(B), dim3(kScanThreads), 0, s, V, inv_t, sel, nch, wsum,
+                       psum);
+  }
+}
+
+// ------------------------------------------------------------------ KV commit / rollback
+__global__ void kv_commit_kernel(int B, int k, int page_size, int max_pages,
+                                 const int32_t *__restrict__ block_table, int32_t *__restrict__ seq_lens,
+                                 const int32_t *__restrict__ n_accept, int32_t *__restrict__ slots) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int m = seq_lens[b];
+  int n = n_accept[b];
+  n = n < 0 ? 0 : (n > k ? k : n);
+  if (slots) {
+    for (int i = 0; i <= k; ++i) {
+      int v = -1;
+      if (i <= n) {
+        const int t = m + i;
+        const int pi = t / page_size;
+        v = pi < max_pages ? block_table[(long)b * max_pages + pi] * page_size + t % page_size : -1;
+      }
+      slots[b * (k + 1) + i] = v;
+    }
+  }
+  seq_lens[b] = m + n + 1;
+}
+
+void launch_kv_commit(int B, int k, int page_size, int max_pages, const int32_t *block_table,
+                      int32_t *seq_lens, const int32_t *n_accept, int32_t *slots, hipStream_t s) {
+  TraceScope ts("kv_commit", s);
+  hipLaunchKernelGGL(kv_commit_kernel, dim3((B + 63) / 64), dim3(64), 0, s, B, k, page_size, max_pages,
+                     block_table, seq_lens, n_accept, slots);
+}
+
+}  // namespace gm

@@ -1,0 +1,164 @@
+"""The C ABI without a GPU: the library loads, exports every entry point that
+include/gm.h declares, sizes its workspaces, and rejects bad arguments on the
+host before launching anything."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2609_16648_amd import gm, layout
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = ctypes.c_void_p(1 << 20)          # never dereferenced: every call below fails validation first
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "gm.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(gm_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    L = gm.lib()
+    names = _declared()
+    assert "gm_verify_forward" in names and "gm_spec_accept" in names
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(gm.EXPORTS) == names
+
+
+def _cfg(shape=synth.QWEN3_4B_LAYER):
+    return gm.model_config(shape)
+
+
+def test_workspace_sizes():
+    cfg = _cfg()
+    for op in (gm.GM_OP_VERIFY_FORWARD, gm.GM_OP_VERIFY_ATTENTION, gm.GM_OP_SPEC_ACCEPT, gm.GM_OP_MTP_DRAFT):
+        assert gm.workspace_size(op, cfg, 64, 3, 4096) > 0
+    assert gm.workspace_size(99, cfg, 64, 3, 4096) == 0
+    assert gm.workspace_size(gm.GM_OP_VERIFY_FORWARD, cfg, 64, 16, 4096) == 0      # k beyond the limit
+    bad = _cfg(synth.ModelShape(1, 256, 4, 4, 64, 1024, 1024, dtype="bf16"))       # bf16 needs head_dim 128
+    assert gm.workspace_size(gm.GM_OP_VERIFY_FORWARD, bad, 4, 3, 128) == 0
+    # the attention partials grow with the context bound
+    a = gm.workspace_size(gm.GM_OP_VERIFY_ATTENTION, cfg, 32, 7, 32768)
+    b = gm.workspace_size(gm.GM_OP_VERIFY_ATTENTION, cfg, 32, 7, 1024)
+    assert a > b
+
+
+def test_spec_accept_rejects_bad_arguments():
+    L = gm.lib()
+    ws = ctypes.c_void_p(1 << 20)
+    args = lambda **kw: dict(dict(B=4, k=3, V=100, mode=gm.GM_SAMPLE, T=1.0, tl=FAKE, dl=FAKE, dt=FAKE, ua=FAKE,
+                                  uf=FAKE, n=FAKE, out=FAKE, ws=ws, nbytes=1 << 30), **kw)
+
+    def call(a):
+        return L.gm_spec_accept(a["B"], a["k"], a["V"], a["mode"], a["T"], a["tl"], a["dl"], a["dt"], a["ua"],
+                                a["uf"], a["n"], a["out"], a["ws"], a["nbytes"], None)
+
+    assert call(args(k=16)) == gm.GM_ERR_INVALID_ARG
+    assert call(args(mode=7)) == gm.GM_ERR_INVALID_ARG
+    assert call(args(T=0.0)) == gm.GM_ERR_INVALID_ARG
+    assert call(args(dl=None)) == gm.GM_ERR_INVALID_ARG
+    assert "draft_logits" in gm.last_error()
+    assert call(args(uf=None)) == gm.GM_ERR_INVALID_ARG
+    assert call(args(tl=None)) == gm.GM_ERR_INVALID_ARG
+    assert call(args(nbytes=16)) == gm.GM_ERR_WORKSPACE
+    assert call(args(ws=ctypes.c_void_p((1 << 20) + 8))) == gm.GM_ERR_WORKSPACE      # misaligned
+    assert call(args(B=0)) == gm.GM_OK                                               # nothing to do
+
+
+class _FakeCache:
+    def __init__(self, n_layers, max_ctx, page_size=16, max_pages=10):
+        self.kp = (ctypes.c_void_p * n_layers)(*([1 << 20] * n_layers))
+        self.desc = gm.KVCacheDesc(self.kp, self.kp, n_layers, page_size, 100, max_pages, FAKE, FAKE, max_ctx)
+
+
+def _weights(n_layers):
+    lw = gm.LayerWeights(*([FAKE] * 8))
+    arr = (gm.LayerWeights * n_layers)(*([lw] * n_layers))
+    return arr, gm.ModelWeights(FAKE, FAKE, FAKE, ctypes.cast(arr, ctypes.POINTER(gm.LayerWeights)))
+
+
+def test_verify_forward_rejects_bad_arguments():
+    L = gm.lib()
+    shape = synth.ModelShape(2, 256, 4, 4, 64, 1024, 1024, dtype="f32")
+    cfg = gm.model_config(shape)
+    keep, w = _weights(2)
+
+    def call(cfg_=cfg, cache=None, B=4, k=3, nbytes=1 << 30):
+        cache = cache or _FakeCache(2, 100)
+        return L.gm_verify_forward(ctypes.byref(cfg_), ctypes.byref(w), ctypes.byref(cache.desc), B, k, FAKE, FAKE,
+                                   FAKE, FAKE, nbytes, None, None)
+
+    assert call(cache=_FakeCache(2, 157)) == gm.GM_ERR_CAPACITY      # 157 + 4 > 10 pages of 16
+    assert "exceed" in gm.last_error()
+    assert call(cache=_FakeCache(1, 100)) == gm.GM_ERR_INVALID_ARG   # cache layers != model layers
+    assert call(cache=_FakeCache(2, 100, page_size=24)) == gm.GM_ERR_UNSUPPORTED
+    assert call(k=-1) == gm.GM_ERR_UNSUPPORTED
+    assert call(nbytes=100) == gm.GM_ERR_WORKSPACE
+    bad = gm.model_config(synth.ModelShape(2, 256, 4, 3, 64, 1024, 1024, dtype="f32"))   # 4 % 3 != 0
+    assert call(cfg_=bad) == gm.GM_ERR_INVALID_ARG
+    big_group = gm.model_config(synth.ModelShape(2, 256, 32, 2, 64, 1024, 1024, dtype="f32"))  # 16 * 4 rows ok
+    assert call(cfg_=big_group, k=4) == gm.GM_ERR_UNSUPPORTED                               # 16 * 5 > 64
+    assert call(B=0) == gm.GM_OK
+
+
+def test_mtp_and_attention_reject_bad_arguments():
+    L = gm.lib()
+    shape = synth.ModelShape(1, 256, 4, 4, 64, 1024, 1024, dtype="f32")
+    cfg = gm.model_config(shape)
+    keep, w = _weights(1)
+    mtp = gm.MtpWeights(FAKE, FAKE, FAKE, FAKE, gm.LayerWeights(*([FAKE] * 8)))
+    c = _FakeCache(1, 100)
+    st = L.gm_mtp_draft(ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(c.desc), 4, 3,
+                        gm.GM_SAMPLE, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, 1 << 30, None, None)
+    assert st == gm.GM_ERR_INVALID_ARG and "u_draft" in gm.last_error()
+    c2 = _FakeCache(1, 150)                                         # 150 + 2k + 1 > 160
+    st = L.gm_mtp_draft(ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(c2.desc), 4, 5,
+                        gm.GM_GREEDY, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, 1 << 30, None, None)
+    assert st == gm.GM_ERR_CAPACITY
+    st = L.gm_verify_attention(ctypes.byref(cfg), ctypes.byref(c.desc), 1, 4, 3, FAKE, FAKE, FAKE, 1 << 30, None, None)
+    assert st == gm.GM_ERR_INVALID_ARG                              # layer out of range
+    st = L.gm_kv_commit(ctypes.byref(c.desc), 4, 3, None, None, None)
+    assert st == gm.GM_ERR_INVALID_ARG
+
+
+# ------------------------------------------------------------------ layout
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_tile_layout_is_a_bijection(head_dim):
+    k, v = layout.tile_offsets(head_dim)
+    for t in (k, v):
+        assert sorted(t.ravel().tolist()) == list(range(16 * head_dim))
+
+
+def test_tile_layout_matches_operand_order():
+    # one 16-byte load per lane (8 bf16) at instruction i reads elements i*512 + 8*lane .. +7
+    k, v = layout.tile_offsets(128)
+    inv_k = {int(o): (s, c) for (s, c), o in np.ndenumerate(k)}
+    inv_v = {int(o): (s, c) for (s, c), o in np.ndenumerate(v)}
+    for i in range(4):
+        for lane in range(64):
+            got = [inv_k[i * 512 + 8 * lane + e] for e in range(8)]
+            # K: token lane % 16, eight consecutive channels of one 32-channel slice
+            assert all(s == lane % 16 for s, _ in got)
+            assert [c for _, c in got] == [32 * i + 8 * (lane // 16) + e for e in range(8)]
+            got = [inv_v[i * 512 + 8 * lane + e] for e in range(8)]
+            # V: channels 32i + lane % 16 (first four) and 32i + 16 + lane % 16 (last four),
+            #    tokens 4 (lane // 16) .. +3 in each half
+            assert [c for _, c in got] == [32 * i + lane % 16] * 4 + [32 * i + 16 + lane % 16] * 4
+            assert [s for s, _ in got] == [4 * (lane // 16) + e for e in range(4)] * 2
+
+
+def test_scatter_gather_round_trip():
+    g = np.random.default_rng(0)
+    page_size, n_kv, d = 32, 2, 64
+    table, num_pages = layout.block_table([3, 5], 5, seed=1)
+    pool = np.zeros((num_pages, n_kv, page_size * d), np.float32)
+    ent = g.standard_normal((150, n_kv, d)).astype(np.float32)
+    pos = np.arange(150)
+    layout.scatter(pool, ent, pos, table[1], page_size, "v")
+    np.testing.assert_array_equal(layout.gather(pool, pos, table[1], page_size, n_kv, d, "v"), ent)
+    assert (table[0, 3:] == -1).all() and sorted(table[table >= 0].tolist()) == list(range(8))

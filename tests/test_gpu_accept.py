@@ -1,0 +1,148 @@
+"""GPU parity of gm_spec_accept and gm_kv_commit against the oracle on the same
+seeded logits.  Accept counts and committed slots must match bit for bit
+outside the flag windows (|u - min(1, p/q)| < 1e-3, top-2 margin < 1e-2, and
+a final draw within 1e-9 Z of a CDF edge); the flagged count is printed."""
+import numpy as np
+import pytest
+import scipy.stats
+import torch
+
+import oracle
+import synth
+from helpers import need_gpu, t32, i32, flag_report
+from paper_2609_16648_amd import gm
+
+pytestmark = pytest.mark.gpu
+FINAL_EPS = 1e-9
+
+
+def _sampled_drafts(zq, u_draft):
+    """d_i ~ q_i by the inverse CDF (drafts drawn from the head, as in rollout)."""
+    B, k, V = zq.shape
+    d = np.zeros((B, k), np.int64)
+    for i in range(k):
+        d[:, i] = oracle.inverse_cdf_rows(oracle.softmax(zq[:, i].astype(np.float64)), u_draft[:, i])[0]
+    return d
+
+
+def _run(zt, zq, drafts, ua, uf, mode):
+    B, k1, V = zt.shape
+    k = k1 - 1
+    n = torch.zeros(B, dtype=torch.int32, device="cuda")
+    out = torch.zeros((B, k1), dtype=torch.int32, device="cuda")
+    ws = gm.Workspace()
+    gm.spec_accept(t32(zt), t32(zq) if zq is not None else None, i32(drafts),
+                   t32(ua) if ua is not None else None, t32(uf) if uf is not None else None, n, out, mode, ws)
+    torch.cuda.synchronize()
+    return n.cpu().numpy(), out.cpu().numpy()
+
+
+def _compare(name, ref, n, out):
+    ok = ~ref.flagged
+    flag_report(name, ref.flagged, len(n))
+    np.testing.assert_array_equal(n[ok], ref.n_accept[ok])
+    np.testing.assert_array_equal(out[ok], ref.out_tokens[ok])
+    # flagged sequences still have valid structure
+    for b in np.flatnonzero(ref.flagged):
+        assert 0 <= n[b] <= out.shape[1] - 1 and (out[b, n[b] + 1:] == -1).all()
+
+
+@pytest.mark.parametrize("B,k,V", [(64, 3, 151936), (32, 7, 151936), (4, 3, 1024), (257, 2, 1000), (3, 0, 5000)])
+def test_sample_accept_matches_oracle(B, k, V):
+    need_gpu()
+    zt = synth.normal_logits((B, k + 1, V), 3, "t", B, k, V)
+    zq = synth.normal_logits((B, k, V), 3, "q", B, k, V)
+    ua, uf, ud = synth.uniforms(B, k, 4, B, k, V)
+    drafts = _sampled_drafts(zq, ud)
+    ref = oracle.spec_accept(zt, zq, drafts, ua, uf, final_eps=FINAL_EPS)
+    n, out = _run(zt, zq, drafts, ua, uf, gm.GM_SAMPLE)
+    _compare("sample B=%d k=%d V=%d" % (B, k, V), ref, n, out)
+    assert ref.flagged.mean() < 0.05
+
+
+@pytest.mark.parametrize("B,k,V", [(64, 3, 151936), (16, 5, 1024)])
+def test_greedy_accept_matches_oracle(B, k, V):
+    need_gpu()
+    zt = synth.normal_logits((B, k + 1, V), 3, "g", B, k, V)
+    top = np.argmax(zt, -1)
+    take, alt = synth.mixing_draws(B, k, V, 0.7, 3, "g", B)
+    drafts = np.where(take, top[:, :k], alt)
+    ref = oracle.spec_accept(zt, None, drafts, None, None, mode="greedy")
+    n, out = _run(zt, None, drafts, None, None, gm.GM_GREEDY)
+    _compare("greedy B=%d k=%d V=%d" % (B, k, V), ref, n, out)
+    assert n.max() == k and n.min() == 0
+
+
+def test_ties_and_edge_ids():
+    need_gpu()
+    B, k, V = 6, 2, 4096
+    zt = np.zeros((B, k + 1, V), np.float32)
+    zt[:, :, 17] = 5.0
+    zt[:, :, 4000] = 5.0          # exact tie: the lowest id wins
+    zt[0, :, 0] = 9.0             # first id
+    zt[1, :, V - 1] = 9.0         # last id
+    drafts = np.full((B, k), 17)
+    drafts[0] = 0
+    drafts[1] = V - 1
+    n, out = _run(zt, None, drafts, None, None, gm.GM_GREEDY)
+    assert list(n) == [k] * B
+    assert out[0, k] == 0 and out[1, k] == V - 1 and (out[2:, k] == 17).all()
+
+
+def test_q_equal_p_accepts_all():
+    need_gpu()
+    B, k, V = 128, 4, 2048
+    zt = synth.normal_logits((B, k + 1, V), 3, "qp")
+    ua, uf, ud = synth.uniforms(B, k, 4, "qp")
+    drafts = _sampled_drafts(zt[:, :k], ud)
+    n, out = _run(zt, zt[:, :k].copy(), drafts, ua, uf, gm.GM_SAMPLE)
+    assert (n == k).all()
+    np.testing.assert_array_equal(out[:, :k], drafts)
+
+
+def test_gpu_chi_square_v4():
+    # on a 4-token vocabulary the first committed token is distributed as p (10^6 trials)
+    need_gpu()
+    trials, V = 1_000_000, 4
+    p = np.array([0.1, 0.2, 0.3, 0.4])
+    q = np.array([0.4, 0.3, 0.2, 0.1])
+    g = synth.stream(4, "gpu-chi")
+    d = oracle.inverse_cdf_rows(np.tile(q, (trials, 1)), g.random(trials))[0]
+    zt = np.tile(np.log(np.stack([p, p])).astype(np.float32), (trials, 1, 1))
+    zq = np.tile(np.log(q).astype(np.float32)[None], (trials, 1, 1))
+    n, out = _run(zt, zq, d[:, None], g.random((trials, 1), dtype=np.float32), g.random(trials, dtype=np.float32),
+                  gm.GM_SAMPLE)
+    counts = np.bincount(out[:, 0], minlength=V)
+    assert scipy.stats.chisquare(counts, trials * p).pvalue > 0.01
+    alpha = np.minimum(p, q).sum()
+    assert abs(n.mean() - alpha) < 5 * np.sqrt(alpha * (1 - alpha) / trials)
+
+
+def test_accept_is_deterministic():
+    need_gpu()
+    B, k, V = 32, 3, 151936
+    zt = synth.normal_logits((B, k + 1, V), 3, "det")
+    zq = synth.normal_logits((B, k, V), 3, "det-q")
+    ua, uf, ud = synth.uniforms(B, k, 4, "det")
+    drafts = _sampled_drafts(zq, ud)
+    a = _run(zt, zq, drafts, ua, uf, gm.GM_SAMPLE)
+    b = _run(zt, zq, drafts, ua, uf, gm.GM_SAMPLE)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+
+
+@pytest.mark.parametrize("page_size", [16, 64])
+def test_kv_commit_matches_oracle(page_size):
+    need_gpu()
+    B, k = 50, 7
+    g = np.random.default_rng(5)
+    shape = synth.QWEN3_4B_LAYER
+    lens = g.integers(1, 600, B)
+    n = g.integers(0, k + 1, B).astype(np.int32)
+    cache = gm.PagedCache(shape, 1, lens, lens + k + 1, page_size=page_size, seed=3)
+    slots = torch.zeros((B, k + 1), dtype=torch.int32, device="cuda")
+    gm.kv_commit(cache, k, i32(n), slots)
+    torch.cuda.synchronize()
+    new_lens, ref = oracle.kv_commit(lens, n, k, cache.block_table_host, page_size)
+    np.testing.assert_array_equal(cache.seq_lens.cpu().numpy(), new_lens)
+    np.testing.assert_array_equal(slots.cpu().numpy(), ref)

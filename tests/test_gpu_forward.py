@@ -1,0 +1,114 @@
+"""GPU parity of gm_verify_forward against the oracle: logits and hiddens
+within 1e-4 (float32 model) or 2e-2 (bf16 model) relative error, the block's
+K/V entries written at positions m_b .. m_b + k, and greedy accept counts on
+the GPU's logits bit-exact with the oracle's outside the flag window."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from helpers import need_gpu, rel_err, device_cache, synth_caches, t32, i32, flag_report, CONTRACT, EXACT
+from paper_2609_16648_amd import gm
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_forward(model, cache, tokens):
+    B, k1 = tokens.shape
+    s = model.shape
+    logits = torch.empty((B, k1, s.vocab), dtype=torch.float32, device="cuda")
+    hidden = torch.empty((B, k1, s.hidden), dtype=torch.float32, device="cuda")
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    gm.verify_forward(model, cache, i32(tokens), logits, hidden, gm.Workspace(), err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    return logits.cpu().numpy(), hidden.cpu().numpy()
+
+
+def _gpu_greedy(logits, drafts):
+    B, k1, V = logits.shape
+    n = torch.zeros(B, dtype=torch.int32, device="cuda")
+    out = torch.zeros((B, k1), dtype=torch.int32, device="cuda")
+    gm.spec_accept(t32(logits), None, i32(drafts), None, None, n, out, gm.GM_GREEDY, gm.Workspace())
+    torch.cuda.synchronize()
+    return n.cpu().numpy(), out.cpu().numpy()
+
+
+@pytest.mark.parametrize("qk_norm", [False, True])
+def test_tiny_f32_forward(qk_norm):
+    need_gpu()
+    wl = synth.WORKLOADS["tiny"]
+    shape = dataclasses.replace(wl.shape, qk_norm=qk_norm)
+    W = synth.model_weights(shape)
+    B, k, T0 = wl.batch, wl.k, wl.ctx_lo
+    prompt = synth.token_ids(B * T0, shape.vocab, 1, "tiny-prompt").reshape(B, T0)
+    caches = oracle.prefill(shape, W, prompt, EXACT)
+    # the cache holds what the GPU stores: float32 entries
+    caches = [([a.astype(np.float32) for a in ks], [a.astype(np.float32) for a in vs]) for ks, vs in caches]
+    lens = np.full(B, T0)
+    tokens = synth.token_ids(B * (k + 1), shape.vocab, 1, "tiny-block").reshape(B, k + 1)
+    model = gm.DeviceModel(shape, W)
+    cache = device_cache(shape, caches, lens, k + 1)
+    logits, hidden = _gpu_forward(model, cache, tokens)
+    ref, ref_h, new_kv = oracle.verify_forward(shape, W, caches, tokens, lens, EXACT)
+    e = rel_err(logits, ref)
+    print("[forward tiny f32 qk_norm=%d] logits rel err %.3e" % (qk_norm, e), flush=True)
+    assert e < 1e-4
+    assert rel_err(hidden, ref_h) < 1e-4
+    for l in range(shape.n_layers):
+        for b in range(B):
+            kk, vv = cache.read(l, b, lens[b] + np.arange(k + 1))
+            assert rel_err(kk, new_kv[l][0][b]) < 1e-5
+            assert rel_err(vv, new_kv[l][1][b]) < 1e-5
+    # no-cache definition: the block rows of a full causal forward
+    full, _, _ = oracle.full_forward(shape, W, np.concatenate([prompt, tokens], 1), EXACT)
+    assert rel_err(logits, full[:, T0:]) < 1e-4
+
+
+@pytest.fixture(scope="module")
+def qwen_layer():
+    wl = synth.WORKLOADS["qwen3_4b_layer"]
+    shape = wl.shape
+    W = synth.model_weights(shape)
+    lens = synth.context_lengths(wl)
+    caches = synth_caches(shape, lens, shape.n_layers)
+    pending = synth.token_ids(wl.batch, shape.vocab, 1, "pending")
+    take, alt = synth.mixing_draws(wl.batch, wl.k, shape.vocab, wl.mix_prob)
+    drafts = oracle.mixing_drafts(shape, W, caches, lens, pending, take, alt, CONTRACT)
+    return wl, shape, W, lens, caches, np.concatenate([pending[:, None], drafts], 1)
+
+
+def test_qwen_layer_bf16_forward(qwen_layer):
+    need_gpu()
+    wl, shape, W, lens, caches, tokens = qwen_layer
+    k = wl.k
+    model = gm.DeviceModel(shape, W)
+    cache = device_cache(shape, caches, lens, k + 1)
+    logits, hidden = _gpu_forward(model, cache, tokens)
+    ref_c, ref_hc, kv_c = oracle.verify_forward(shape, W, caches, tokens, lens, CONTRACT)
+    ref_e, _, _ = oracle.verify_forward(shape, W, caches, tokens, lens, EXACT)
+    e_exact, e_contract = rel_err(logits, ref_e), rel_err(logits, ref_c)
+    print("[forward qwen3 layer bf16] logits rel err vs exact %.3e, vs contract %.3e; hidden %.3e"
+          % (e_exact, e_contract, rel_err(hidden, ref_hc)), flush=True)
+    assert e_exact < 2e-2
+    # float32 accumulation still flips ~0.1% of the bf16 roundings the contract mirrors; a float32
+    # CPU emulation of the same arithmetic lands 4-5e-3 from the float64 contract oracle
+    assert e_contract < 1e-2
+    assert rel_err(hidden, ref_hc) < 1e-2
+    for b in range(0, wl.batch, 9):
+        kk, vv = cache.read(0, b, lens[b] + np.arange(k + 1))
+        assert np.abs(kk - kv_c[0][0][b]).max() <= 2.0 ** -7 * np.abs(kv_c[0][0][b]).max()
+        assert np.abs(vv - kv_c[0][1][b]).max() <= 2.0 ** -7 * np.abs(kv_c[0][1][b]).max()
+    # greedy acceptance on the GPU's logits equals the oracle's outside the flags
+    drafts = tokens[:, 1:]
+    ref = oracle.spec_accept(ref_c, None, drafts, None, None, mode="greedy")
+    n, out = _gpu_greedy(logits, drafts)
+    flag_report("forward+greedy qwen3 layer", ref.flagged, len(n))
+    ok = ~ref.flagged
+    np.testing.assert_array_equal(n[ok], ref.n_accept[ok])
+    np.testing.assert_array_equal(out[ok], ref.out_tokens[ok])
+    tau = 1 + n.mean()
+    print("[forward+greedy qwen3 layer] tau %.3f (0.7 mixing predicts %.3f)" % (tau, (1 - 0.7 ** 4) / 0.3), flush=True)

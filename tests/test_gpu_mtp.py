@@ -1,0 +1,129 @@
+"""GPU parity of gm_mtp_draft against the oracle's draft head: draft logits
+within 1e-4 (float32) / 2e-3 of the rounding-contract oracle (bf16), drafts
+identical up to the first flagged position, the extend entries written at
+the committed slots and the head's length moved to the new boundary."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from helpers import need_gpu, rel_err, device_cache, t32, i32, flag_report, CONTRACT, EXACT
+from paper_2609_16648_amd import gm
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(shape, B, k, lo, hi, seed):
+    g = np.random.default_rng(seed)
+    lens = g.integers(lo, hi, B)
+    caches = [synth.kv_prefix(shape, lens, layer=100 + seed)]
+    hidden = g.standard_normal((B, k + 1, shape.hidden)).astype(np.float32)
+    n = g.integers(0, k + 1, B).astype(np.int32)
+    out = g.integers(0, shape.vocab, (B, k + 1)).astype(np.int32)
+    for b in range(B):
+        out[b, n[b] + 1:] = -1
+    u = synth.uniforms(B, k, 4, "mtp", seed)[2]
+    return lens, caches, hidden, n, out, u
+
+
+def _flags(logits, drafts, u, mode, margin=1e-2, final_eps=1e-9):
+    """First position of every sequence whose draft a correct float32 evaluation could change."""
+    B, k, V = logits.shape
+    first = np.full(B, k)
+    for b in range(B):
+        for j in range(k):
+            z = logits[b, j].astype(np.float32)
+            if mode == gm.GM_GREEDY:
+                s = np.partition(z, V - 2)
+                bad = s[-1] - s[-2] < margin
+            else:
+                _, dist, zz = oracle.inverse_cdf(oracle.softmax(z.astype(np.float64)), u[b, j])
+                bad = dist < final_eps * zz
+            if bad:
+                first[b] = j
+                break
+    return first
+
+
+def _run(shape, W, Wm, lens, caches, hidden, n, out, u, k, mode, rnd, tol):
+    B = len(lens)
+    model = gm.DeviceModel(shape, W)
+    mtp = gm.DeviceMtp(shape, Wm)
+    cache = device_cache(shape, caches, lens, 2 * k + 2)
+    drafts = torch.zeros((B, k), dtype=torch.int32, device="cuda")
+    dlog = torch.zeros((B, k, shape.vocab), dtype=torch.float32, device="cuda")
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    gm.mtp_draft(model, mtp, cache, k, mode, t32(hidden), i32(n), i32(out), t32(u), drafts, dlog, gm.Workspace(),
+                 dev_err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    ref = oracle.mtp_draft(shape, Wm, W, caches[0][0], caches[0][1], lens, hidden, n, out, u, k,
+                           "greedy" if mode == gm.GM_GREEDY else "sample", 1.0, rnd)
+    got_d, got_l = drafts.cpu().numpy(), dlog.cpu().numpy()
+    np.testing.assert_array_equal(cache.seq_lens.cpu().numpy(), ref["new_lens"])
+    first = _flags(ref["draft_logits"], ref["drafts"], u, mode)
+    flag_report("mtp mode=%d" % mode, first < k, B)
+    worst = 0.0
+    for b in range(B):
+        f = first[b]
+        np.testing.assert_array_equal(got_d[b, :f], ref["drafts"][b, :f])
+        upto = min(f + 1, k)         # logits up to the first flagged draw are still comparable
+        worst = max(worst, rel_err(got_l[b, :upto], ref["draft_logits"][b, :upto]))
+        ek, ev = cache.read(0, b, lens[b] + np.arange(n[b] + 1))
+        assert rel_err(ek, ref["ext_k"][b]) < tol and rel_err(ev, ref["ext_v"][b]) < tol
+    print("[mtp mode=%d] draft logits rel err %.3e" % (mode, worst), flush=True)
+    assert worst < tol
+    return got_d
+
+
+@pytest.mark.parametrize("mode", [gm.GM_GREEDY, gm.GM_SAMPLE])
+def test_tiny_f32_mtp(mode):
+    need_gpu()
+    shape = synth.TINY
+    W = synth.model_weights(shape)
+    Wm = synth.mtp_weights(shape)
+    k = 3
+    lens, caches, hidden, n, out, u = _inputs(shape, 6, k, 1, 150, 1)
+    _run(shape, W, Wm, lens, caches, hidden, n, out, u, k, mode, EXACT, 1e-4)
+
+
+@pytest.fixture(scope="module")
+def qwen_mtp():
+    shape = synth.QWEN3_4B_LAYER
+    return shape, synth.model_weights(shape), synth.mtp_weights(shape)
+
+
+def test_qwen_layer_bf16_mtp_greedy(qwen_mtp):
+    # bf16 logits sit ~1e-3 from the oracle's: drafts are compared in greedy mode (top-2 margin flags)
+    need_gpu()
+    shape, W, Wm = qwen_mtp
+    k = 3
+    lens, caches, hidden, n, out, u = _inputs(shape, 8, k, 1, 3000, 2)
+    _run(shape, W, Wm, lens, caches, hidden, n, out, u, k, gm.GM_GREEDY, CONTRACT, 1e-2)
+
+
+def test_qwen_layer_bf16_mtp_sample_logits(qwen_mtp):
+    # sample mode: the first draft's logits do not depend on any draw; report the draw match rate
+    need_gpu()
+    shape, W, Wm = qwen_mtp
+    k = 3
+    lens, caches, hidden, n, out, u = _inputs(shape, 8, k, 1, 3000, 3)
+    B = len(lens)
+    model, mtp = gm.DeviceModel(shape, W), gm.DeviceMtp(shape, Wm)
+    cache = device_cache(shape, caches, lens, 2 * k + 2)
+    drafts = torch.zeros((B, k), dtype=torch.int32, device="cuda")
+    dlog = torch.zeros((B, k, shape.vocab), dtype=torch.float32, device="cuda")
+    gm.mtp_draft(model, mtp, cache, k, gm.GM_SAMPLE, t32(hidden), i32(n), i32(out), t32(u), drafts, dlog,
+                 gm.Workspace())
+    torch.cuda.synchronize()
+    ref = oracle.mtp_draft(shape, Wm, W, caches[0][0], caches[0][1], lens, hidden, n, out, u, k, "sample", 1.0,
+                           CONTRACT)
+    e = rel_err(dlog.cpu().numpy()[:, 0], ref["draft_logits"][:, 0])
+    match = float((drafts.cpu().numpy()[:, 0] == ref["drafts"][:, 0]).mean())
+    print("[mtp bf16 sample] first-draft logits rel err %.3e, first-draft match rate %.2f" % (e, match), flush=True)
+    assert e < 1e-2
+    got = drafts.cpu().numpy()
+    assert ((got >= 0) & (got < shape.vocab)).all()

@@ -1,0 +1,396 @@
+#!/usr/bin/env python3
+"""Benchmark of the batched speculative-decoding step on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--mode sample|greedy]
+
+One step is the whole hot path over one batch: gm_verify_forward (target
+forward over the k+1 block positions), gm_spec_accept, gm_kv_commit and
+gm_mtp_draft (the draft of the next block).  Inputs are seeded synthetic
+tensors with the shapes of the workload (weights N(0, 0.02), KV N(0, 1));
+they are resident in HBM before the timed region.  Each step restarts from
+the same committed lengths, so every timed step does identical work.
+
+Prints one JSON line: throughput (committed tokens/s), the roofline of the
+dominant kernel measured with HIP events inside the timed region, the
+per-kernel breakdown, and the CPU oracle timed on a bounded sample of the
+same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+HBM_GBS = 8000.0            # MI355X HBM3E peak, GB/s
+BF16_TFLOPS = 2500.0        # MI355X dense bf16 matrix peak, TFLOP/s
+METRIC = "accepted tokens/s per verify step; verify-attn HBM GB/s & GEMM MFMA % of peak"
+
+DESCRIPTIONS = {
+    "qwen3_4b_layer": "one Qwen3-4B-shaped layer (H 2560, 32/8 heads x 128, FFN 9728) + LM head (V 151936) "
+                      "+ 1-layer MTP head of the same shape; B=64, contexts U[1024,4096], k=3, drafts = target "
+                      "top-1 w.p. 0.7 else uniform; T=1",
+    "qwen3_4b_full": "36-layer Qwen3-4B shape + 1-layer MTP head; B=256, contexts 512+U[0,8192], k=3; T=1",
+    "long_ctx": "Qwen3-4B-shaped verify attention + accept only; B=32, contexts U[16384,32768], k=7, "
+                "drafts sampled from q = softmax(N(0,1)); T=1",
+}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+# ----------------------------------------------------------------------------- accounting
+def accounting(wl, lens):
+    """Algorithmic flops and HBM bytes per step, per kernel name."""
+    s, B, k = wl.shape, wl.batch, wl.k
+    R, M = k + 1, wl.batch * (k + 1)
+    H, F, V, d = s.hidden, s.ffn, s.vocab, s.head_dim
+    nq, nkv, L = s.n_heads, s.n_kv_heads, s.n_layers
+    qw, qd = (nq + 2 * nkv) * d, nq * d
+    ctx = lens.astype(np.float64) + R
+    kv_bytes = float((ctx * nkv * d * 2 * 2).sum())            # K and V, bf16
+    attn_flops = float((4.0 * R * nq * ctx * d).sum())
+
+    def gemm(m, n, kk, out_bytes, add=False):
+        return 2.0 * m * n * kk, 2.0 * n * kk + 2.0 * m * kk + m * n * out_bytes * (2 if add else 1)
+
+    acc = {}
+
+    def put(name, fb, launches):
+        f, b = fb
+        acc[name] = dict(flops=f * launches, bytes=b * launches, launches=launches)
+
+    if wl.name != "long_ctx":
+        put("gemm_qkv", gemm(M, qw, H, 4), L)
+        put("gemm_o", gemm(M, H, qd, 4, add=True), L)
+        put("gemm_gate_up", (2.0 * M * 2 * F * H, 2.0 * 2 * F * H + 2.0 * M * H + 2.0 * M * F), L)
+        put("gemm_down", gemm(M, H, F, 4, add=True), L)
+        put("gemm_lm_head", gemm(M, V, H, 4), 1)
+    put("attn_verify", (attn_flops, kv_bytes + 2.0 * 2 * M * qd), L)
+    put("accept_row_stats", (0.0, 4.0 * B * (2 * k + 1) * V), 1)
+    if wl.with_mtp:
+        mkv = float((lens.astype(np.float64) * nkv * d * 2 * 2).sum())
+        put("mtp_gemm_lm_head", gemm(B, V, H, 4), k)
+        put("mtp_gemm_proj", ((2.0 * (M + (k - 1) * B) * H * 2 * H) / k, 2.0 * H * 2 * H), k)
+        put("mtp_gemm_qkv", ((2.0 * (M + (k - 1) * B) * qw * H) / k, 2.0 * qw * H), k)
+        put("mtp_gemm_o", gemm(B, H, qd, 4, add=True), k)
+        put("mtp_gemm_gate_up", (2.0 * B * 2 * F * H, 2.0 * 2 * F * H + 2.0 * B * H + 2.0 * B * F), k)
+        put("mtp_gemm_down", gemm(B, H, F, 4, add=True), k)
+        put("attn_mtp", (4.0 * nq * float(lens.sum()) * d * k, mkv), k)
+        put("draft_row_stats", (0.0, 4.0 * B * V), k)
+    return acc
+
+
+# ----------------------------------------------------------------------------- workloads
+class Step:
+    """Device state of one workload and the enqueue of one step."""
+
+    def __init__(self, wl, mode, device="cuda"):
+        import torch
+        from paper_2609_16648_amd import gm
+        self.torch, self.gm, self.wl = torch, gm, wl
+        s, B, k = wl.shape, wl.batch, wl.k
+        self.mode = gm.GM_SAMPLE if mode == "sample" else gm.GM_GREEDY
+        t0 = time.time()
+        self.lens = synth.context_lengths(wl)
+        cap = self.lens + 2 * k + 2
+        gen = torch.Generator(device=device)
+        gen.manual_seed(synth.SEED_KV)
+
+        def random_pools(cache):
+            for t in cache.k + cache.v:
+                t.normal_(generator=gen)
+
+        self.cache = gm.PagedCache(s, 1 if wl.name == "long_ctx" else s.n_layers, self.lens, cap,
+                                   page_size=wl.page_size, fill="empty")
+        random_pools(self.cache)
+        self.lens0 = self.cache.seq_lens.clone()
+        V = s.vocab
+        u_acc, u_fin, u_dr = synth.uniforms(B, k)
+        dev = lambda a, dt=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).to(device=device, dtype=dt)
+        self.ua, self.uf, self.ud = dev(u_acc), dev(u_fin), dev(u_dr)
+        self.zq = dev(synth.normal_logits((B, k, V), synth.SEED_DRAFT, wl.name, "zq"))
+        self.n = torch.zeros(B, dtype=torch.int32, device=device)
+        self.out = torch.zeros((B, k + 1), dtype=torch.int32, device=device)
+        self.slots = torch.zeros((B, k + 1), dtype=torch.int32, device=device)
+        self.ws_v, self.ws_a, self.ws_m = gm.Workspace(device), gm.Workspace(device), gm.Workspace(device)
+        self.cfg = gm.model_config(s)
+        if wl.name == "long_ctx":
+            R = k + 1
+            self.q = torch.empty((B, R, s.n_heads, s.head_dim), dtype=torch.bfloat16, device=device)
+            self.q.normal_(generator=gen)
+            self.attn_out = torch.empty_like(self.q)
+            self.zt = dev(synth.normal_logits((B, R, V), synth.SEED_DRAFT, wl.name, "zt"))
+            # drafts d_i ~ q_i by the inverse CDF with u_draft (set-up, not timed)
+            p = torch.softmax(self.zq.double(), -1).cumsum(-1)
+            tgt = self.ud.double()[..., None] * p[..., -1:]
+            self.drafts = torch.searchsorted(p, tgt, right=True).clamp_(max=V - 1)[..., 0].to(torch.int32)
+        else:
+            self.W = synth.model_weights(s)
+            self.model = gm.DeviceModel(s, self.W, device)
+            self.logits = torch.empty((B, k + 1, V), dtype=torch.float32, device=device)
+            self.hidden = torch.empty((B, k + 1, s.hidden), dtype=torch.float32, device=device)
+            if wl.with_mtp:
+                self.Wm = synth.mtp_weights(s)
+                self.mtp = gm.DeviceMtp(s, self.Wm, device)
+                self.mcache = gm.PagedCache(s, 1, self.lens, cap, page_size=wl.page_size, fill="empty")
+                random_pools(self.mcache)
+                self.next_drafts = torch.zeros((B, k), dtype=torch.int32, device=device)
+                self.dlog = torch.zeros((B, k, V), dtype=torch.float32, device=device)
+            self.pending = dev(synth.token_ids(B, V, synth.SEED_TOKENS, wl.name, "pending"), torch.int32)
+            self.drafts = self._mixing_drafts(device)
+            self.tokens = torch.cat([self.pending[:, None], self.drafts], 1).contiguous()
+        torch.cuda.synchronize()
+        log("[bench] set-up of %s took %.1f s" % (wl.name, time.time() - t0))
+
+    def _mixing_drafts(self, device):
+        """Draft i = the target's top-1 at block position i given the drafts before it with
+        probability mix_prob, else a uniform token (set-up: one verify forward per position)."""
+        torch, gm, wl = self.torch, self.gm, self.wl
+        B, k, V = wl.batch, wl.k, wl.shape.vocab
+        prob = wl.mix_prob if wl.mix_prob is not None else 0.0
+        take, alt = synth.mixing_draws(B, k, V, prob, synth.SEED_DRAFT, wl.name)
+        take, alt = torch.from_numpy(take).to(device), torch.from_numpy(alt).to(device)
+        drafts = alt.clone()
+        for i in range(k):
+            toks = torch.cat([self.pending[:, None], drafts], 1).contiguous()
+            self.cache.seq_lens.copy_(self.lens0)
+            gm.verify_forward(self.model, self.cache, toks, self.logits, self.hidden, self.ws_v)
+            top1 = torch.argmax(self.logits[:, i], -1).to(torch.int32)
+            drafts[:, i] = torch.where(take[:, i], top1, alt[:, i])
+        return drafts.contiguous()
+
+    def __call__(self):
+        gm, wl = self.gm, self.wl
+        k = wl.k
+        self.cache.seq_lens.copy_(self.lens0)
+        if wl.name == "long_ctx":
+            gm.verify_attention(self.cfg, self.cache, 0, self.q, self.attn_out, self.ws_v)
+            gm.spec_accept(self.zt, self.zq, self.drafts, self.ua, self.uf, self.n, self.out, self.mode, self.ws_a)
+            gm.kv_commit(self.cache, k, self.n, self.slots)
+            return
+        gm.verify_forward(self.model, self.cache, self.tokens, self.logits, self.hidden, self.ws_v)
+        gm.spec_accept(self.logits, self.zq, self.drafts, self.ua, self.uf, self.n, self.out, self.mode, self.ws_a)
+        gm.kv_commit(self.cache, k, self.n, self.slots)
+        if wl.with_mtp:
+            self.mcache.seq_lens.copy_(self.lens0)
+            gm.mtp_draft(self.model, self.mtp, self.mcache, k, self.mode, self.hidden, self.n, self.out, self.ud,
+                         self.next_drafts, self.dlog, self.ws_m)
+
+
+# ----------------------------------------------------------------------------- CPU baseline
+def cpu_baseline(wl, mode, budget_s, weights=None):
+    """The oracle, as it stands, on a bounded sample of the same workload: the
+    same step (verify forward in the rounding-contract mode, accept, commit,
+    MTP draft) for the first few sequences."""
+    import oracle
+    from threadpoolctl import threadpool_info
+    s, k = wl.shape, wl.k
+    rnd = oracle.Rounding("contract")
+    lens_all = synth.context_lengths(wl)
+    W = weights[0] if weights else (synth.model_weights(s) if wl.name != "long_ctx" else None)
+    Wm = weights[1] if weights and len(weights) > 1 else (synth.mtp_weights(s) if wl.with_mtp else None)
+    V = s.vocab
+    u_acc, u_fin, u_dr = synth.uniforms(wl.batch, k)
+    zq_all = synth.normal_logits((wl.batch, k, V), synth.SEED_DRAFT, wl.name, "zq")
+
+    def run(nseq):
+        idx = list(range(nseq))
+        lens = lens_all[:nseq]
+        if wl.name == "long_ctx":
+            ks, vs = synth.kv_prefix(s, lens + k + 1, 0, seqs=idx)
+            q = synth.normal_tensor((nseq, k + 1, s.n_heads, s.head_dim), 5, "bf16", "cpu-q")
+            zt = synth.normal_logits((nseq, k + 1, V), synth.SEED_DRAFT, wl.name, "cpu-zt")
+            dr = np.stack([oracle.inverse_cdf_rows(oracle.softmax(zq_all[:nseq, i].astype(np.float64)),
+                                                   u_dr[:nseq, i])[0] for i in range(k)], 1)
+            t0 = time.perf_counter()
+            for b in range(nseq):
+                oracle.attention(q[b].astype(np.float64), ks[b].astype(np.float64), vs[b].astype(np.float64),
+                                 lens[b] + np.arange(k + 1) + 1)
+            res = oracle.spec_accept(zt, zq_all[:nseq], dr, u_acc[:nseq], u_fin[:nseq])
+            oracle.kv_commit(lens, res.n_accept, k, np.arange(nseq * 4096).reshape(nseq, 4096), 16)
+            return time.perf_counter() - t0, int((res.n_accept + 1).sum())
+        caches = [synth.kv_prefix(s, lens, l, seqs=idx) for l in range(s.n_layers)]
+        pending = synth.token_ids(wl.batch, V, synth.SEED_TOKENS, wl.name, "pending")[:nseq]
+        prob = wl.mix_prob if wl.mix_prob is not None else 0.0
+        take, alt = synth.mixing_draws(wl.batch, k, V, prob, synth.SEED_DRAFT, wl.name)
+        dr = oracle.mixing_drafts(s, W, caches, lens, pending, take[:nseq], alt[:nseq], rnd)
+        block = np.concatenate([pending[:, None], dr], 1)
+        mk, mv = (synth.kv_prefix(s, lens, 99, seqs=idx) if wl.with_mtp else (None, None))
+        t0 = time.perf_counter()
+        logits, hid, _ = oracle.verify_forward(s, W, caches, block, lens, rnd)
+        if mode == "sample":
+            res = oracle.spec_accept(logits.astype(np.float32), zq_all[:nseq], dr, u_acc[:nseq], u_fin[:nseq])
+        else:
+            res = oracle.spec_accept(logits.astype(np.float32), None, dr, None, None, mode="greedy")
+        oracle.kv_commit(lens, res.n_accept, k, np.arange(nseq * 4096).reshape(nseq, 4096), 16)
+        if wl.with_mtp:
+            oracle.mtp_draft(s, Wm, W, mk, mv, lens, hid, res.n_accept, res.out_tokens, u_dr[:nseq], k, mode, 1.0, rnd)
+        return time.perf_counter() - t0, int((res.n_accept + 1).sum())
+
+    # the oracle works in float64: hand it float64 weights once, outside the timed runs
+    def f64(w):
+        if isinstance(w, dict):
+            return {kk: f64(vv) for kk, vv in w.items()}
+        if isinstance(w, list):
+            return [f64(vv) for vv in w]
+        return np.asarray(w, dtype=np.float64)
+    if W is not None:
+        tied = W["lm_head"] is W["embed"]
+        W = f64(W)
+        if tied:
+            W["lm_head"] = W["embed"]
+    if Wm is not None:
+        Wm = f64(Wm)
+    t1, c1 = run(1)
+    per_seq = max(t1, 1e-3)
+    nseq = int(max(1, min(wl.batch, budget_s / per_seq)))
+    t, c = run(nseq) if nseq > 1 else (t1, c1)
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": c / t, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": "%d of %d sequences of the %s workload, one full step (verify forward in the bf16 "
+                      "rounding-contract mode, accept, commit%s) in %.1f s, %d committed tokens"
+                      % (nseq, wl.batch, wl.name, ", MTP draft" if wl.with_mtp else "", t, c)}
+
+
+# ----------------------------------------------------------------------------- main
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="qwen3_4b_layer", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--mode", default="sample", choices=["sample", "greedy"])
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="also time a plain device copy of this many MiB (HBM counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs the step on one GPU only; N > 1 is not supported "
+              "(sequences are independent: data parallelism would need no exchange)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_16648_amd import gm
+    gm.lib()
+    torch.cuda.set_device(0)
+    wl = synth.WORKLOADS[args.workload]
+    step = Step(wl, args.mode)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    n_warm = step.n.clone()
+
+    # all kernels of a few steps, to find the dominant one and the breakdown
+    gm.trace_start()
+    probe_steps = 3
+    for _ in range(probe_steps):
+        step()
+    per_kernel = gm.trace_stop()
+    dominant = max(per_kernel, key=lambda n: per_kernel[n][1])
+
+    # timed region: K identical steps; the dominant kernel is bracketed by HIP events
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    gm.trace_start(dominant)
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    dom = gm.trace_stop()[dominant]
+    ms = e0.elapsed_time(e1) / args.steps
+    if not torch.equal(step.n, n_warm):
+        raise RuntimeError("steps are not identical: accept counts changed between steps")
+    n = step.n.cpu().numpy()
+    committed = int((n + 1).sum())
+    value = committed / (ms / 1e3)
+
+    acc = accounting(wl, step.lens)
+    kernels = {}
+    for name, (launches, tot) in sorted(per_kernel.items(), key=lambda kv: -kv[1][1]):
+        ms_step = tot / probe_steps
+        row = {"ms_per_step": round(ms_step, 4), "launches_per_step": launches // probe_steps}
+        if name in acc and ms_step > 0:
+            a = acc[name]
+            row["GB_s"] = round(a["bytes"] / (ms_step * 1e-3) / 1e9, 1)
+            row["hbm_frac"] = round(row["GB_s"] / HBM_GBS, 3)
+            if a["flops"]:
+                row["TFLOP_s"] = round(a["flops"] / (ms_step * 1e-3) / 1e12, 1)
+                row["mfma_frac"] = round(row["TFLOP_s"] / BF16_TFLOPS, 3)
+        kernels[name] = row
+
+    a = acc.get(dominant)
+    dom_ms = dom[1] / dom[0]
+    if a is not None:
+        per_launch_bytes = a["bytes"] / a["launches"]
+        per_launch_flops = a["flops"] / a["launches"]
+        intensity = per_launch_flops / per_launch_bytes if per_launch_bytes else 0.0
+        if intensity * HBM_GBS * 1e9 > BF16_TFLOPS * 1e12:
+            roof = {"bound": "mfma", "achieved": round(per_launch_flops / (dom_ms * 1e-3) / 1e12, 1),
+                    "peak": BF16_TFLOPS, "unit": "TFLOP/s"}
+        else:
+            roof = {"bound": "hbm", "achieved": round(per_launch_bytes / (dom_ms * 1e-3) / 1e9, 1),
+                    "peak": HBM_GBS, "unit": "GB/s"}
+        roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+        roof["traffic"] = None
+        roof["kernel"] = dominant
+        roof["avg_launch_ms"] = round(dom_ms, 4)
+        roof["launches"] = dom[0]
+    else:
+        roof = {"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None,
+                "kernel": dominant}
+
+    gemm_names = [x for x in kernels if x.startswith("gemm_")]
+    verify_gemm_ms = sum(kernels[x]["ms_per_step"] for x in gemm_names)
+    verify_gemm_flops = sum(acc[x]["flops"] for x in gemm_names if x in acc)
+    summary = {
+        "verify_attn_GB_s": kernels.get("attn_verify", {}).get("GB_s"),
+        "verify_attn_hbm_frac": kernels.get("attn_verify", {}).get("hbm_frac"),
+        "verify_gemm_TFLOP_s": round(verify_gemm_flops / (verify_gemm_ms * 1e-3) / 1e12, 1) if verify_gemm_ms else None,
+        "verify_gemm_mfma_frac": round(verify_gemm_flops / (verify_gemm_ms * 1e-3) / 1e12 / BF16_TFLOPS, 3)
+        if verify_gemm_ms else None,
+        "tau": round(1.0 + float(n.mean()), 4),
+        "committed_tokens_per_step": committed,
+    }
+
+    if args.copy_probe_mib:
+        src = torch.empty(args.copy_probe_mib << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        summary["copy_probe_mib"] = args.copy_probe_mib
+
+    line = {"metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": args.workload, "description": DESCRIPTIONS[args.workload],
+                       "batch": wl.batch, "k": wl.k, "accept_mode": args.mode, "parallelism": "none (1 GPU)"},
+            "roofline": roof, "summary": summary, "kernels": kernels}
+    if not args.no_cpu_baseline:
+        weights = None
+        if hasattr(step, "W"):
+            weights = (step.W, step.Wm) if wl.with_mtp else (step.W,)
+        line["cpu_baseline"] = cpu_baseline(wl, args.mode, args.cpu_budget, weights)
+    else:
+        line["cpu_baseline"] = None
+    for name, row in kernels.items():
+        log("[bench] %-24s %s" % (name, row))
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

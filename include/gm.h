@@ -66,8 +66,9 @@ typedef enum {
  * / grouped-query attention / SwiGLU, the layer of the paper's backbones
  * (App. "Models and Draft Heads").  Limits of this build: head_dim 128 for
  * GM_BF16 (64 or 128 for GM_F32), n_heads a multiple of n_kv_heads with
- * (n_heads / n_kv_heads) * (k + 1) <= 64, hidden and ffn multiples of 64,
- * GM_BF16 needs vocab, hidden, ffn and n_heads * head_dim multiples of 128. */
+ * (n_heads / n_kv_heads) * (k + 1) <= 64, hidden and ffn multiples of 64;
+ * GM_BF16 needs vocab a multiple of 128 and hidden, ffn and
+ * n_heads * head_dim multiples of 256. */
 typedef struct {
   int n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab;
   float rope_base;       /* 10000 */
@@ -77,7 +78,16 @@ typedef struct {
   int tie_embed;         /* informational: lm_head may alias embed */
 } gm_model_config;
 
-/* One decoder layer.  Linear weights are row-major [out, in] (y = W x). */
+/* One decoder layer.  A linear weight W[out][in] (y = W x) is stored
+ *  - GM_F32: row-major;
+ *  - GM_BF16: tiled, in tiles of 16 rows x 32 columns: element (n, c) at
+ *      ((n / 16) * (in / 32) + c / 32) * 512 + ((c % 32) / 8) * 128 + (n % 16) * 8 + c % 8,
+ *    so that a 16-row strip of W is a run of 1 KiB tiles along `in`, each
+ *    read by one 16-byte-per-lane load of a 64-lane wave in the operand order
+ *    of the matrix cores.  (Row-major W converts to this layout by viewing it
+ *    as [out/16][16][in/32][4][8] and permuting to [out/16][in/32][4][16][8].)
+ * The tiled layout applies to w_qkv, w_o, w_gate_up, w_down, the MTP w_proj
+ * and lm_head; embeddings and norm weights are plain vectors / row-major. */
 typedef struct {
   const void *attn_norm;  /* [H] */
   const void *w_qkv;      /* [(n_heads + 2 n_kv_heads) head_dim, H]: the rows of W_q, then W_k, then W_v */

@@ -102,7 +102,7 @@ def verify_forward(shape, W, caches, tokens: np.ndarray, lens: np.ndarray, rnd: 
     lm_rows selects the block rows whose logits are wanted."""
     tokens = np.asarray(tokens)
     B, R = tokens.shape
-    x = _f64(W["embed"])[tokens]
+    x = _f64(np.asarray(W["embed"])[tokens])
     pos = np.asarray(lens, dtype=np.int64)[:, None] + np.arange(R)[None, :]
     new_kv = []
     for li, Wl in enumerate(W["layers"]):

@@ -50,7 +50,7 @@ def mtp_apply(shape, Wm, W, h: np.ndarray, toks: np.ndarray, pos: np.ndarray,
     cache [s, n_kv, d] entries the rows attend before their own.
     Returns (g [R, H] layer outputs, logits [R, V], k [R,n_kv,d], v [R,n_kv,d])."""
     a = rmsnorm(h, Wm["norm_h"], shape.rms_eps)
-    e = rmsnorm(_f64(W["embed"])[np.asarray(toks)], Wm["norm_e"], shape.rms_eps)
+    e = rmsnorm(_f64(np.asarray(W["embed"])[np.asarray(toks)]), Wm["norm_e"], shape.rms_eps)
     x = rnd(np.concatenate([a, e], axis=-1)) @ _f64(Wm["w_proj"]).T
     g, k, v = layer_forward(shape, Wm["layer"], x[None], np.asarray(pos)[None],
                             [cache_k], [cache_v], rnd)

@@ -65,8 +65,9 @@ gm_status check_config(const gm_model_config *cfg, int B, int k) {
   if (!(cfg->rms_eps >= 0.f) || !(cfg->rope_base > 0.f)) return fail(GM_ERR_INVALID_ARG, "bad rms_eps or rope_base");
   if (cfg->dtype == GM_BF16) {
     if (cfg->head_dim != 128) return fail(GM_ERR_UNSUPPORTED, "bf16 path needs head_dim 128, got %d", cfg->head_dim);
-    if (cfg->vocab % 128 || cfg->hidden % 128 || cfg->ffn % 128 || (cfg->n_heads * cfg->head_dim) % 128)
-      return fail(GM_ERR_UNSUPPORTED, "bf16 path needs vocab, hidden, ffn and n_heads*head_dim multiples of 128");
+    if (cfg->vocab % 128 || cfg->hidden % 256 || cfg->ffn % 256 || (cfg->n_heads * cfg->head_dim) % 256)
+      return fail(GM_ERR_UNSUPPORTED,
+                  "bf16 path needs vocab a multiple of 128 and hidden, ffn, n_heads*head_dim multiples of 256");
   } else {
     if (cfg->head_dim != 64 && cfg->head_dim != 128)
       return fail(GM_ERR_UNSUPPORTED, "f32 path needs head_dim 64 or 128, got %d", cfg->head_dim);
@@ -152,11 +153,11 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
   RowStat *tstat = (RowStat *)(w + p.tstat), *dstat = (RowStat *)(w + p.dstat);
   RowSel *sel = (RowSel *)(w + p.sel);
   const float inv_t = 1.0f / temperature;
-  launch_row_stats(target_logits, V, B * (k + 1), V, inv_t, tstat, s);
-  if (mode == GM_SAMPLE && k > 0) launch_row_stats(draft_logits, V, B * k, V, inv_t, dstat, s);
+  launch_row_stats("accept_row_stats", target_logits, V, B * (k + 1), V, inv_t, tstat, s);
+  if (mode == GM_SAMPLE && k > 0) launch_row_stats("accept_row_stats", draft_logits, V, B * k, V, inv_t, dstat, s);
   launch_accept_decide(B, k, V, mode, inv_t, target_logits, draft_logits, tstat, dstat, draft_tokens, u_accept,
                        u_final, n_accept, out_tokens, sel, s);
-  if (mode == GM_SAMPLE) launch_residual_draw(B, V, inv_t, sel, (double *)(w + p.wsum), (double *)(w + p.psum), s);
+  if (mode == GM_SAMPLE) launch_residual_draw("accept_residual_chunk", "accept_residual_scan", B, V, inv_t, sel, (double *)(w + p.wsum), (double *)(w + p.psum), s);
   return check_launch("gm_spec_accept");
 }
 
@@ -189,6 +190,8 @@ extern "C" gm_status gm_verify_attention(const gm_model_config *cfg, const gm_kv
   st = check_ws(ws, ws_bytes, p.total);
   if (st != GM_OK) return st;
   AttnArgs a = attn_args(*cfg, *cache, layer, B, k + 1, cache->seq_lens, 0, nullptr);
+  a.trace = "attn_verify";
+  a.trace_combine = "attn_verify_combine";
   a.q = q;
   a.out = out;
   a.dev_err = dev_err;

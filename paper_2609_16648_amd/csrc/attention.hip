@@ -302,6 +302,8 @@ AttnArgs attn_args(const gm_model_config &cfg, const gm_kv_cache &c, int layer, 
   a.blk_len = blk_len;
   a.blk_len_add = 0;
   a.scale = 1.0f / sqrtf((float)cfg.head_dim);
+  a.trace = "attn";
+  a.trace_combine = "attn_combine";
   return a;
 }
 
@@ -334,12 +336,12 @@ void run_attention(const AttnArgs &a, const AttnPlan &p, char *ws, hipStream_t s
     k.scale_log2 = a.scale * 1.4426950408889634f;
     dim3 grid(p.splits, a.n_kv, a.B);
     {
-      TraceScope ts("attn_mfma", s);
+      TraceScope ts(a.trace, s);
       if (p.rows_pad == 16) hipLaunchKernelGGL(attn_mfma_kernel<1>, grid, dim3(64), 0, s, k);
       else if (p.rows_pad == 32) hipLaunchKernelGGL(attn_mfma_kernel<2>, grid, dim3(64), 0, s, k);
       else hipLaunchKernelGGL(attn_mfma_kernel<4>, grid, dim3(64), 0, s, k);
     }
-    TraceScope ts("attn_combine", s);
+    TraceScope ts(a.trace_combine, s);
     hipLaunchKernelGGL(attn_combine_kernel, dim3(a.n_kv, a.B), dim3(256), 0, s, k, (uint16_t *)a.out);
   } else {
     AttnF f{};
@@ -362,7 +364,7 @@ void run_attention(const AttnArgs &a, const AttnPlan &p, char *ws, hipStream_t s
     f.num_pages = a.num_pages;
     f.scale = a.scale;
     dim3 grid(a.R, a.n_heads, a.B);
-    TraceScope ts("attn_f32", s);
+    TraceScope ts(a.trace, s);
     if (a.head_dim == 64) hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(64), 0, s, f);
     else hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(64), 0, s, f);
   }

@@ -9,6 +9,23 @@ namespace {
 size_t esize(int dtype) { return dtype == GM_BF16 ? 2 : 4; }
 int qkv_width(const gm_model_config &c) { return (c.n_heads + 2 * c.n_kv_heads) * c.head_dim; }
 
+// largest K-split partial buffer over the layer GEMMs at M rows (plus the LM head)
+size_t part_bytes(const gm_model_config &c, int M, bool with_proj) {
+  const int H = c.hidden, qd = c.n_heads * c.head_dim;
+  size_t b = 0;
+  auto upd = [&](int epi, int N, int K) {
+    const size_t x = plan_gemm(c.dtype, epi, M, N, K).part_bytes;
+    if (x > b) b = x;
+  };
+  upd(EPI_STORE_F32, qkv_width(c), H);
+  upd(EPI_ADD_F32, H, qd);
+  upd(EPI_SWIGLU, c.ffn, H);
+  upd(EPI_ADD_F32, H, c.ffn);
+  upd(EPI_STORE_F32, c.vocab, H);
+  if (with_proj) upd(EPI_STORE_F32, H, 2 * H);
+  return b;
+}
+
 RopeArgs rope_args(const gm_model_config &cfg, const gm_kv_cache &c, int layer, int M, int R, const float *qkv,
                    void *q_out, const int32_t *base, int base_off, const int32_t *blk_len, int pos_off,
                    const gm_layer_weights &L, int32_t *dev_err) {
@@ -54,6 +71,7 @@ ForwardPlan plan_forward(const gm_model_config &cfg, int B, int k, int max_ctx) 
   p.attn = c.take(M * qd * e);
   p.attn_plan = plan_attention(cfg, B, k + 1, max_ctx);
   p.attn_ws = c.take(p.attn_plan.total);
+  p.part = c.take(part_bytes(cfg, (int)M, false));
   p.total = c.off;
   return p;
 }
@@ -67,25 +85,27 @@ void run_verify_forward(const gm_model_config &cfg, const gm_model_weights &w, c
   const int qd = cfg.n_heads * cfg.head_dim;
   void *nbuf = ws + p.nbuf, *act = ws + p.act, *q = ws + p.q, *attn = ws + p.attn;
   float *qkv = (float *)(ws + p.qkv);
-  float *x = hidden;
+  float *x = hidden, *part = (float *)(ws + p.part);
   launch_embed(dt, M, H, V, tokens, w.embed, x, dev_err, s);
   for (int l = 0; l < cfg.n_layers; ++l) {
     const gm_layer_weights &L = w.layers[l];
     launch_rmsnorm(dt, M, H, cfg.rms_eps, x, L.attn_norm, nbuf, s);
-    launch_gemm("gemm_qkv", dt, EPI_STORE_F32, M, qkv_width(cfg), H, nbuf, H, L.w_qkv, qkv, qkv_width(cfg), s);
+    launch_gemm("gemm_qkv", dt, EPI_STORE_F32, M, qkv_width(cfg), H, nbuf, H, L.w_qkv, qkv, qkv_width(cfg), part, s);
     launch_rope_append(rope_args(cfg, c, l, M, R, qkv, q, c.seq_lens, 0, nullptr, 0, L, dev_err), s);
     AttnArgs a = attn_args(cfg, c, l, B, R, c.seq_lens, 0, nullptr);
+    a.trace = "attn_verify";
+    a.trace_combine = "attn_verify_combine";
     a.q = q;
     a.out = attn;
     a.dev_err = dev_err;
     run_attention(a, p.attn_plan, ws + p.attn_ws, s);
-    launch_gemm("gemm_o", dt, EPI_ADD_F32, M, H, qd, attn, qd, L.w_o, x, H, s);
+    launch_gemm("gemm_o", dt, EPI_ADD_F32, M, H, qd, attn, qd, L.w_o, x, H, part, s);
     launch_rmsnorm(dt, M, H, cfg.rms_eps, x, L.ffn_norm, nbuf, s);
-    launch_gemm("gemm_gate_up", dt, EPI_SWIGLU, M, F, H, nbuf, H, L.w_gate_up, act, F, s);
-    launch_gemm("gemm_down", dt, EPI_ADD_F32, M, H, F, act, F, L.w_down, x, H, s);
+    launch_gemm("gemm_gate_up", dt, EPI_SWIGLU, M, F, H, nbuf, H, L.w_gate_up, act, F, part, s);
+    launch_gemm("gemm_down", dt, EPI_ADD_F32, M, H, F, act, F, L.w_down, x, H, part, s);
   }
   launch_rmsnorm(dt, M, H, cfg.rms_eps, x, w.final_norm, nbuf, s);
-  launch_gemm("gemm_lm_head", dt, EPI_STORE_F32, M, V, H, nbuf, H, w.lm_head, logits, V, s);
+  launch_gemm("gemm_lm_head", dt, EPI_STORE_F32, M, V, H, nbuf, H, w.lm_head, logits, V, part, s);
 }
 
 // ---------------------------------------------------------------- MTP draft
@@ -111,6 +131,8 @@ MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx) {
   p.sel = c.take(sizeof(RowSel) * (size_t)B);
   p.wsum = c.take(sizeof(double) * (size_t)B * scan_chunks(V));
   p.psum = c.take(sizeof(double) * (size_t)B * scan_chunks(V));
+  const size_t pe = part_bytes(cfg, (int)Me, true), pb = part_bytes(cfg, B, true);
+  p.part = c.take(pe > pb ? pe : pb);
   p.total = c.off;
   return p;
 }
@@ -133,34 +155,37 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
   RowStat *stat = (RowStat *)(ws + p.stat);
   RowSel *sel = (RowSel *)(ws + p.sel);
   double *wsum = (double *)(ws + p.wsum), *psum = (double *)(ws + p.psum);
+  float *part = (float *)(ws + p.part);
   int32_t *lens = c.seq_lens;
 
   // the layer tail on one row per sequence (x1 [B][H] float32 in place), then the
   // shared LM head into draft_logits[:, j, :] and the draw of drafts[:, j]
   auto tail_and_draw = [&](float *x1, int j) {
-    launch_gemm("mtp_gemm_o", dt, EPI_ADD_F32, B, H, qd, attn_g, qd, L.w_o, x1, H, s);
+    launch_gemm("mtp_gemm_o", dt, EPI_ADD_F32, B, H, qd, attn_g, qd, L.w_o, x1, H, part, s);
     launch_rmsnorm(dt, B, H, cfg.rms_eps, x1, L.ffn_norm, nbuf, s);
-    launch_gemm("mtp_gemm_gate_up", dt, EPI_SWIGLU, B, F, H, nbuf, H, L.w_gate_up, act, F, s);
-    launch_gemm("mtp_gemm_down", dt, EPI_ADD_F32, B, H, F, act, F, L.w_down, x1, H, s);
+    launch_gemm("mtp_gemm_gate_up", dt, EPI_SWIGLU, B, F, H, nbuf, H, L.w_gate_up, act, F, part, s);
+    launch_gemm("mtp_gemm_down", dt, EPI_ADD_F32, B, H, F, act, F, L.w_down, x1, H, part, s);
     launch_rmsnorm(dt, B, H, cfg.rms_eps, x1, mtp.final_norm, nbuf, s);
     float *zl = draft_logits + (long)j * V;
-    launch_gemm("mtp_gemm_lm_head", dt, EPI_STORE_F32, B, V, H, nbuf, H, shared.lm_head, zl, (long)k * V, s);
-    launch_row_stats(zl, (long)k * V, B, V, inv_t, stat, s);
+    launch_gemm("mtp_gemm_lm_head", dt, EPI_STORE_F32, B, V, H, nbuf, H, shared.lm_head, zl, (long)k * V, part, s);
+    launch_row_stats("draft_row_stats", zl, (long)k * V, B, V, inv_t, stat, s);
     launch_draft_select(B, V, mode, inv_t, zl, (long)k * V, stat, u_draft ? u_draft + j : nullptr, k, drafts + j, k,
                         sel, s);
-    if (mode == GM_SAMPLE) launch_residual_draw(B, V, inv_t, sel, wsum, psum, s);
+    if (mode == GM_SAMPLE) launch_residual_draw("draft_residual_chunk", "draft_residual_scan", B, V, inv_t, sel, wsum, psum, s);
   };
 
   // ---- extend: rows (h_{m+i}, x_{m+i+1}), i = 0..n_b, at slots m_b + i
   launch_mtp_input(dt, Me, H, V, cfg.rms_eps, verify_hidden, out_tokens, 1, shared.embed, mtp.norm_h, mtp.norm_e, u,
                    dev_err, s);
-  launch_gemm("mtp_gemm_proj", dt, EPI_STORE_F32, Me, H, 2 * H, u, 2 * H, mtp.w_proj, x, H, s);
+  launch_gemm("mtp_gemm_proj", dt, EPI_STORE_F32, Me, H, 2 * H, u, 2 * H, mtp.w_proj, x, H, part, s);
   launch_rmsnorm(dt, Me, H, cfg.rms_eps, x, L.attn_norm, nbuf, s);
-  launch_gemm("mtp_gemm_qkv", dt, EPI_STORE_F32, Me, qw, H, nbuf, H, L.w_qkv, qkv, qw, s);
+  launch_gemm("mtp_gemm_qkv", dt, EPI_STORE_F32, Me, qw, H, nbuf, H, L.w_qkv, qkv, qw, part, s);
   launch_rope_append(rope_args(cfg, c, 0, Me, R, qkv, q, lens, 0, n_accept, 1, L, dev_err), s);
   {
     AttnArgs a = attn_args(cfg, c, 0, B, R, lens, 0, n_accept);
     a.blk_len_add = 1;
+    a.trace = "attn_mtp";
+    a.trace_combine = "attn_mtp_combine";
     a.q = q;
     a.out = attn;
     a.dev_err = dev_err;
@@ -176,11 +201,13 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
   for (int j = 1; j < k; ++j) {
     launch_mtp_input(dt, B, H, V, cfg.rms_eps, xg, drafts + (j - 1), k, shared.embed, mtp.norm_h, mtp.norm_e, u,
                      dev_err, s);
-    launch_gemm("mtp_gemm_proj", dt, EPI_STORE_F32, B, H, 2 * H, u, 2 * H, mtp.w_proj, xg, H, s);
+    launch_gemm("mtp_gemm_proj", dt, EPI_STORE_F32, B, H, 2 * H, u, 2 * H, mtp.w_proj, xg, H, part, s);
     launch_rmsnorm(dt, B, H, cfg.rms_eps, xg, L.attn_norm, nbuf, s);
-    launch_gemm("mtp_gemm_qkv", dt, EPI_STORE_F32, B, qw, H, nbuf, H, L.w_qkv, qkv, qw, s);
+    launch_gemm("mtp_gemm_qkv", dt, EPI_STORE_F32, B, qw, H, nbuf, H, L.w_qkv, qkv, qw, part, s);
     launch_rope_append(rope_args(cfg, c, 0, B, 1, qkv, q, lens, j - 1, nullptr, 1, L, dev_err), s);
     AttnArgs a = attn_args(cfg, c, 0, B, 1, lens, j - 1, nullptr);
+    a.trace = "attn_mtp";
+    a.trace_combine = "attn_mtp_combine";
     a.q = q;
     a.out = attn_g;
     a.dev_err = dev_err;

@@ -39,6 +39,7 @@ struct AttnArgs {
   void *out;                  // [B][R][n_heads][head_dim] model dtype
   int32_t *dev_err;
   float scale;                // 1 / sqrt(head_dim)
+  const char *trace, *trace_combine;   // kernel names for gm_trace
 };
 AttnArgs attn_args(const gm_model_config &cfg, const gm_kv_cache &c, int layer, int B, int R,
                    const int32_t *base_lens, int base_off, const int32_t *blk_len);
@@ -51,8 +52,14 @@ enum GemmEpi {
   EPI_STORE_ACT = 2,   // Y (model dtype) = acc
   EPI_SWIGLU = 3       // W = [W_gate; W_up] (2N rows); Y (model dtype)[m][n] = silu(gate) * up
 };
+struct GemmPlan {
+  int shape, Nw, n_tiles, m_tiles, k_iters, splits;
+  size_t part_bytes;   // float32 K-split partials
+};
+GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K);
+// bf16: W pre-tiled (gm.h), X row-major [M][ldx]; `part` must hold plan_gemm().part_bytes
 void launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, const void *X, int ldx,
-                 const void *W, void *Y, long ldy, hipStream_t s);
+                 const void *W, void *Y, long ldy, float *part, hipStream_t s);
 
 // ---------------------------------------------------------------- row kernels
 void launch_embed(int dtype, int M, int H, int V, const int32_t *tokens, const void *E, float *x,
@@ -84,7 +91,7 @@ void launch_gather_rows(int M_out, int R, int C, size_t elem, const void *src, c
 
 // ---------------------------------------------------------------- orchestration
 struct ForwardPlan {
-  size_t nbuf, act, qkv, q, attn, attn_ws, total;
+  size_t nbuf, act, qkv, q, attn, attn_ws, part, total;
   AttnPlan attn_plan;
 };
 ForwardPlan plan_forward(const gm_model_config &cfg, int B, int k, int max_ctx);
@@ -93,7 +100,7 @@ void run_verify_forward(const gm_model_config &cfg, const gm_model_weights &w, c
                         int32_t *dev_err, hipStream_t s);
 
 struct MtpPlan {
-  size_t u, x, xg, nbuf, act, qkv, q, attn, attn_g, attn_ws, stat, sel, wsum, psum, total;
+  size_t u, x, xg, nbuf, act, qkv, q, attn, attn_g, attn_ws, stat, sel, wsum, psum, part, total;
   AttnPlan attn_ext, attn_chain;
 };
 MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx);

@@ -1,148 +1,209 @@
 // Dense layers of the verify forward and the draft head: Y[M,N] = X[M,K] W[N,K]^T.
 //
-// bf16 path: 256 threads, 128-column (or 64 SwiGLU features) x BM-row tiles,
-// k-steps of 64 staged through LDS with the next step's global loads in
-// flight, v_mfma_f32_16x16x32_bf16 with float32 accumulation.  The tile order
-// is XCD-aware: workgroups are dealt to the 8 XCDs round-robin, so the
-// logical tile index is remapped such that the M-tiles that share a weight
-// tile run on the same XCD and hit its L2.  Epilogues: float32 store, float32
-// residual add in place, store in the model dtype, or SwiGLU (gate and up
-// columns of the same features computed by the same lanes).
-// float32 path: a plain LDS-tiled FMA kernel.
+// bf16 path ("streaming" GEMM for M <= 256 rows per tile, the regime of a
+// verify step: every weight byte is read once and used for all M rows).
+//  * Weights are stored pre-tiled (gm.h): tiles of 16 rows x 32 k (1 KiB)
+//    laid out so that one 16-byte-per-lane load of a wave is the B operand of
+//    v_mfma_f32_16x16x32_bf16.  A wave streams its strips of 16 rows along K
+//    as consecutive 1 KiB tiles, straight from HBM into registers, through a
+//    prefetch ring several k-steps deep; W never touches LDS.
+//  * Activations (small, L2-resident) are staged in LDS in 32 KiB chunks,
+//    double-buffered, one barrier per chunk, shared by the 4 waves.
+//  * Small N is split along K (deterministic two-pass reduction: float32
+//    partials, then a reduce kernel that sums the splits in order and applies
+//    the epilogue) so that a launch fills the 256 CUs.
+//  * Tile order is XCD-aware: the M tiles and K splits of one weight strip are
+//    dealt to the same XCD, so a weight strip re-read by several M tiles hits
+//    that XCD's L2.
+//  * Epilogues: float32 store, float32 residual add in place, store in the
+//    model dtype, SwiGLU (gate and up strips of the same features sit in the
+//    same wave, so silu(gate) * up is formed in registers).
+// float32 path: a plain LDS-tiled FMA kernel on row-major weights.
 #include "common.h"
 #include "forward.h"
 
 namespace gm {
 
 namespace {
-struct GemmK {
+struct GemmS {
   const uint16_t *X, *W;
   void *Y;
+  float *part;        // [splits][M][Nw] float32 partials when splits > 1
   long ldy;
-  int M, N, K, ldx, n_m, n_n;
+  int M, N, K, ldx;   // N: output columns (features for SwiGLU); Nw: weight rows
+  int Nw, n_tiles, m_tiles, splits, k_iters;
 };
-
-constexpr int kBN = 128, kBK = 64, kLds = kBK + 8;
-
-__device__ __forceinline__ void tile_of(int bid, int n_m, int n_n, int &tm, int &tn) {
-  const int T = n_m * n_n;
-  const int x = bid & 7, slot = bid >> 3, q = T >> 3, rem = T & 7;
-  const int L = x * q + (x < rem ? x : rem) + slot;
-  tm = L % n_m;
-  tn = L / n_m;
-}
 
 __device__ __forceinline__ float silu(float x) { return x / (1.f + expf(-x)); }
 
-template <int BM, int EPI>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmK g) {
-  __shared__ uint16_t As[BM][kLds];
-  __shared__ uint16_t Bs[kBN][kLds];
-  constexpr int TM = BM / 32;              // 16-row MFMA tiles per wave (waves 2 x 2)
-  constexpr int AL = BM * 8 / 256;         // 16-byte A chunks per thread and k-step
-  constexpr int BL = kBN * 8 / 256;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 1, wn = w & 1;
+// logical tile index of workgroup `bid`: workgroups are dealt round-robin to
+// the 8 XCDs; consecutive logical indices (same weight strip) share an XCD
+__device__ __forceinline__ int xcd_remap(int bid, int T) {
+  const int x = bid & 7, slot = bid >> 3, q = T >> 3, rem = T & 7;
+  return x * q + (x < rem ? x : rem) + slot;
+}
+
+// MT: 16-row tiles per wave; NT: 16-column strips per wave; WM: waves along M (1 or 2)
+template <int MT, int NT, int WM, int EPI>
+__global__ __launch_bounds__(256) void gemm_stream_kernel(GemmS g) {
+  constexpr int WN = 4 / WM;
+  constexpr int BM = 16 * MT * WM;            // rows per workgroup
+  constexpr int BKA = 16384 / BM;             // k per LDS chunk of A (32 KiB)
+  constexpr int SPC = BKA / 32;               // k32 steps per chunk
+  constexpr int D = NT >= 4 ? 4 : 8;          // W prefetch depth (k32 steps)
+  constexpr int ITER = D > SPC ? D : SPC;     // k32 steps per unrolled iteration
+  constexpr int LDA = BKA + 8;
+  constexpr int AL = BM * BKA / 8 / 256;      // 16-byte A loads per thread per chunk
+  static_assert(ITER % SPC == 0 && ITER % D == 0, "unroll must cover whole chunks and ring turns");
+  __shared__ uint16_t As[2][BM * LDA];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w % WM, wn = w / WM;
   const int j = lane & 15, g4 = lane >> 4;
-  int tm, tn;
-  tile_of(blockIdx.x, g.n_m, g.n_n, tm, tn);
-  const int m0 = tm * BM;
+  const int T = g.n_tiles * g.m_tiles * g.splits;
+  const int L = xcd_remap(blockIdx.x, T);
+  const int mt = L % g.m_tiles, rest = L / g.m_tiles;
+  const int ks = rest % g.splits, nt = rest / g.splits;
+  const int m0 = mt * BM;
+  // this split's k range, in whole unrolled iterations
+  const int it0 = (int)((long)g.k_iters * ks / g.splits), it1 = (int)((long)g.k_iters * (ks + 1) / g.splits);
+  const int k_begin = it0 * ITER * 32, k_end = it1 * ITER * 32;
+  const int nsteps = (k_end - k_begin) / 32;
 
-  // source rows of this thread's loads
-  const uint16_t *asrc[AL];
-  bool aval[AL];
+  // weight strips of this wave: strip index (16-row groups of W)
+  int strip[NT];
 #pragma unroll
-  for (int u = 0; u < AL; ++u) {
-    const int c = tid + 256 * u, row = c >> 3, kc = c & 7;
-    aval[u] = m0 + row < g.M;
-    asrc[u] = g.X + (long)(aval[u] ? m0 + row : 0) * g.ldx + kc * 8;
-  }
-  const uint16_t *bsrc[BL];
-#pragma unroll
-  for (int u = 0; u < BL; ++u) {
-    const int c = tid + 256 * u, row = c >> 3, kc = c & 7;
-    long wrow;
+  for (int t = 0; t < NT; ++t) {
     if (EPI == EPI_SWIGLU) {
-      const int half = row >> 6, within = row & 63, f0 = tn * 64 + half * 32;
-      wrow = within < 32 ? f0 + within : (long)g.N + f0 + within - 32;
+      // NT/2 gate strips then the NT/2 up strips of the same 16 * NT/2 features
+      const int f_strip = (nt * WN + wn) * (NT / 2) + (t % (NT / 2));
+      strip[t] = (t < NT / 2) ? f_strip : g.N / 16 + f_strip;
     } else {
-      wrow = (long)tn * kBN + row;
+      strip[t] = (nt * WN + wn) * NT + t;
     }
-    bsrc[u] = g.W + wrow * g.K + kc * 8;
   }
+  const int kt_total = g.K / 32;
+  const uint16_t *wbase[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) wbase[t] = g.W + ((long)strip[t] * kt_total + k_begin / 32) * 512 + lane * 8;
 
-  floatx4_t acc[TM][4];
-#pragma unroll
-  for (int a = 0; a < TM; ++a)
-#pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-
-  uint4 ra[AL], rb[BL];
-#pragma unroll
-  for (int u = 0; u < AL; ++u) ra[u] = aval[u] ? *reinterpret_cast<const uint4 *>(asrc[u]) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-  for (int u = 0; u < BL; ++u) rb[u] = *reinterpret_cast<const uint4 *>(bsrc[u]);
-
-  for (int k0 = 0; k0 < g.K; k0 += kBK) {
-    __syncthreads();
+  // A chunk loader
+  uint4 ra[AL];
+  auto load_a = [&](int chunk_k) {
 #pragma unroll
     for (int u = 0; u < AL; ++u) {
-      const int c = tid + 256 * u;
-      *reinterpret_cast<uint4 *>(&As[c >> 3][(c & 7) * 8]) = ra[u];
+      const int c = tid + 256 * u, row = c / (BKA / 8), col = (c % (BKA / 8)) * 8;
+      ra[u] = (m0 + row < g.M) ? *reinterpret_cast<const uint4 *>(g.X + (long)(m0 + row) * g.ldx + chunk_k + col)
+                               : make_uint4(0, 0, 0, 0);
     }
+  };
+  auto store_a = [&](int buf) {
 #pragma unroll
-    for (int u = 0; u < BL; ++u) {
-      const int c = tid + 256 * u;
-      *reinterpret_cast<uint4 *>(&Bs[c >> 3][(c & 7) * 8]) = rb[u];
+    for (int u = 0; u < AL; ++u) {
+      const int c = tid + 256 * u, row = c / (BKA / 8), col = (c % (BKA / 8)) * 8;
+      *reinterpret_cast<uint4 *>(&As[buf][row * LDA + col]) = ra[u];
     }
+  };
+
+  floatx4_t acc[MT][NT];
+#pragma unroll
+  for (int a = 0; a < MT; ++a)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[a][t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  // prime the weight ring and the first A chunk
+  uint4 ring[D][NT];
+#pragma unroll
+  for (int s = 0; s < D; ++s)
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      ring[s][t] = s < nsteps ? *reinterpret_cast<const uint4 *>(wbase[t] + (long)s * 512) : make_uint4(0, 0, 0, 0);
+  if (nsteps > 0) {
+    load_a(k_begin);
+    store_a(0);
     __syncthreads();
-    if (k0 + kBK < g.K) {
-#pragma unroll
-      for (int u = 0; u < AL; ++u)
-        ra[u] = aval[u] ? *reinterpret_cast<const uint4 *>(asrc[u] + k0 + kBK) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-      for (int u = 0; u < BL; ++u) rb[u] = *reinterpret_cast<const uint4 *>(bsrc[u] + k0 + kBK);
-    }
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      bf16x8_t af[TM], bfr[4];
-#pragma unroll
-      for (int a = 0; a < TM; ++a)
-        af[a] = as_bf16x8(*reinterpret_cast<const uint4 *>(&As[wm * (BM / 2) + 16 * a + j][kk * 32 + 8 * g4]));
-#pragma unroll
-      for (int b = 0; b < 4; ++b)
-        bfr[b] = as_bf16x8(*reinterpret_cast<const uint4 *>(&Bs[wn * 64 + 16 * b + j][kk * 32 + 8 * g4]));
-#pragma unroll
-      for (int a = 0; a < TM; ++a)
-#pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
-    }
+    if (SPC < nsteps) load_a(k_begin + BKA);
   }
 
-  // lane holds C[row 16a + 4 g4 + r][col 16b + j] of the wave tile
+  for (int s0 = 0; s0 < nsteps; s0 += ITER) {
 #pragma unroll
-  for (int a = 0; a < TM; ++a) {
+    for (int u = 0; u < ITER; ++u) {
+      const int s = s0 + u;                 // global k32 step
+      const int buf = (s / SPC) & 1;
+      const int ko = (u % SPC) * 32;        // offset inside the chunk
+      uint4 wv[NT];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = m0 + wm * (BM / 2) + 16 * a + 4 * g4 + r;
-      if (m >= g.M) continue;
-      if (EPI == EPI_SWIGLU) {
-        uint16_t *y = (uint16_t *)g.Y + (long)m * g.ldy;
+      for (int t = 0; t < NT; ++t) {
+        wv[t] = ring[u % D][t];
+        if (s + D < nsteps) ring[u % D][t] = *reinterpret_cast<const uint4 *>(wbase[t] + (long)(s + D) * 512);
+      }
+      bf16x8_t af[MT];
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
-          const int f = tn * 64 + wn * 32 + 16 * b + j;
-          y[f] = f32_to_bf16(silu(acc[a][b][r]) * acc[a][b + 2][r]);
-        }
-      } else {
+      for (int a = 0; a < MT; ++a)
+        af[a] = as_bf16x8(*reinterpret_cast<const uint4 *>(&As[buf][(wm * 16 * MT + 16 * a + j) * LDA + ko + 8 * g4]));
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const int n = tn * kBN + wn * 64 + 16 * b + j;
-          const float v = acc[a][b][r];
-          if (EPI == EPI_STORE_F32) ((float *)g.Y)[(long)m * g.ldy + n] = v;
-          else if (EPI == EPI_ADD_F32) ((float *)g.Y)[(long)m * g.ldy + n] += v;
-          else ((uint16_t *)g.Y)[(long)m * g.ldy + n] = f32_to_bf16(v);
+      for (int a = 0; a < MT; ++a)
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], as_bf16x8(wv[t]), acc[a][t], 0, 0, 0);
+      if ((u % SPC) == SPC - 1) {           // end of an A chunk: rotate the double buffer
+        const int next = s + 1;             // first step of the next chunk
+        if (next < nsteps) {
+          store_a(buf ^ 1);
+          __syncthreads();
+          if (next + SPC < nsteps) load_a(k_begin + (next + SPC) * 32);
         }
       }
     }
+  }
+
+  // lane holds C[row 16a + 4 g4 + r][col 16t + j] of the wave tile
+#pragma unroll
+  for (int a = 0; a < MT; ++a) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = m0 + wm * 16 * MT + 16 * a + 4 * g4 + r;
+      if (m >= g.M) continue;
+      if (g.splits > 1) {
+        float *p = g.part + ((long)ks * g.M + m) * g.Nw;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) p[strip[t] * 16 + j] = acc[a][t][r];
+      } else if (EPI == EPI_SWIGLU) {
+        uint16_t *y = (uint16_t *)g.Y + (long)m * g.ldy;
+#pragma unroll
+        for (int t = 0; t < NT / 2; ++t)
+          y[strip[t] * 16 + j] = f32_to_bf16(silu(acc[a][t][r]) * acc[a][t + NT / 2][r]);
+      } else {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const long o = (long)m * g.ldy + strip[t] * 16 + j;
+          const float v = acc[a][t][r];
+          if (EPI == EPI_STORE_F32) ((float *)g.Y)[o] = v;
+          else if (EPI == EPI_ADD_F32) ((float *)g.Y)[o] += v;
+          else ((uint16_t *)g.Y)[o] = f32_to_bf16(v);
+        }
+      }
+    }
+  }
+}
+
+// sum of the K-split partials in split order, then the epilogue
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmS g) {
+  const long total = (long)g.M * g.N;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
+    const int m = (int)(i / g.N), n = (int)(i % g.N);
+    float a = 0.f, b = 0.f;
+    for (int s = 0; s < g.splits; ++s) {
+      const float *p = g.part + ((long)s * g.M + m) * g.Nw;
+      a += p[n];
+      if (EPI == EPI_SWIGLU) b += p[g.N + n];
+    }
+    const long o = (long)m * g.ldy + n;
+    if (EPI == EPI_STORE_F32) ((float *)g.Y)[o] = a;
+    else if (EPI == EPI_ADD_F32) ((float *)g.Y)[o] += a;
+    else if (EPI == EPI_SWIGLU) ((uint16_t *)g.Y)[o] = f32_to_bf16(silu(a) * b);
+    else ((uint16_t *)g.Y)[o] = f32_to_bf16(a);
   }
 }
 
@@ -195,31 +256,80 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF g) {
     else *y = acc[0][q];
   }
 }
+
+template <int MT, int NT, int WM, int EPI>
+void launch_stream(const GemmS &g, hipStream_t s) {
+  hipLaunchKernelGGL((gemm_stream_kernel<MT, NT, WM, EPI>), dim3(g.n_tiles * g.m_tiles * g.splits), dim3(256), 0, s, g);
+}
+
+template <int EPI>
+void launch_stream_shape(int shape, const GemmS &g, hipStream_t s) {
+  switch (shape) {
+    case 0: launch_stream<4, 2, 1, EPI>(g, s); break;   // M <= 64:  64 x 128 tiles
+    case 1: launch_stream<8, 2, 1, EPI>(g, s); break;   // M <= 128: 128 x 128 tiles
+    default: launch_stream<8, 4, 2, EPI>(g, s); break;  // M > 128:  256 x 128 tiles
+  }
+}
 }  // namespace
 
+// Tile shape and K split.  Every launch streams each weight byte from HBM
+// once; the choices trade workgroup count (to keep the CUs streaming) against
+// extra traffic:
+//  * wide outputs (>= 256 column tiles, e.g. the LM head) take the largest M
+//    tile, so weight strips are fetched once per 256 rows;
+//  * narrow outputs use 64-row tiles, several M tiles of one strip served
+//    from the XCD's L2, plus a K split capped so that the float32 partials
+//    move at most half as many bytes as the weights.
+GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
+  GemmPlan p{};
+  if (dtype != GM_BF16 || M <= 0) return p;
+  const int cols = 128;                             // weight rows per workgroup
+  p.Nw = epi == EPI_SWIGLU ? 2 * N : N;
+  p.n_tiles = p.Nw / cols;
+  const int target = 256;                           // workgroups that keep every CU streaming
+  if (M <= 64 || p.n_tiles < target) p.shape = 0;
+  else p.shape = M <= 128 ? 1 : 2;
+  const int BM = p.shape == 0 ? 64 : (p.shape == 1 ? 128 : 256);
+  const int ITER = p.shape == 2 ? 4 : 8;            // k32 steps per unrolled iteration (see kernel)
+  p.m_tiles = (M + BM - 1) / BM;
+  p.k_iters = K / (ITER * 32);
+  int splits = (target + p.n_tiles * p.m_tiles - 1) / (p.n_tiles * p.m_tiles);
+  const int cap = K / (8 * M);                      // 2 * S * M * Nw * 4 <= Nw * K * 2 / 2
+  if (splits > cap) splits = cap;
+  if (splits > p.k_iters) splits = p.k_iters;
+  if (splits < 1) splits = 1;
+  p.splits = splits;
+  p.part_bytes = splits > 1 ? (size_t)splits * M * p.Nw * sizeof(float) : 0;
+  return p;
+}
+
 void launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, const void *X, int ldx, const void *W,
-                 void *Y, long ldy, hipStream_t s) {
+                 void *Y, long ldy, float *part, hipStream_t s) {
   if (M <= 0) return;
   if (dtype == GM_BF16) {
-    GemmK g{(const uint16_t *)X, (const uint16_t *)W, Y, ldy, M, N, K, ldx, 0, 0};
-    const bool small = M <= 64;
-    const int BM = small ? 64 : 128;
-    g.n_m = (M + BM - 1) / BM;
-    g.n_n = epi == EPI_SWIGLU ? N / 64 : N / kBN;
-    const dim3 grid(g.n_m * g.n_n), block(256);
-    TraceScope ts(name, s);
-#define GM_GEMM_CASE(E)                                                                   \
-  case E:                                                                                 \
-    if (small) hipLaunchKernelGGL((gemm_bf16_kernel<64, E>), grid, block, 0, s, g);       \
-    else hipLaunchKernelGGL((gemm_bf16_kernel<128, E>), grid, block, 0, s, g);            \
-    break;
-    switch (epi) {
-      GM_GEMM_CASE(EPI_STORE_F32)
-      GM_GEMM_CASE(EPI_ADD_F32)
-      GM_GEMM_CASE(EPI_STORE_ACT)
-      GM_GEMM_CASE(EPI_SWIGLU)
+    const GemmPlan p = plan_gemm(dtype, epi, M, N, K);
+    GemmS g{(const uint16_t *)X, (const uint16_t *)W, Y, part, ldy, M, N, K, ldx, p.Nw, p.n_tiles, p.m_tiles,
+            p.splits, p.k_iters};
+    {
+      TraceScope ts(name, s);
+      switch (epi) {
+        case EPI_STORE_F32: launch_stream_shape<EPI_STORE_F32>(p.shape, g, s); break;
+        case EPI_ADD_F32: launch_stream_shape<EPI_ADD_F32>(p.shape, g, s); break;
+        case EPI_STORE_ACT: launch_stream_shape<EPI_STORE_ACT>(p.shape, g, s); break;
+        case EPI_SWIGLU: launch_stream_shape<EPI_SWIGLU>(p.shape, g, s); break;
+      }
     }
-#undef GM_GEMM_CASE
+    if (p.splits > 1) {
+      TraceScope ts("gemm_split_reduce", s);
+      const long total = (long)M * N;
+      const int blocks = (int)((total + 255) / 256 < 2048 ? (total + 255) / 256 : 2048);
+      switch (epi) {
+        case EPI_STORE_F32: hipLaunchKernelGGL(gemm_reduce_kernel<EPI_STORE_F32>, dim3(blocks), dim3(256), 0, s, g); break;
+        case EPI_ADD_F32: hipLaunchKernelGGL(gemm_reduce_kernel<EPI_ADD_F32>, dim3(blocks), dim3(256), 0, s, g); break;
+        case EPI_STORE_ACT: hipLaunchKernelGGL(gemm_reduce_kernel<EPI_STORE_ACT>, dim3(blocks), dim3(256), 0, s, g); break;
+        case EPI_SWIGLU: hipLaunchKernelGGL(gemm_reduce_kernel<EPI_SWIGLU>, dim3(blocks), dim3(256), 0, s, g); break;
+      }
+    }
   } else {
     GemmF g{(const float *)X, (const float *)W, (float *)Y, ldy, M, N, K, ldx};
     const dim3 grid((N + 63) / 64, (M + 15) / 16), block(256);

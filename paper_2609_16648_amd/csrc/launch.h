@@ -44,7 +44,7 @@ constexpr int kScanChunk = kScanThreads * kScanPer;           // 4096 ids per ch
 inline int stat_chunks(int V) { return (V + kStatChunk - 1) / kStatChunk; }
 inline int scan_chunks(int V) { return (V + kScanChunk - 1) / kScanChunk; }
 
-void launch_row_stats(const float *logits, long row_stride, int n_rows, int V, float inv_t,
+void launch_row_stats(const char *name, const float *logits, long row_stride, int n_rows, int V, float inv_t,
                       RowStat *out, hipStream_t s);
 void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const float *tlog,
                           const float *dlog, const RowStat *tstat, const RowStat *dstat,
@@ -53,7 +53,7 @@ void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const floa
 void launch_draft_select(int B, int V, int mode, float inv_t, const float *dlog, long row_stride,
                          const RowStat *stat, const float *u, int u_stride, int32_t *dst,
                          int dst_stride, RowSel *sel, hipStream_t s);
-void launch_residual_draw(int B, int V, float inv_t, const RowSel *sel, double *wsum,
+void launch_residual_draw(const char *chunk_name, const char *scan_name, int B, int V, float inv_t, const RowSel *sel, double *wsum,
                           double *psum, hipStream_t s);
 
 // ---------------------------------------------------------------- KV index

@@ -87,10 +87,10 @@ __global__ __launch_bounds__(kStatThreads) void row_stats_kernel(const float *__
   }
 }
 
-void launch_row_stats(const float *logits, long row_stride, int n_rows, int V, float inv_t,
+void launch_row_stats(const char *name, const float *logits, long row_stride, int n_rows, int V, float inv_t,
                       RowStat *out, hipStream_t s) {
   if (n_rows <= 0) return;
-  TraceScope ts("row_stats", s);
+  TraceScope ts(name, s);
   dim3 grid(n_rows, stat_chunks(V));
   hipLaunchKernelGGL(row_stats_kernel, grid, dim3(kStatThreads), 0, s, logits, row_stride, V, inv_t,
                      stat_chunks(V), out);
@@ -333,16 +333,16 @@ __global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, floa
   }
 }
 
-void launch_residual_draw(int B, int V, float inv_t, const RowSel *sel, double *wsum, double *psum,
+void launch_residual_draw(const char *chunk_name, const char *scan_name, int B, int V, float inv_t, const RowSel *sel, double *wsum, double *psum,
                           hipStream_t s) {
   const int nch = scan_chunks(V);
   {
-    TraceScope ts("residual_chunk", s);
+    TraceScope ts(chunk_name, s);
     hipLaunchKernelGGL(residual_chunk_kernel, dim3(B, nch), dim3(kScanThreads), 0, s, V, inv_t, sel, nch,
                        wsum, psum);
   }
   {
-    TraceScope ts("residual_scan", s);
+    TraceScope ts(scan_name, s);
     hipLaunchKernelGGL(residual_scan_kernel, dim3(B), dim3(kScanThreads), 0, s, V, inv_t, sel, nch, wsum,
                        psum);
   }

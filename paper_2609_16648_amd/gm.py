@@ -152,6 +152,12 @@ def _dev(a: np.ndarray, dtype, device) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device=device, dtype=dtype)
 
 
+def _dev_linear(a: np.ndarray, dtype, device) -> torch.Tensor:
+    """A linear weight in the layout gm.h gives its dtype: tiled for bf16, row-major for float32."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    return _dev(layout.tile_weight(a) if dtype == torch.bfloat16 else a, dtype, device)
+
+
 class DeviceLayer:
     """One decoder layer's weights on the device, packed as gm.h lays them out."""
 
@@ -159,11 +165,11 @@ class DeviceLayer:
         dt = torch_dtype(shape)
         self.t = {
             "attn_norm": _dev(w["attn_norm"], dt, device),
-            "w_qkv": _dev(np.concatenate([w["wq"], w["wk"], w["wv"]], 0), dt, device),
-            "w_o": _dev(w["wo"], dt, device),
+            "w_qkv": _dev_linear(np.concatenate([w["wq"], w["wk"], w["wv"]], 0), dt, device),
+            "w_o": _dev_linear(w["wo"], dt, device),
             "ffn_norm": _dev(w["ffn_norm"], dt, device),
-            "w_gate_up": _dev(np.concatenate([w["w_gate"], w["w_up"]], 0), dt, device),
-            "w_down": _dev(w["w_down"], dt, device),
+            "w_gate_up": _dev_linear(np.concatenate([w["w_gate"], w["w_up"]], 0), dt, device),
+            "w_down": _dev_linear(w["w_down"], dt, device),
         }
         if shape.qk_norm:
             self.t["q_norm"] = _dev(w["q_norm"], dt, device)
@@ -183,7 +189,11 @@ class DeviceModel:
         self.cfg = model_config(shape)
         dt = torch_dtype(shape)
         self.embed = _dev(w["embed"], dt, device)
-        self.lm_head = self.embed if w["lm_head"] is w["embed"] else _dev(w["lm_head"], dt, device)
+        # the LM head is a linear weight (tiled for bf16), the embedding a row-major table
+        if w["lm_head"] is w["embed"] and dt != torch.bfloat16:
+            self.lm_head = self.embed
+        else:
+            self.lm_head = _dev_linear(w["lm_head"], dt, device)
         self.final_norm = _dev(w["final_norm"], dt, device)
         self.layers = [DeviceLayer(shape, L, device) for L in w["layers"]]
         self._layer_arr = (LayerWeights * len(self.layers))(*[L.struct() for L in self.layers])
@@ -198,7 +208,7 @@ class DeviceMtp:
         dt = torch_dtype(shape)
         self.norm_h = _dev(w["norm_h"], dt, device)
         self.norm_e = _dev(w["norm_e"], dt, device)
-        self.w_proj = _dev(w["w_proj"], dt, device)
+        self.w_proj = _dev_linear(w["w_proj"], dt, device)
         self.final_norm = _dev(w["final_norm"], dt, device)
         self.layer = DeviceLayer(shape, w["layer"], device)
         self.struct = MtpWeights(_ptr(self.norm_h), _ptr(self.norm_e), _ptr(self.w_proj), _ptr(self.final_norm),

@@ -162,3 +162,18 @@ def test_scatter_gather_round_trip():
     layout.scatter(pool, ent, pos, table[1], page_size, "v")
     np.testing.assert_array_equal(layout.gather(pool, pos, table[1], page_size, n_kv, d, "v"), ent)
     assert (table[0, 3:] == -1).all() and sorted(table[table >= 0].tolist()) == list(range(8))
+
+
+def test_weight_tiling_matches_header_formula():
+    g = np.random.default_rng(1)
+    n, k = 48, 96
+    w = g.standard_normal((n, k)).astype(np.float32)
+    flat = layout.tile_weight(w)
+    r, c = np.meshgrid(np.arange(n), np.arange(k), indexing="ij")
+    off = ((r // 16) * (k // 32) + c // 32) * 512 + ((c % 32) // 8) * 128 + (r % 16) * 8 + c % 8
+    np.testing.assert_array_equal(flat[off], w)
+    np.testing.assert_array_equal(layout.untile_weight(flat, n, k), w)
+    # one 16-byte load per lane at lane * 8 of a tile: row lane % 16, columns 8 (lane // 16) .. +7
+    t = flat[:512].reshape(64, 8)
+    for lane in range(64):
+        np.testing.assert_array_equal(t[lane], w[lane % 16, 8 * (lane // 16): 8 * (lane // 16) + 8])

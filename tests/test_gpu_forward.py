@@ -112,3 +112,20 @@ def test_qwen_layer_bf16_forward(qwen_layer):
     np.testing.assert_array_equal(out[ok], ref.out_tokens[ok])
     tau = 1 + n.mean()
     print("[forward+greedy qwen3 layer] tau %.3f (0.7 mixing predicts %.3f)" % (tau, (1 - 0.7 ** 4) / 0.3), flush=True)
+
+
+def test_qwen_layer_bf16_forward_mid_batch(qwen_layer):
+    # 24 sequences: M = 96 block rows takes the 128-row GEMM tile on the LM head and
+    # 64-row tiles with K splits on the narrow projections
+    need_gpu()
+    wl, shape, W, lens, caches, tokens = qwen_layer
+    B, k = 24, wl.k
+    lens, tokens = lens[:B], tokens[:B]
+    caches = [(ks[:B], vs[:B]) for ks, vs in caches]
+    model = gm.DeviceModel(shape, W)
+    cache = device_cache(shape, caches, lens, k + 1, page_size=32)
+    logits, hidden = _gpu_forward(model, cache, tokens)
+    ref_c, ref_hc, _ = oracle.verify_forward(shape, W, caches, tokens, lens, CONTRACT)
+    print("[forward qwen3 layer bf16 B=24] logits rel err vs contract %.3e, hidden %.3e"
+          % (rel_err(logits, ref_c), rel_err(hidden, ref_hc)), flush=True)
+    assert rel_err(logits, ref_c) < 1e-2 and rel_err(hidden, ref_hc) < 1e-2

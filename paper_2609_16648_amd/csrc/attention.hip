@@ -41,6 +41,68 @@ __device__ __forceinline__ int block_rows(const int32_t *blen, int add, int b, i
 
 __device__ __forceinline__ uint32_t zero_half(uint32_t v, int hi) { return hi ? (v & 0x0000ffffu) : (v & 0xffff0000u); }
 
+// One 16-token tile: S^T = K Q^T, online softmax (exp2 domain, rescale only when
+// a row's running max grows), O^T += V^T (P_hi + P_lo).
+template <int NT, bool TAIL>
+__device__ __forceinline__ void attn_tile(int tb, int L, int g, float scale_log2, uint4 (&kc)[4], uint4 (&vc)[4],
+                                          const bf16x8_t (&qf)[NT][4], const int (&vis)[NT], float (&mrow)[NT],
+                                          float (&lsum)[NT], floatx4_t (&O)[NT][8]) {
+  if (TAIL) {  // tail tile: entries past the context may hold anything, keep them out of P.V
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (tb + 4 * g + e >= L) {
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          if (e < 2) { vc[p].x = zero_half(vc[p].x, e); vc[p].z = zero_half(vc[p].z, e); }
+          else { vc[p].y = zero_half(vc[p].y, e - 2); vc[p].w = zero_half(vc[p].w, e - 2); }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    floatx4_t S = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) S = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kc[ii]), qf[nt][ii], S, 0, 0, 0);
+    float s[4], tmax = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int tok = tb + 4 * g + r;
+      s[r] = tok < vis[nt] ? S[r] * scale_log2 : -INFINITY;
+      tmax = fmaxf(tmax, s[r]);
+    }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
+    const float mnew = fmaxf(mrow[nt], tmax);
+    const bool grow = mnew > mrow[nt];
+    if (__any(grow)) {
+      const float alpha = grow ? exp2f(mrow[nt] - mnew) : 1.f;
+      lsum[nt] *= alpha;
+#pragma unroll
+      for (int mm = 0; mm < 8; ++mm) O[nt][mm] *= alpha;
+    }
+    mrow[nt] = mnew;
+    const bool none = mnew == -INFINITY;
+    uint16_t hi[4], lo[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float p = none ? 0.f : exp2f(s[r] - mnew);
+      lsum[nt] += p;
+      hi[r] = f32_to_bf16(p);
+      lo[r] = f32_to_bf16(p - bf16_to_f32(hi[r]));
+    }
+    const uint2 phi = make_uint2(hi[0] | (uint32_t(hi[1]) << 16), hi[2] | (uint32_t(hi[3]) << 16));
+    const uint2 plo = make_uint2(lo[0] | (uint32_t(lo[1]) << 16), lo[2] | (uint32_t(lo[3]) << 16));
+#pragma unroll
+    for (int mm = 0; mm < 8; ++mm) {
+      const uint4 &v4 = vc[mm >> 1];
+      const uint2 vv = (mm & 1) ? make_uint2(v4.z, v4.w) : make_uint2(v4.x, v4.y);
+      O[nt][mm] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_bf16x4(vv), as_bf16x4(phi), O[nt][mm], 0, 0, 0);
+      O[nt][mm] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_bf16x4(vv), as_bf16x4(plo), O[nt][mm], 0, 0, 0);
+    }
+  }
+}
+
 template <int NT>
 __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnK a) {
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
@@ -81,72 +143,56 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnK a) {
     for (int mm = 0; mm < 8; ++mm) O[nt][mm] = floatx4_t{0.f, 0.f, 0.f, 0.f};
   }
 
-  const long kv_head_stride = (long)a.page_size * 128;
-  for (int tb = t0; tb < t1; tb += 16) {
-    const int pi = tb / a.page_size;
+  // The pages this split touches, looked up once into LDS: in the loop a lookup is then an
+  // LDS read, whose counter is separate from the KV loads', so no wait drains the prefetch.
+  // A page outside the pool ends the split before its first token (and is reported).
+  __shared__ int page_sh[kAttnMaxSplitPages];
+  __shared__ int bad_sh;
+  const int p0 = t0 / a.page_size, np = (t1 - 1) / a.page_size - p0 + 1;
+  if (lane == 0) bad_sh = np;
+  __syncthreads();
+  for (int i = lane; i < np; i += kWave) {
+    const int pi = p0 + i;
     const int page = pi < a.max_pages ? a.bt[(long)b * a.max_pages + pi] : -1;
-    if (page < 0 || page >= a.num_pages) {
-      raise_dev_err(a.dev_err, GM_DEVERR_PAGE);
-      break;
+    page_sh[i] = page;
+    if (page < 0 || page >= a.num_pages) atomicMin(&bad_sh, i);
+  }
+  __syncthreads();
+  int tend = t1;
+  if (bad_sh < np) {
+    raise_dev_err(a.dev_err, GM_DEVERR_PAGE);
+    tend = max(t0, (p0 + bad_sh) * a.page_size);
+  }
+  const long head_off = (long)kvh * a.page_size * 128;
+  auto tile_off = [&](int tb) -> long {
+    const int page = page_sh[tb / a.page_size - p0];
+    return (long)page * a.n_kv * a.page_size * 128 + head_off + (long)(tb % a.page_size) * 128;
+  };
+  auto load_tile = [&](long off, uint4 (&kf)[4], uint4 (&vf)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) kf[i] = *reinterpret_cast<const uint4 *>(a.kp + off + i * 512 + lane * 8);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) vf[i] = *reinterpret_cast<const uint4 *>(a.vp + off + i * 512 + lane * 8);
+  };
+  // full tiles: two register buffers, alternating, every load unconditional (the last
+  // prefetch re-reads a valid tile), so the loads of the next tile are always in flight
+  // while the current one is consumed and no register copy waits on them
+  const int full_end = min(tend, (L / 16) * 16);
+  const int n_full = full_end > t0 ? (full_end - t0) / 16 : 0;
+  uint4 ka[4], va[4], kb[4], vb[4];
+  if (n_full > 0) {
+    load_tile(tile_off(t0), ka, va);
+    for (int i = 0; i < n_full; i += 2) {
+      load_tile(tile_off(t0 + 16 * min(i + 1, n_full - 1)), kb, vb);
+      attn_tile<NT, false>(t0 + 16 * i, L, g, a.scale_log2, ka, va, qf, vis, mrow, lsum, O);
+      if (i + 1 >= n_full) break;
+      load_tile(tile_off(t0 + 16 * min(i + 2, n_full - 1)), ka, va);
+      attn_tile<NT, false>(t0 + 16 * (i + 1), L, g, a.scale_log2, kb, vb, qf, vis, mrow, lsum, O);
     }
-    const long tile = ((long)page * a.n_kv + kvh) * kv_head_stride + (long)(tb % a.page_size) * 128;
-    const uint16_t *kt = a.kp + tile, *vt = a.vp + tile;
-    uint4 kf[4], vf[4];
-#pragma unroll
-    for (int ii = 0; ii < 4; ++ii) kf[ii] = *reinterpret_cast<const uint4 *>(kt + ii * 512 + lane * 8);
-#pragma unroll
-    for (int p = 0; p < 4; ++p) vf[p] = *reinterpret_cast<const uint4 *>(vt + p * 512 + lane * 8);
-    if (tb + 16 > L) {  // tail tile: entries past the context may hold anything, keep them out of P.V
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (tb + 4 * g + e >= L) {
-#pragma unroll
-          for (int p = 0; p < 4; ++p) {
-            if (e < 2) { vf[p].x = zero_half(vf[p].x, e); vf[p].z = zero_half(vf[p].z, e); }
-            else { vf[p].y = zero_half(vf[p].y, e - 2); vf[p].w = zero_half(vf[p].w, e - 2); }
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      floatx4_t S = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ii = 0; ii < 4; ++ii) S = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf[ii]), qf[nt][ii], S, 0, 0, 0);
-      float s[4], tmax = -INFINITY;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int tok = tb + 4 * g + r;
-        s[r] = tok < vis[nt] ? S[r] * a.scale_log2 : -INFINITY;
-        tmax = fmaxf(tmax, s[r]);
-      }
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
-      const float mnew = fmaxf(mrow[nt], tmax);
-      const bool none = mnew == -INFINITY;
-      const float alpha = none ? 1.f : exp2f(mrow[nt] - mnew);
-      mrow[nt] = mnew;
-      lsum[nt] *= alpha;
-#pragma unroll
-      for (int mm = 0; mm < 8; ++mm) O[nt][mm] *= alpha;
-      uint16_t hi[4], lo[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float p = none ? 0.f : exp2f(s[r] - mnew);
-        lsum[nt] += p;
-        hi[r] = f32_to_bf16(p);
-        lo[r] = f32_to_bf16(p - bf16_to_f32(hi[r]));
-      }
-      const uint2 phi = make_uint2(hi[0] | (uint32_t(hi[1]) << 16), hi[2] | (uint32_t(hi[3]) << 16));
-      const uint2 plo = make_uint2(lo[0] | (uint32_t(lo[1]) << 16), lo[2] | (uint32_t(lo[3]) << 16));
-#pragma unroll
-      for (int mm = 0; mm < 8; ++mm) {
-        const uint4 &v4 = vf[mm >> 1];
-        const uint2 vv = (mm & 1) ? make_uint2(v4.z, v4.w) : make_uint2(v4.x, v4.y);
-        O[nt][mm] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_bf16x4(vv), as_bf16x4(phi), O[nt][mm], 0, 0, 0);
-        O[nt][mm] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_bf16x4(vv), as_bf16x4(plo), O[nt][mm], 0, 0, 0);
-      }
-    }
+  }
+  if (full_end < tend) {  // the partial tile at the end of the context
+    load_tile(tile_off(full_end), ka, va);
+    attn_tile<NT, true>(full_end, L, g, a.scale_log2, ka, va, qf, vis, mrow, lsum, O);
   }
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
@@ -171,25 +217,35 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnK a, uint16_t *__
   if (n_act > a.splits) n_act = a.splits;
   const int rows = a.G * a.R;
   const long pbase = ((long)b * a.n_kv + kvh) * a.splits * a.rows_pad;
-  for (int idx = threadIdx.x; idx < rows * 128; idx += blockDim.x) {
-    const int r = idx >> 7, d = idx & 127;
+  // 32 threads per row, four channels each
+  for (int idx = threadIdx.x; idx < rows * 32; idx += blockDim.x) {
+    const int r = idx >> 5, d = (idx & 31) * 4;
     const int hl = r / a.R, i = r % a.R;
-    float v = 0.f;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
     if (i < blen) {
       float M = -INFINITY;
       for (int s = 0; s < n_act; ++s) M = fmaxf(M, a.part_ml[pbase + (long)s * a.rows_pad + r].x);
       if (M != -INFINITY) {
-        float num = 0.f, den = 0.f;
+        float den = 0.f;
+        float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
         for (int s = 0; s < n_act; ++s) {
-          const float2 ml = a.part_ml[pbase + (long)s * a.rows_pad + r];
+          const long pr = pbase + (long)s * a.rows_pad + r;
+          const float2 ml = a.part_ml[pr];
           const float w = exp2f(ml.x - M);
+          const float4 o = *reinterpret_cast<const float4 *>(a.part_o + pr * 128 + d);
           den += ml.y * w;
-          num += a.part_o[(pbase + (long)s * a.rows_pad + r) * 128 + d] * w;
+          num.x += o.x * w;
+          num.y += o.y * w;
+          num.z += o.z * w;
+          num.w += o.w * w;
         }
-        v = num / den;
+        const float inv = 1.f / den;
+        v = make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv);
       }
     }
-    out[(((long)b * a.R + i) * a.n_heads + kvh * a.G + hl) * 128 + d] = f32_to_bf16(v);
+    const uint2 packed = make_uint2(f32_to_bf16(v.x) | (uint32_t(f32_to_bf16(v.y)) << 16),
+                                    f32_to_bf16(v.z) | (uint32_t(f32_to_bf16(v.w)) << 16));
+    *reinterpret_cast<uint2 *>(out + (((long)b * a.R + i) * a.n_heads + kvh * a.G + hl) * 128 + d) = packed;
   }
 }
 

@@ -127,10 +127,7 @@ MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx) {
   p.attn_chain = plan_attention(cfg, B, 1, max_ctx + 2 * k);
   p.attn_ws = c.take(p.attn_ext.total > p.attn_chain.total ? p.attn_ext.total : p.attn_chain.total);
   const int V = cfg.vocab;
-  p.stat = c.take(sizeof(RowStat) * (size_t)B * stat_chunks(V));
-  p.sel = c.take(sizeof(RowSel) * (size_t)B);
-  p.wsum = c.take(sizeof(double) * (size_t)B * scan_chunks(V));
-  p.psum = c.take(sizeof(double) * (size_t)B * scan_chunks(V));
+  p.stat = c.take(sizeof(RowStat) * (size_t)B * vocab_tiles(V));
   const size_t pe = part_bytes(cfg, (int)Me, true), pb = part_bytes(cfg, B, true);
   p.part = c.take(pe > pb ? pe : pb);
   p.total = c.off;
@@ -152,9 +149,7 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
   void *u = ws + p.u, *nbuf = ws + p.nbuf, *act = ws + p.act, *q = ws + p.q, *attn = ws + p.attn,
        *attn_g = ws + p.attn_g;
   float *x = (float *)(ws + p.x), *xg = (float *)(ws + p.xg), *qkv = (float *)(ws + p.qkv);
-  RowStat *stat = (RowStat *)(ws + p.stat);
-  RowSel *sel = (RowSel *)(ws + p.sel);
-  double *wsum = (double *)(ws + p.wsum), *psum = (double *)(ws + p.psum);
+  RowStat *tiles = (RowStat *)(ws + p.stat);
   float *part = (float *)(ws + p.part);
   int32_t *lens = c.seq_lens;
 
@@ -167,11 +162,11 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
     launch_gemm("mtp_gemm_down", dt, EPI_ADD_F32, B, H, F, act, F, L.w_down, x1, H, part, s);
     launch_rmsnorm(dt, B, H, cfg.rms_eps, x1, mtp.final_norm, nbuf, s);
     float *zl = draft_logits + (long)j * V;
-    launch_gemm("mtp_gemm_lm_head", dt, EPI_STORE_F32, B, V, H, nbuf, H, shared.lm_head, zl, (long)k * V, part, s);
-    launch_row_stats("draft_row_stats", zl, (long)k * V, B, V, inv_t, stat, s);
-    launch_draft_select(B, V, mode, inv_t, zl, (long)k * V, stat, u_draft ? u_draft + j : nullptr, k, drafts + j, k,
-                        sel, s);
-    if (mode == GM_SAMPLE) launch_residual_draw("draft_residual_chunk", "draft_residual_scan", B, V, inv_t, sel, wsum, psum, s);
+    // the LM head emits the logits and their softmax statistics per 128-id tile; the draw
+    // then reads only the tile statistics and one tile of logits per sequence
+    launch_gemm("mtp_gemm_lm_head", dt, EPI_STATS, B, V, H, nbuf, H, shared.lm_head, zl, (long)k * V, part, s, tiles,
+                inv_t);
+    launch_tile_draw(B, V, mode, inv_t, zl, (long)k * V, tiles, u_draft ? u_draft + j : nullptr, k, drafts + j, k, s);
   };
 
   // ---- extend: rows (h_{m+i}, x_{m+i+1}), i = 0..n_b, at slots m_b + i

@@ -7,6 +7,8 @@
 namespace gm {
 
 constexpr int kAttnMaxRows = 64;   // (n_heads / n_kv_heads) * block rows per KV head
+constexpr int kAttnMaxSplitTokens = 4096;                           // tokens per attention split
+constexpr int kAttnMaxSplitPages = kAttnMaxSplitTokens / 16 + 8;    // pages one split can touch
 
 struct Carve {
   size_t off = 0;
@@ -50,7 +52,8 @@ enum GemmEpi {
   EPI_STORE_F32 = 0,   // Y (float) = acc
   EPI_ADD_F32 = 1,     // Y (float) += acc
   EPI_STORE_ACT = 2,   // Y (model dtype) = acc
-  EPI_SWIGLU = 3       // W = [W_gate; W_up] (2N rows); Y (model dtype)[m][n] = silu(gate) * up
+  EPI_SWIGLU = 3,      // W = [W_gate; W_up] (2N rows); Y (model dtype)[m][n] = silu(gate) * up
+  EPI_STATS = 4        // Y (float) = acc, plus softmax statistics of Y / T per 128-column tile
 };
 struct GemmPlan {
   int shape, Nw, n_tiles, m_tiles, k_iters, splits;
@@ -59,7 +62,8 @@ struct GemmPlan {
 GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K);
 // bf16: W pre-tiled (gm.h), X row-major [M][ldx]; `part` must hold plan_gemm().part_bytes
 void launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, const void *X, int ldx,
-                 const void *W, void *Y, long ldy, float *part, hipStream_t s);
+                 const void *W, void *Y, long ldy, float *part, hipStream_t s,
+                 RowStat *tile_stats = nullptr, float inv_t = 1.f);
 
 // ---------------------------------------------------------------- row kernels
 void launch_embed(int dtype, int M, int H, int V, const int32_t *tokens, const void *E, float *x,
@@ -100,7 +104,7 @@ void run_verify_forward(const gm_model_config &cfg, const gm_model_weights &w, c
                         int32_t *dev_err, hipStream_t s);
 
 struct MtpPlan {
-  size_t u, x, xg, nbuf, act, qkv, q, attn, attn_g, attn_ws, stat, sel, wsum, psum, part, total;
+  size_t u, x, xg, nbuf, act, qkv, q, attn, attn_g, attn_ws, stat, part, total;
   AttnPlan attn_ext, attn_chain;
 };
 MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx);

@@ -32,6 +32,8 @@ struct GemmS {
   long ldy;
   int M, N, K, ldx;   // N: output columns (features for SwiGLU); Nw: weight rows
   int Nw, n_tiles, m_tiles, splits, k_iters;
+  RowStat *stats;     // EPI_STATS: [M][Nw / 128] tile statistics of Y / T
+  float inv_t;
 };
 
 __device__ __forceinline__ float silu(float x) { return x / (1.f + expf(-x)); }
@@ -178,11 +180,72 @@ __global__ __launch_bounds__(256) void gemm_stream_kernel(GemmS g) {
         for (int t = 0; t < NT; ++t) {
           const long o = (long)m * g.ldy + strip[t] * 16 + j;
           const float v = acc[a][t][r];
-          if (EPI == EPI_STORE_F32) ((float *)g.Y)[o] = v;
+          if (EPI == EPI_STORE_F32 || EPI == EPI_STATS) ((float *)g.Y)[o] = v;
           else if (EPI == EPI_ADD_F32) ((float *)g.Y)[o] += v;
           else ((uint16_t *)g.Y)[o] = f32_to_bf16(v);
         }
       }
+    }
+  }
+
+  if (EPI == EPI_STATS) {
+    // softmax statistics of this workgroup's 128 columns, per row: every wave
+    // reduces its own columns over the 16 lanes of a row, the waves of a row
+    // meet in LDS (A's buffers are free once the K loop is done)
+    __syncthreads();
+    float *sm = reinterpret_cast<float *>(&As[0][0]);          // [BM][WN][3]
+#pragma unroll
+    for (int a = 0; a < MT; ++a) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float vmax = -INFINITY;
+        int varg = 0x7fffffff;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const float v = acc[a][t][r] * g.inv_t;
+          const int col = strip[t] * 16 + j;
+          if (v > vmax || (v == vmax && col < varg)) { vmax = v; varg = col; }
+        }
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) {
+          const float om = __shfl_xor(vmax, o, kWave);
+          const int oa = __shfl_xor(varg, o, kWave);
+          if (om > vmax || (om == vmax && oa < varg)) { vmax = om; varg = oa; }
+        }
+        float s = 0.f;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) s += expf(acc[a][t][r] * g.inv_t - vmax);
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) s += __shfl_xor(s, o, kWave);
+        if (j == 0) {
+          float *e = sm + ((wm * 16 * MT + 16 * a + 4 * g4 + r) * WN + wn) * 3;
+          e[0] = vmax;
+          e[1] = s;
+          e[2] = __int_as_float(varg);
+        }
+      }
+    }
+    __syncthreads();
+    for (int rl = tid; rl < BM; rl += 256) {
+      const int m = m0 + rl;
+      if (m >= g.M) continue;
+      const float *e = sm + rl * WN * 3;
+      float M = e[0];
+      int arg = __float_as_int(e[2]);
+#pragma unroll
+      for (int q = 1; q < WN; ++q) {
+        const float mq = e[3 * q];
+        const int aq = __float_as_int(e[3 * q + 2]);
+        if (mq > M || (mq == M && aq < arg)) { M = mq; arg = aq; }
+      }
+      double S = 0.0;
+#pragma unroll
+      for (int q = 0; q < WN; ++q) S += (double)e[3 * q + 1] * exp((double)e[3 * q] - (double)M);
+      RowStat o;
+      o.max = M;
+      o.argmax = arg;
+      o.sum = S;
+      g.stats[(long)m * (g.Nw / 128) + nt] = o;
     }
   }
 }
@@ -190,20 +253,29 @@ __global__ __launch_bounds__(256) void gemm_stream_kernel(GemmS g) {
 // sum of the K-split partials in split order, then the epilogue
 template <int EPI>
 __global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmS g) {
-  const long total = (long)g.M * g.N;
+  // four consecutive columns per thread (N % 4 == 0)
+  const long total = (long)g.M * (g.N / 4);
   for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
-    const int m = (int)(i / g.N), n = (int)(i % g.N);
-    float a = 0.f, b = 0.f;
+    const int m = (int)(i / (g.N / 4)), n = (int)(i % (g.N / 4)) * 4;
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int s = 0; s < g.splits; ++s) {
       const float *p = g.part + ((long)s * g.M + m) * g.Nw;
-      a += p[n];
-      if (EPI == EPI_SWIGLU) b += p[g.N + n];
+      const float4 x = *reinterpret_cast<const float4 *>(p + n);
+      a.x += x.x; a.y += x.y; a.z += x.z; a.w += x.w;
+      if (EPI == EPI_SWIGLU) {
+        const float4 y = *reinterpret_cast<const float4 *>(p + g.N + n);
+        b.x += y.x; b.y += y.y; b.z += y.z; b.w += y.w;
+      }
     }
+    const float av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
     const long o = (long)m * g.ldy + n;
-    if (EPI == EPI_STORE_F32) ((float *)g.Y)[o] = a;
-    else if (EPI == EPI_ADD_F32) ((float *)g.Y)[o] += a;
-    else if (EPI == EPI_SWIGLU) ((uint16_t *)g.Y)[o] = f32_to_bf16(silu(a) * b);
-    else ((uint16_t *)g.Y)[o] = f32_to_bf16(a);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (EPI == EPI_STORE_F32 || EPI == EPI_STATS) ((float *)g.Y)[o + q] = av[q];
+      else if (EPI == EPI_ADD_F32) ((float *)g.Y)[o + q] += av[q];
+      else if (EPI == EPI_SWIGLU) ((uint16_t *)g.Y)[o + q] = f32_to_bf16(silu(av[q]) * bv[q]);
+      else ((uint16_t *)g.Y)[o + q] = f32_to_bf16(av[q]);
+    }
   }
 }
 
@@ -265,9 +337,8 @@ void launch_stream(const GemmS &g, hipStream_t s) {
 template <int EPI>
 void launch_stream_shape(int shape, const GemmS &g, hipStream_t s) {
   switch (shape) {
-    case 0: launch_stream<4, 2, 1, EPI>(g, s); break;   // M <= 64:  64 x 128 tiles
-    case 1: launch_stream<8, 2, 1, EPI>(g, s); break;   // M <= 128: 128 x 128 tiles
-    default: launch_stream<8, 4, 2, EPI>(g, s); break;  // M > 128:  256 x 128 tiles
+    case 0: launch_stream<4, 2, 1, EPI>(g, s); break;   // 64 x 128 tiles
+    default: launch_stream<8, 2, 1, EPI>(g, s); break;  // 128 x 128 tiles
   }
 }
 }  // namespace
@@ -275,11 +346,13 @@ void launch_stream_shape(int shape, const GemmS &g, hipStream_t s) {
 // Tile shape and K split.  Every launch streams each weight byte from HBM
 // once; the choices trade workgroup count (to keep the CUs streaming) against
 // extra traffic:
-//  * wide outputs (>= 256 column tiles, e.g. the LM head) take the largest M
-//    tile, so weight strips are fetched once per 256 rows;
-//  * narrow outputs use 64-row tiles, several M tiles of one strip served
-//    from the XCD's L2, plus a K split capped so that the float32 partials
-//    move at most half as many bytes as the weights.
+//  * wide outputs (>= 256 column tiles, e.g. the LM head) with 65..128 rows
+//    take 128-row tiles, so each weight strip is fetched once;
+//  * everything else uses 64-row tiles: the M tiles of one strip run on the
+//    same XCD and re-read it from that XCD's L2 (measured faster than
+//    256-row tiles at 256 rows: more workgroups in flight per strip), plus,
+//    for narrow outputs, a K split capped so that the float32 partials move
+//    at most half as many bytes as the weights.
 GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
   GemmPlan p{};
   if (dtype != GM_BF16 || M <= 0) return p;
@@ -287,29 +360,28 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
   p.Nw = epi == EPI_SWIGLU ? 2 * N : N;
   p.n_tiles = p.Nw / cols;
   const int target = 256;                           // workgroups that keep every CU streaming
-  if (M <= 64 || p.n_tiles < target) p.shape = 0;
-  else p.shape = M <= 128 ? 1 : 2;
-  const int BM = p.shape == 0 ? 64 : (p.shape == 1 ? 128 : 256);
-  const int ITER = p.shape == 2 ? 4 : 8;            // k32 steps per unrolled iteration (see kernel)
+  p.shape = (M > 64 && M <= 128 && p.n_tiles >= target) ? 1 : 0;
+  const int BM = p.shape == 0 ? 64 : 128;
+  const int ITER = 8;                               // k32 steps per unrolled iteration (see kernel)
   p.m_tiles = (M + BM - 1) / BM;
   p.k_iters = K / (ITER * 32);
   int splits = (target + p.n_tiles * p.m_tiles - 1) / (p.n_tiles * p.m_tiles);
   const int cap = K / (8 * M);                      // 2 * S * M * Nw * 4 <= Nw * K * 2 / 2
   if (splits > cap) splits = cap;
   if (splits > p.k_iters) splits = p.k_iters;
-  if (splits < 1) splits = 1;
+  if (splits < 1 || epi == EPI_STATS) splits = 1;   // tile statistics need whole dot products
   p.splits = splits;
   p.part_bytes = splits > 1 ? (size_t)splits * M * p.Nw * sizeof(float) : 0;
   return p;
 }
 
 void launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, const void *X, int ldx, const void *W,
-                 void *Y, long ldy, float *part, hipStream_t s) {
+                 void *Y, long ldy, float *part, hipStream_t s, RowStat *tile_stats, float inv_t) {
   if (M <= 0) return;
   if (dtype == GM_BF16) {
     const GemmPlan p = plan_gemm(dtype, epi, M, N, K);
     GemmS g{(const uint16_t *)X, (const uint16_t *)W, Y, part, ldy, M, N, K, ldx, p.Nw, p.n_tiles, p.m_tiles,
-            p.splits, p.k_iters};
+            p.splits, p.k_iters, tile_stats, inv_t};
     {
       TraceScope ts(name, s);
       switch (epi) {
@@ -317,11 +389,12 @@ void launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, cons
         case EPI_ADD_F32: launch_stream_shape<EPI_ADD_F32>(p.shape, g, s); break;
         case EPI_STORE_ACT: launch_stream_shape<EPI_STORE_ACT>(p.shape, g, s); break;
         case EPI_SWIGLU: launch_stream_shape<EPI_SWIGLU>(p.shape, g, s); break;
+        case EPI_STATS: launch_stream_shape<EPI_STATS>(p.shape, g, s); break;
       }
     }
     if (p.splits > 1) {
       TraceScope ts("gemm_split_reduce", s);
-      const long total = (long)M * N;
+      const long total = (long)M * (N / 4);
       const int blocks = (int)((total + 255) / 256 < 2048 ? (total + 255) / 256 : 2048);
       switch (epi) {
         case EPI_STORE_F32: hipLaunchKernelGGL(gemm_reduce_kernel<EPI_STORE_F32>, dim3(blocks), dim3(256), 0, s, g); break;
@@ -333,6 +406,14 @@ void launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, cons
   } else {
     GemmF g{(const float *)X, (const float *)W, (float *)Y, ldy, M, N, K, ldx};
     const dim3 grid((N + 63) / 64, (M + 15) / 16), block(256);
+    if (epi == EPI_STATS) {     // no fused epilogue on this path: a pass over the output rows
+      {
+        TraceScope ts(name, s);
+        hipLaunchKernelGGL(gemm_f32_kernel<EPI_STORE_F32>, grid, block, 0, s, g);
+      }
+      launch_tile_stats((const float *)Y, ldy, M, N, inv_t, tile_stats, s);
+      return;
+    }
     TraceScope ts(name, s);
     switch (epi) {
       case EPI_STORE_F32: hipLaunchKernelGGL(gemm_f32_kernel<EPI_STORE_F32>, grid, block, 0, s, g); break;

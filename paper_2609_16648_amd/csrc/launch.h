@@ -44,15 +44,26 @@ constexpr int kScanChunk = kScanThreads * kScanPer;           // 4096 ids per ch
 inline int stat_chunks(int V) { return (V + kStatChunk - 1) / kStatChunk; }
 inline int scan_chunks(int V) { return (V + kScanChunk - 1) / kScanChunk; }
 
+// Softmax statistics per 128-id tile of a logits row (RowStat per tile), the
+// form the LM-head GEMM epilogue emits; a draw from such a row needs no
+// further pass over the vocabulary.
+constexpr int kTileIds = 128;
+inline int vocab_tiles(int V) { return (V + kTileIds - 1) / kTileIds; }
+// tile statistics by a pass over rows of logits (paths without the GEMM epilogue)
+void launch_tile_stats(const float *logits, long row_stride, int n_rows, int V, float inv_t, RowStat *tiles,
+                       hipStream_t s);
+// one draw per row from softmax(z / T) given its tile statistics: argmax (greedy) or the
+// inverse-CDF draw with u[b * u_stride]; writes dst[b * dst_stride]
+void launch_tile_draw(int B, int V, int mode, float inv_t, const float *logits, long row_stride,
+                      const RowStat *tiles, const float *u, int u_stride, int32_t *dst, int dst_stride,
+                      hipStream_t s);
+
 void launch_row_stats(const char *name, const float *logits, long row_stride, int n_rows, int V, float inv_t,
                       RowStat *out, hipStream_t s);
 void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const float *tlog,
                           const float *dlog, const RowStat *tstat, const RowStat *dstat,
                           const int32_t *drafts, const float *u_accept, const float *u_final,
                           int32_t *n_accept, int32_t *out_tokens, RowSel *sel, hipStream_t s);
-void launch_draft_select(int B, int V, int mode, float inv_t, const float *dlog, long row_stride,
-                         const RowStat *stat, const float *u, int u_stride, int32_t *dst,
-                         int dst_stride, RowSel *sel, hipStream_t s);
 void launch_residual_draw(const char *chunk_name, const char *scan_name, int B, int V, float inv_t, const RowSel *sel, double *wsum,
                           double *psum, hipStream_t s);
 

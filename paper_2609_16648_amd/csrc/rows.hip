@@ -27,18 +27,28 @@ __global__ __launch_bounds__(256) void embed_kernel(int H, int V, const int32_t 
   for (int c = threadIdx.x; c < H; c += blockDim.x) xr[c] = Elem<T>::load(er, c);
 }
 
+// one wave per row, four channels per lane and step (H % 4 == 0)
 template <typename T>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(int H, float eps, const float *__restrict__ x,
+__global__ __launch_bounds__(256) void rmsnorm_kernel(int M, int H, float eps, const float *__restrict__ x,
                                                       const T *__restrict__ w, T *__restrict__ out) {
-  __shared__ float red[16];
-  const int r = blockIdx.x;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (r >= M) return;
   const float *xr = x + (long)r * H;
   float ss = 0.f;
-  for (int c = threadIdx.x; c < H; c += blockDim.x) ss += xr[c] * xr[c];
-  ss = block_sum(ss, red);
+  for (int c = lane * 4; c < H; c += 256) {
+    const float4 v = *reinterpret_cast<const float4 *>(xr + c);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = wave_sum(ss);
   const float inv = 1.0f / sqrtf(ss / (float)H + eps);
   T *o = out + (long)r * H;
-  for (int c = threadIdx.x; c < H; c += blockDim.x) Elem<T>::store(o, c, xr[c] * inv * Elem<T>::load(w, c));
+  for (int c = lane * 4; c < H; c += 256) {
+    const float4 v = *reinterpret_cast<const float4 *>(xr + c);
+    Elem<T>::store(o, c, v.x * inv * Elem<T>::load(w, c));
+    Elem<T>::store(o, c + 1, v.y * inv * Elem<T>::load(w, c + 1));
+    Elem<T>::store(o, c + 2, v.z * inv * Elem<T>::load(w, c + 2));
+    Elem<T>::store(o, c + 3, v.w * inv * Elem<T>::load(w, c + 3));
+  }
 }
 
 template <typename T>
@@ -103,6 +113,9 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
   }
   const float *src_row = a.qkv + (long)row * nh * D;
   const T *qn = (const T *)a.q_norm, *kn = (const T *)a.k_norm;
+  // the rotation of pair `lane` at this position, shared by every head of the row
+  double sn = 0.0, cs = 1.0;
+  if (lane < half) sincos(pos * pow((double)a.rope_base, -2.0 * lane / D), &sn, &cs);
   for (int hh = w; hh < nh; hh += 4) {
     const float *src = src_row + hh * D;
     const int kind = hh < a.n_heads ? 0 : (hh < a.n_heads + a.n_kv ? 1 : 2);
@@ -120,9 +133,6 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
     if (!act) continue;
     float y1 = x1, y2 = x2;
     if (kind < 2) {
-      const double ang = pos * pow((double)a.rope_base, -2.0 * lane / D);
-      double sn, cs;
-      sincos(ang, &sn, &cs);
       y1 = (float)((double)x1 * cs - (double)x2 * sn);
       y2 = (float)((double)x2 * cs + (double)x1 * sn);
     }
@@ -170,10 +180,11 @@ void launch_embed(int dtype, int M, int H, int V, const int32_t *tokens, const v
 void launch_rmsnorm(int dtype, int M, int H, float eps, const float *x, const void *w, void *out, hipStream_t s) {
   if (M <= 0) return;
   TraceScope ts("rmsnorm", s);
+  const dim3 grid((M + 3) / 4);
   if (dtype == GM_BF16)
-    hipLaunchKernelGGL(rmsnorm_kernel<bf16>, dim3(M), dim3(256), 0, s, H, eps, x, (const bf16 *)w, (bf16 *)out);
+    hipLaunchKernelGGL(rmsnorm_kernel<bf16>, grid, dim3(256), 0, s, M, H, eps, x, (const bf16 *)w, (bf16 *)out);
   else
-    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(M), dim3(256), 0, s, H, eps, x, (const float *)w, (float *)out);
+    hipLaunchKernelGGL(rmsnorm_kernel<float>, grid, dim3(256), 0, s, M, H, eps, x, (const float *)w, (float *)out);
 }
 
 void launch_rope_append(const RopeArgs &a, hipStream_t s) {

@@ -11,8 +11,11 @@
 //     prepares one draw per sequence (residual max(0, p - q) at the first
 //     rejection, p_{k+1} after a full accept).
 //  3. residual_chunk + residual_scan: an inverse-CDF draw in ascending id
-//     order evaluated in float64 (p, q and the running sum), first as chunk
-//     masses, then a scan inside the chunk that holds u * Z.
+//     order (per-id exponentials in float32, normalisers, differences and
+//     running sums in float64), first as chunk masses, then a scan inside the
+//     chunk that holds u * Z.
+//  4. tile_stats / tile_draw: per 128-id tile statistics (also emitted by
+//     the LM-head GEMM epilogue) and a draw that needs no pass over the row.
 #include <float.h>
 
 #include "common.h"
@@ -178,48 +181,15 @@ void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const floa
                      out_tokens, sel);
 }
 
-// one draw per sequence from softmax(z / T) of a draft-logits row (greedy: its argmax)
-__global__ void draft_select_kernel(int B, int V, int mode, const float *__restrict__ dlog,
-                                    long row_stride, const RowStat *__restrict__ stat, int nch,
-                                    const float *__restrict__ u, int u_stride, int32_t *__restrict__ dst,
-                                    int dst_stride, RowSel *__restrict__ sel) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= B) return;
-  RowSel rs;
-  int am;
-  combine_stats(stat + (long)b * nch, nch, rs.mp, rs.sp, am);
-  rs.p_row = dlog + (long)b * row_stride;
-  rs.q_row = nullptr;
-  rs.mq = 0.0;
-  rs.sq = 1.0;
-  rs.pad = 0;
-  rs.dst = dst + (long)b * dst_stride;
-  if (mode == GM_GREEDY) {
-    *rs.dst = am;
-    rs.active = 0;
-    rs.u = 0.0;
-  } else {
-    rs.u = (double)u[(long)b * u_stride];
-    rs.active = 1;
-  }
-  sel[b] = rs;
-}
-
-void launch_draft_select(int B, int V, int mode, float inv_t, const float *dlog, long row_stride,
-                         const RowStat *stat, const float *u, int u_stride, int32_t *dst,
-                         int dst_stride, RowSel *sel, hipStream_t s) {
-  (void)inv_t;
-  TraceScope ts("draft_select", s);
-  hipLaunchKernelGGL(draft_select_kernel, dim3((B + 63) / 64), dim3(64), 0, s, B, V, mode, dlog,
-                     row_stride, stat, stat_chunks(V), u, u_stride, dst, dst_stride, sel);
-}
-
 // ------------------------------------------------------------------ 3. inverse-CDF draw
-// weight of id x: max(0, p(x) - q(x)) with q, p(x) without; every quantity in float64
-__device__ __forceinline__ double draw_weight(const RowSel &s, int x, float inv_t, bool use_p) {
-  const double p = exp((double)(s.p_row[x] * inv_t) - s.mp) / s.sp;
+// weight of id x: max(0, p(x) - q(x)) with q, p(x) without.  Each exponential is a
+// float32 expf of z / T - max (both float32); scaling by the float64 normaliser
+// and every sum are float64.
+__device__ __forceinline__ double draw_weight(const RowSel &s, int x, float inv_t, bool use_p, double isp,
+                                              double isq) {
+  const double p = (double)expf(s.p_row[x] * inv_t - (float)s.mp) * isp;
   if (use_p || s.q_row == nullptr) return p;
-  const double q = exp((double)(s.q_row[x] * inv_t) - s.mq) / s.sq;
+  const double q = (double)expf(s.q_row[x] * inv_t - (float)s.mq) * isq;
   return fmax(p - q, 0.0);
 }
 
@@ -234,12 +204,13 @@ __global__ __launch_bounds__(kScanThreads) void residual_chunk_kernel(int V, flo
   const RowSel s = sel[b];
   if (!s.active) return;
   const int x0 = c * kScanChunk + tid * kScanPer;
+  const double isp = 1.0 / s.sp, isq = 1.0 / s.sq;
   double w = 0.0, p = 0.0;
   for (int j = 0; j < kScanPer; ++j) {
     const int x = x0 + j;
     if (x < V) {
-      const double px = exp((double)(s.p_row[x] * inv_t) - s.mp) / s.sp;
-      const double qx = s.q_row ? exp((double)(s.q_row[x] * inv_t) - s.mq) / s.sq : 0.0;
+      const double px = (double)expf(s.p_row[x] * inv_t - (float)s.mp) * isp;
+      const double qx = s.q_row ? (double)expf(s.q_row[x] * inv_t - (float)s.mq) * isq : 0.0;
       w += s.q_row ? fmax(px - qx, 0.0) : px;
       p += px;
     }
@@ -298,10 +269,11 @@ __global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, floa
   __syncthreads();
   const int cs = sh_chunk;
   const bool use_p = sh_use_p != 0;
+  const double isp = 1.0 / s.sp, isq = 1.0 / s.sq;
   const int x0 = cs * kScanChunk + tid * kScanPer;
   double w = 0.0;
   for (int j = 0; j < kScanPer; ++j)
-    if (x0 + j < V) w += draw_weight(s, x0 + j, inv_t, use_p);
+    if (x0 + j < V) w += draw_weight(s, x0 + j, inv_t, use_p, isp, isq);
   st[tid] = w;
   __syncthreads();
   if (tid == 0) {
@@ -324,7 +296,7 @@ __global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, floa
     for (int j = 0; j < kScanPer; ++j) {
       const int x = x0 + j;
       if (x >= V) break;
-      const double wx = draw_weight(s, x, inv_t, use_p);
+      const double wx = draw_weight(s, x, inv_t, use_p, isp, isq);
       if (wx > 0.0) x_last = x;
       acc += wx;
       if (sh_found && x_hit < 0 && acc > sh_t) x_hit = x;
@@ -376,6 +348,156 @@ void launch_kv_commit(int B, int k, int page_size, int max_pages, const int32_t 
   TraceScope ts("kv_commit", s);
   hipLaunchKernelGGL(kv_commit_kernel, dim3((B + 63) / 64), dim3(64), 0, s, B, k, page_size, max_pages,
                      block_table, seq_lens, n_accept, slots);
+}
+
+}  // namespace gm
+
+// ------------------------------------------------------------------ tile statistics and tile draws
+namespace gm {
+
+// one wave per 128-id tile: max of z / T, the lowest id attaining it, sum exp(z / T - max)
+__global__ __launch_bounds__(256) void tile_stats_kernel(const float *__restrict__ logits, long row_stride, int V,
+                                                         float inv_t, int n_tiles, RowStat *__restrict__ out) {
+  const int r = blockIdx.x, t = blockIdx.y * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (t >= n_tiles) return;
+  const float *row = logits + (long)r * row_stride;
+  const int x0 = t * kTileIds + lane, x1 = x0 + 64;
+  const float v0 = x0 < V ? row[x0] * inv_t : -INFINITY, v1 = x1 < V ? row[x1] * inv_t : -INFINITY;
+  float m = v0;
+  int a = x0 < V ? x0 : 0x7fffffff;
+  if (v1 > m) { m = v1; a = x1; }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float om = __shfl_xor(m, o, kWave);
+    const int oa = __shfl_xor(a, o, kWave);
+    if (om > m || (om == m && oa < a)) { m = om; a = oa; }
+  }
+  float s = expf(v0 - m) + expf(v1 - m);
+  s = wave_sum(s);
+  if (lane == 0) {
+    RowStat o;
+    o.max = m;
+    o.argmax = a;
+    o.sum = (double)s;
+    out[(long)r * n_tiles + t] = o;
+  }
+}
+
+void launch_tile_stats(const float *logits, long row_stride, int n_rows, int V, float inv_t, RowStat *tiles,
+                       hipStream_t s) {
+  if (n_rows <= 0) return;
+  TraceScope ts("draft_tile_stats", s);
+  const int nt = vocab_tiles(V);
+  hipLaunchKernelGGL(tile_stats_kernel, dim3(n_rows, (nt + 3) / 4), dim3(256), 0, s, logits, row_stride, V, inv_t,
+                     nt, tiles);
+}
+
+// One block per row.  The row's max and arg-max come from its tile statistics;
+// a sampled draw accumulates the tile masses s_t exp(m_t - M) in float64 in
+// ascending tile order to find the tile holding u * S, then one wave scans
+// that tile's 128 ids (the same per-id terms exp(z / T - m_t) the tile sums
+// were made of, scaled in float64) for the first running sum above u * S.
+__global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float inv_t, const float *__restrict__ logits,
+                                                        long row_stride, const RowStat *__restrict__ tiles,
+                                                        int n_tiles, const float *__restrict__ u, int u_stride,
+                                                        int32_t *__restrict__ dst, int dst_stride) {
+  __shared__ double seg[256];
+  __shared__ float red_m[4];
+  __shared__ int red_a[4];
+  __shared__ double sh_base, sh_t;
+  __shared__ int sh_tile;
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const RowStat *st = tiles + (long)b * n_tiles;
+  float m = -INFINITY;
+  int a = 0x7fffffff;
+  for (int t = tid; t < n_tiles; t += 256) {
+    const RowStat s = st[t];
+    if (s.max > m || (s.max == m && s.argmax < a)) { m = s.max; a = s.argmax; }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float om = __shfl_xor(m, o, kWave);
+    const int oa = __shfl_xor(a, o, kWave);
+    if (om > m || (om == m && oa < a)) { m = om; a = oa; }
+  }
+  if (lane == 0) { red_m[wid] = m; red_a[wid] = a; }
+  __syncthreads();
+  m = red_m[0];
+  a = red_a[0];
+  for (int w = 1; w < 4; ++w)
+    if (red_m[w] > m || (red_m[w] == m && red_a[w] < a)) { m = red_m[w]; a = red_a[w]; }
+  if (mode == GM_GREEDY) {
+    if (tid == 0) dst[(long)b * dst_stride] = a;
+    return;
+  }
+  const double M = (double)m;
+  const int per = (n_tiles + 255) / 256, t0 = tid * per, t1 = min(n_tiles, t0 + per);
+  double w = 0.0;
+  for (int t = t0; t < t1; ++t) w += st[t].sum * exp((double)st[t].max - M);
+  seg[tid] = w;
+  __syncthreads();
+  if (tid == 0) {
+    double S = 0.0;
+    for (int i = 0; i < 256; ++i) S += seg[i];
+    const double target = (double)u[(long)b * u_stride] * S;
+    double acc = 0.0;
+    int tile = -1, last = 0;
+    for (int i = 0; i < 256 && tile < 0; ++i) {
+      if (seg[i] > 0.0) last = i;
+      if (acc + seg[i] > target) {
+        for (int t = i * per; t < min(n_tiles, (i + 1) * per); ++t) {
+          const double W = st[t].sum * exp((double)st[t].max - M);
+          if (acc + W > target) { tile = t; break; }
+          acc += W;
+        }
+        if (tile < 0) tile = min(n_tiles, (i + 1) * per) - 1;   // rounding: end of this segment
+      } else {
+        acc += seg[i];
+      }
+    }
+    if (tile < 0) {   // rounding put u * S past the end: last tile of the last segment with mass
+      tile = min(n_tiles, (last + 1) * per) - 1;
+      acc = 0.0;
+      for (int t = 0; t < tile; ++t) acc += st[t].sum * exp((double)st[t].max - M);
+    }
+    sh_tile = tile;
+    sh_base = acc;
+    sh_t = target;
+  }
+  __syncthreads();
+  if (wid != 0) return;
+  const int tile = sh_tile;
+  const float mt = st[tile].max;
+  const double scale = exp((double)mt - M);
+  const float *row = logits + (long)b * row_stride;
+  const int xa = tile * kTileIds + 2 * lane, xb = xa + 1;
+  const double ea = xa < V ? (double)expf(row[xa] * inv_t - mt) * scale : 0.0;
+  const double eb = xb < V ? (double)expf(row[xb] * inv_t - mt) * scale : 0.0;
+  double incl = ea + eb;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double n = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += n;
+  }
+  double excl = __shfl_up(incl, 1, kWave);
+  if (lane == 0) excl = 0.0;
+  const double acc_a = sh_base + excl + ea, acc_b = acc_a + eb;
+  const unsigned long long hit = __ballot(acc_a > sh_t || acc_b > sh_t);
+  const unsigned long long nz = __ballot(ea > 0.0 || eb > 0.0);
+  // the first hit lane decides between its two ids (running sums grow along lanes)
+  const int first = hit ? __ffsll((long long)hit) - 1 : -1;
+  const int lastnz = nz ? 63 - __clzll((long long)nz) : -1;
+  if (first >= 0 && lane == first) dst[(long)b * dst_stride] = acc_a > sh_t ? xa : xb;
+  if (first < 0 && lastnz >= 0 && lane == lastnz) dst[(long)b * dst_stride] = eb > 0.0 ? xb : xa;
+  if (first < 0 && lastnz < 0 && lane == 0) dst[(long)b * dst_stride] = a;
+}
+
+void launch_tile_draw(int B, int V, int mode, float inv_t, const float *logits, long row_stride, const RowStat *tiles,
+                      const float *u, int u_stride, int32_t *dst, int dst_stride, hipStream_t s) {
+  if (B <= 0) return;
+  TraceScope ts("draft_draw", s);
+  hipLaunchKernelGGL(tile_draw_kernel, dim3(B), dim3(256), 0, s, V, mode, inv_t, logits, row_stride, tiles,
+                     vocab_tiles(V), u, u_stride, dst, dst_stride);
 }
 
 }  // namespace gm

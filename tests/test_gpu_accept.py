@@ -1,7 +1,7 @@
 """GPU parity of gm_spec_accept and gm_kv_commit against the oracle on the same
 seeded logits.  Accept counts and committed slots must match bit for bit
 outside the flag windows (|u - min(1, p/q)| < 1e-3, top-2 margin < 1e-2, and
-a final draw within 1e-9 Z of a CDF edge); the flagged count is printed."""
+a final draw within 1e-8 Z of a CDF edge); the flagged count is printed."""
 import numpy as np
 import pytest
 import scipy.stats
@@ -13,7 +13,7 @@ from helpers import need_gpu, t32, i32, flag_report
 from paper_2609_16648_amd import gm
 
 pytestmark = pytest.mark.gpu
-FINAL_EPS = 1e-9
+FINAL_EPS = 1e-8
 
 
 def _sampled_drafts(zq, u_draft):

@@ -24,6 +24,11 @@ CFLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH, "-Wall", "-Wno
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-I" + os.path.join(ROOT, "include")]
 
+# Per-source extra flags.  attention.hip: keep MFMA accumulators in ordinary
+# VGPRs (the online-softmax rescale multiplies them with vector ALU ops, which
+# would otherwise copy them out of and back into accumulation registers).
+EXTRA_FLAGS = {"attention.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form"]}
+
 
 def hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
@@ -38,7 +43,7 @@ def sources():
 
 def _compile(src: str) -> str:
     obj = os.path.join(OUT_DIR, os.path.basename(src) + ".o")
-    cmd = [hipcc()] + CFLAGS + ["-c", src, "-o", obj]
+    cmd = [hipcc()] + CFLAGS + EXTRA_FLAGS.get(os.path.basename(src), []) + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("compile failed: %s\n%s\n%s" % (" ".join(cmd), r.stdout, r.stderr))

@@ -7,8 +7,8 @@
 namespace gm {
 
 constexpr int kAttnMaxRows = 64;   // (n_heads / n_kv_heads) * block rows per KV head
-constexpr int kAttnMaxSplitTokens = 4096;                           // tokens per attention split
-constexpr int kAttnMaxSplitPages = kAttnMaxSplitTokens / 16 + 8;    // pages one split can touch
+constexpr int kAttnMaxSplitTokens = 4096;                           // tokens of one workgroup's range
+constexpr int kAttnMaxSplitPages = kAttnMaxSplitTokens / 16 + 8;    // pages one range can touch
 
 struct Carve {
   size_t off = 0;
@@ -21,10 +21,9 @@ struct Carve {
 
 // ---------------------------------------------------------------- attention
 struct AttnPlan {
-  int splits;          // context splits per (sequence, kv head)
-  int split_tokens;    // tokens per split (multiple of 16)
+  int parts;           // ranges the tiles of all sequences are cut into (workgroups per head group)
   int rows_pad;        // 16-row tiles * 16
-  size_t part_o, part_ml, total;
+  size_t part_o, part_ml, cum, total;
 };
 AttnPlan plan_attention(const gm_model_config &cfg, int B, int R, int max_ctx);
 

@@ -66,7 +66,8 @@ typedef enum {
  * / grouped-query attention / SwiGLU, the layer of the paper's backbones
  * (App. "Models and Draft Heads").  Limits of this build: head_dim 128 for
  * GM_BF16 (64 or 128 for GM_F32), n_heads a multiple of n_kv_heads with
- * (n_heads / n_kv_heads) * (k + 1) <= 64, hidden and ffn multiples of 64;
+ * (n_heads / n_kv_heads) * (k + 1) <= 64, hidden and ffn multiples of 64,
+ * hidden and (n_heads + 2 n_kv_heads) * head_dim at most 16384;
  * GM_BF16 needs vocab a multiple of 128 and hidden, ffn and
  * n_heads * head_dim multiples of 256. */
 typedef struct {

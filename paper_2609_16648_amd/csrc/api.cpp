@@ -62,6 +62,9 @@ gm_status check_config(const gm_model_config *cfg, int B, int k) {
   if (G * (k + 1) > kAttnMaxRows)
     return fail(GM_ERR_UNSUPPORTED, "(n_heads / n_kv_heads) * (k + 1) = %d exceeds %d", G * (k + 1), kAttnMaxRows);
   if (cfg->hidden % 64 || cfg->ffn % 64) return fail(GM_ERR_UNSUPPORTED, "hidden and ffn must be multiples of 64");
+  // row kernels stage one hidden row or one projected q/k/v row in 64 KiB of LDS
+  if (cfg->hidden > kMaxRowFloats || (cfg->n_heads + 2 * cfg->n_kv_heads) * cfg->head_dim > kMaxRowFloats)
+    return fail(GM_ERR_UNSUPPORTED, "hidden and (n_heads + 2 n_kv_heads) * head_dim must be at most %d", kMaxRowFloats);
   if (!(cfg->rms_eps >= 0.f) || !(cfg->rope_base > 0.f)) return fail(GM_ERR_INVALID_ARG, "bad rms_eps or rope_base");
   if (cfg->dtype == GM_BF16) {
     if (cfg->head_dim != 128) return fail(GM_ERR_UNSUPPORTED, "bf16 path needs head_dim 128, got %d", cfg->head_dim);

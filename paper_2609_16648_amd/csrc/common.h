@@ -74,6 +74,32 @@ __device__ __forceinline__ F block_sum(F v, F *smem /* >= 16 */) {
   return t;
 }
 
+// Sum, in split order, of `splits` float4 values stride floats apart (K-split
+// partials of one output element group); the loads of a batch are all issued
+// before the first add.
+__device__ __forceinline__ float4 sum_splits(const float *p, long stride, int splits) {
+  constexpr int kBatch = 8;
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s0 = 0; s0 < splits; s0 += kBatch) {
+    float4 v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int sp = s0 + u < splits ? s0 + u : splits - 1;
+      v[u] = *reinterpret_cast<const float4 *>(p + sp * stride);
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      if (s0 + u < splits) {
+        a.x += v[u].x;
+        a.y += v[u].y;
+        a.z += v[u].z;
+        a.w += v[u].w;
+      }
+    }
+  }
+  return a;
+}
+
 // ----------------------------------------------------------------- KV tile layout
 // Offsets inside the 16-token tile of one (page, kv head); see gm.h.
 __device__ __forceinline__ int k_tile_off(int s, int c) {

@@ -26,9 +26,19 @@ size_t part_bytes(const gm_model_config &c, int M, bool with_proj) {
   return b;
 }
 
+// GEMM into the float32 residual rows Y [M][N] followed by the RMSNorm of those
+// rows into nbuf: with a K split the reduce and the norm run as one kernel.
+void gemm_norm(const char *name, int dt, int epi, int M, int N, int K, const void *X, int ldx, const void *W,
+               float *Y, float *part, const void *norm_w, float eps, void *nbuf, hipStream_t s) {
+  const int sp = launch_gemm(name, dt, epi, M, N, K, X, ldx, W, Y, N, part, s, nullptr, 1.f, true);
+  if (sp > 1) launch_reduce_norm(dt, epi, M, N, sp, part, Y, norm_w, eps, nbuf, s);
+  else launch_rmsnorm(dt, M, N, eps, Y, norm_w, nbuf, s);
+}
+
+// qkv projection: `splits` > 1 leaves the partials in `part` for the RoPE kernel to sum
 RopeArgs rope_args(const gm_model_config &cfg, const gm_kv_cache &c, int layer, int M, int R, const float *qkv,
-                   void *q_out, const int32_t *base, int base_off, const int32_t *blk_len, int pos_off,
-                   const gm_layer_weights &L, int32_t *dev_err) {
+                   const float *part, int splits, void *q_out, const int32_t *base, int base_off,
+                   const int32_t *blk_len, int pos_off, const gm_layer_weights &L, int32_t *dev_err) {
   RopeArgs a{};
   a.dtype = cfg.dtype;
   a.M = M;
@@ -37,6 +47,8 @@ RopeArgs rope_args(const gm_model_config &cfg, const gm_kv_cache &c, int layer, 
   a.n_kv = cfg.n_kv_heads;
   a.head_dim = cfg.head_dim;
   a.qkv = qkv;
+  a.part = part;
+  a.splits = splits;
   a.q_out = q_out;
   a.k_pages = c.k_pages[layer];
   a.v_pages = c.v_pages[layer];
@@ -86,12 +98,15 @@ void run_verify_forward(const gm_model_config &cfg, const gm_model_weights &w, c
   void *nbuf = ws + p.nbuf, *act = ws + p.act, *q = ws + p.q, *attn = ws + p.attn;
   float *qkv = (float *)(ws + p.qkv);
   float *x = hidden, *part = (float *)(ws + p.part);
-  launch_embed(dt, M, H, V, tokens, w.embed, x, dev_err, s);
+  const float eps = cfg.rms_eps;
+  // the RMSNorm that opens a layer (or the final one) runs fused into the kernel before it
+  auto next_norm = [&](int l) { return l < cfg.n_layers ? w.layers[l].attn_norm : w.final_norm; };
+  launch_embed_norm(dt, M, H, V, tokens, w.embed, x, next_norm(0), eps, nbuf, dev_err, s);
   for (int l = 0; l < cfg.n_layers; ++l) {
     const gm_layer_weights &L = w.layers[l];
-    launch_rmsnorm(dt, M, H, cfg.rms_eps, x, L.attn_norm, nbuf, s);
-    launch_gemm("gemm_qkv", dt, EPI_STORE_F32, M, qkv_width(cfg), H, nbuf, H, L.w_qkv, qkv, qkv_width(cfg), part, s);
-    launch_rope_append(rope_args(cfg, c, l, M, R, qkv, q, c.seq_lens, 0, nullptr, 0, L, dev_err), s);
+    const int sq = launch_gemm("gemm_qkv", dt, EPI_STORE_F32, M, qkv_width(cfg), H, nbuf, H, L.w_qkv, qkv,
+                               qkv_width(cfg), part, s, nullptr, 1.f, true);
+    launch_rope_append(rope_args(cfg, c, l, M, R, qkv, part, sq, q, c.seq_lens, 0, nullptr, 0, L, dev_err), s);
     AttnArgs a = attn_args(cfg, c, l, B, R, c.seq_lens, 0, nullptr);
     a.trace = "attn_verify";
     a.trace_combine = "attn_verify_combine";
@@ -99,12 +114,10 @@ void run_verify_forward(const gm_model_config &cfg, const gm_model_weights &w, c
     a.out = attn;
     a.dev_err = dev_err;
     run_attention(a, p.attn_plan, ws + p.attn_ws, s);
-    launch_gemm("gemm_o", dt, EPI_ADD_F32, M, H, qd, attn, qd, L.w_o, x, H, part, s);
-    launch_rmsnorm(dt, M, H, cfg.rms_eps, x, L.ffn_norm, nbuf, s);
+    gemm_norm("gemm_o", dt, EPI_ADD_F32, M, H, qd, attn, qd, L.w_o, x, part, L.ffn_norm, eps, nbuf, s);
     launch_gemm("gemm_gate_up", dt, EPI_SWIGLU, M, F, H, nbuf, H, L.w_gate_up, act, F, part, s);
-    launch_gemm("gemm_down", dt, EPI_ADD_F32, M, H, F, act, F, L.w_down, x, H, part, s);
+    gemm_norm("gemm_down", dt, EPI_ADD_F32, M, H, F, act, F, L.w_down, x, part, next_norm(l + 1), eps, nbuf, s);
   }
-  launch_rmsnorm(dt, M, H, cfg.rms_eps, x, w.final_norm, nbuf, s);
   launch_gemm("gemm_lm_head", dt, EPI_STORE_F32, M, V, H, nbuf, H, w.lm_head, logits, V, part, s);
 }
 
@@ -155,12 +168,11 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
 
   // the layer tail on one row per sequence (x1 [B][H] float32 in place), then the
   // shared LM head into draft_logits[:, j, :] and the draw of drafts[:, j]
+  const float eps = cfg.rms_eps;
   auto tail_and_draw = [&](float *x1, int j) {
-    launch_gemm("mtp_gemm_o", dt, EPI_ADD_F32, B, H, qd, attn_g, qd, L.w_o, x1, H, part, s);
-    launch_rmsnorm(dt, B, H, cfg.rms_eps, x1, L.ffn_norm, nbuf, s);
+    gemm_norm("mtp_gemm_o", dt, EPI_ADD_F32, B, H, qd, attn_g, qd, L.w_o, x1, part, L.ffn_norm, eps, nbuf, s);
     launch_gemm("mtp_gemm_gate_up", dt, EPI_SWIGLU, B, F, H, nbuf, H, L.w_gate_up, act, F, part, s);
-    launch_gemm("mtp_gemm_down", dt, EPI_ADD_F32, B, H, F, act, F, L.w_down, x1, H, part, s);
-    launch_rmsnorm(dt, B, H, cfg.rms_eps, x1, mtp.final_norm, nbuf, s);
+    gemm_norm("mtp_gemm_down", dt, EPI_ADD_F32, B, H, F, act, F, L.w_down, x1, part, mtp.final_norm, eps, nbuf, s);
     float *zl = draft_logits + (long)j * V;
     // the LM head emits the logits and their softmax statistics per 128-id tile; the draw
     // then reads only the tile statistics and one tile of logits per sequence
@@ -172,10 +184,11 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
   // ---- extend: rows (h_{m+i}, x_{m+i+1}), i = 0..n_b, at slots m_b + i
   launch_mtp_input(dt, Me, H, V, cfg.rms_eps, verify_hidden, out_tokens, 1, shared.embed, mtp.norm_h, mtp.norm_e, u,
                    dev_err, s);
-  launch_gemm("mtp_gemm_proj", dt, EPI_STORE_F32, Me, H, 2 * H, u, 2 * H, mtp.w_proj, x, H, part, s);
-  launch_rmsnorm(dt, Me, H, cfg.rms_eps, x, L.attn_norm, nbuf, s);
-  launch_gemm("mtp_gemm_qkv", dt, EPI_STORE_F32, Me, qw, H, nbuf, H, L.w_qkv, qkv, qw, part, s);
-  launch_rope_append(rope_args(cfg, c, 0, Me, R, qkv, q, lens, 0, n_accept, 1, L, dev_err), s);
+  gemm_norm("mtp_gemm_proj", dt, EPI_STORE_F32, Me, H, 2 * H, u, 2 * H, mtp.w_proj, x, part, L.attn_norm, eps, nbuf,
+            s);
+  int sq = launch_gemm("mtp_gemm_qkv", dt, EPI_STORE_F32, Me, qw, H, nbuf, H, L.w_qkv, qkv, qw, part, s, nullptr, 1.f,
+                       true);
+  launch_rope_append(rope_args(cfg, c, 0, Me, R, qkv, part, sq, q, lens, 0, n_accept, 1, L, dev_err), s);
   {
     AttnArgs a = attn_args(cfg, c, 0, B, R, lens, 0, n_accept);
     a.blk_len_add = 1;
@@ -196,10 +209,11 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
   for (int j = 1; j < k; ++j) {
     launch_mtp_input(dt, B, H, V, cfg.rms_eps, xg, drafts + (j - 1), k, shared.embed, mtp.norm_h, mtp.norm_e, u,
                      dev_err, s);
-    launch_gemm("mtp_gemm_proj", dt, EPI_STORE_F32, B, H, 2 * H, u, 2 * H, mtp.w_proj, xg, H, part, s);
-    launch_rmsnorm(dt, B, H, cfg.rms_eps, xg, L.attn_norm, nbuf, s);
-    launch_gemm("mtp_gemm_qkv", dt, EPI_STORE_F32, B, qw, H, nbuf, H, L.w_qkv, qkv, qw, part, s);
-    launch_rope_append(rope_args(cfg, c, 0, B, 1, qkv, q, lens, j - 1, nullptr, 1, L, dev_err), s);
+    gemm_norm("mtp_gemm_proj", dt, EPI_STORE_F32, B, H, 2 * H, u, 2 * H, mtp.w_proj, xg, part, L.attn_norm, eps, nbuf,
+              s);
+    sq = launch_gemm("mtp_gemm_qkv", dt, EPI_STORE_F32, B, qw, H, nbuf, H, L.w_qkv, qkv, qw, part, s, nullptr, 1.f,
+                     true);
+    launch_rope_append(rope_args(cfg, c, 0, B, 1, qkv, part, sq, q, lens, j - 1, nullptr, 1, L, dev_err), s);
     AttnArgs a = attn_args(cfg, c, 0, B, 1, lens, j - 1, nullptr);
     a.trace = "attn_mtp";
     a.trace_combine = "attn_mtp_combine";

@@ -6,6 +6,7 @@
 
 namespace gm {
 
+constexpr int kMaxRowFloats = 16384;   // float32 row that the row kernels stage in LDS (64 KiB)
 constexpr int kAttnMaxRows = 64;   // (n_heads / n_kv_heads) * block rows per KV head
 constexpr int kAttnMaxSplitTokens = 4096;                           // tokens of one workgroup's range
 constexpr int kAttnMaxSplitPages = kAttnMaxSplitTokens / 16 + 8;    // pages one range can touch
@@ -59,19 +60,29 @@ struct GemmPlan {
   size_t part_bytes;   // float32 K-split partials
 };
 GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K);
-// bf16: W pre-tiled (gm.h), X row-major [M][ldx]; `part` must hold plan_gemm().part_bytes
-void launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, const void *X, int ldx,
-                 const void *W, void *Y, long ldy, float *part, hipStream_t s,
-                 RowStat *tile_stats = nullptr, float inv_t = 1.f);
+// bf16: W pre-tiled (gm.h), X row-major [M][ldx]; `part` must hold plan_gemm().part_bytes.
+// Returns the K splits; with defer_reduce and more than one split, no reduce runs and
+// the partials stay in `part` ([splits][M][Nw] float32) for the consumer to sum.
+int launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, const void *X, int ldx,
+                const void *W, void *Y, long ldy, float *part, hipStream_t s,
+                RowStat *tile_stats = nullptr, float inv_t = 1.f, bool defer_reduce = false);
+// Y[M][N] (+)= sum of `splits` partials, then out = RMSNorm(Y) * norm_w (epi: STORE_F32 or ADD_F32)
+void launch_reduce_norm(int dtype, int epi, int M, int N, int splits, const float *part, float *Y,
+                        const void *norm_w, float eps, void *out, hipStream_t s);
 
 // ---------------------------------------------------------------- row kernels
 void launch_embed(int dtype, int M, int H, int V, const int32_t *tokens, const void *E, float *x,
                   int32_t *dev_err, hipStream_t s);
 void launch_rmsnorm(int dtype, int M, int H, float eps, const float *x, const void *w, void *out,
                     hipStream_t s);
+// x = E[tokens] (float32) and out = RMSNorm(x) * norm_w (model dtype)
+void launch_embed_norm(int dtype, int M, int H, int V, const int32_t *tokens, const void *E, float *x,
+                       const void *norm_w, float eps, void *out, int32_t *dev_err, hipStream_t s);
 struct RopeArgs {
   int dtype, M, R, n_heads, n_kv, head_dim;
-  const float *qkv;            // [M][(n_heads + 2 n_kv) head_dim]
+  const float *qkv;            // [M][(n_heads + 2 n_kv) head_dim], or, with splits > 1,
+  const float *part;           // the projection's K-split partials [splits][M][...] to sum
+  int splits;
   void *q_out;                 // [M][n_heads][head_dim]
   void *k_pages, *v_pages;
   const int32_t *block_table;

@@ -279,6 +279,42 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmS g) {
   }
 }
 
+// The K-split partials of a [M][N] float32 output summed in split order (plus the
+// residual already in Y for EPI_ADD_F32) into Y, followed by the RMSNorm of each
+// row into `out` (model dtype, weight w): the reduce and the norm that always
+// follows it in one pass.  One block per row, a float4 column group per thread
+// and step (N % 4 == 0), the row kept in LDS between the two passes.
+template <typename T, int EPI>
+__global__ __launch_bounds__(1024) void reduce_norm_kernel(int M, int N, int splits, const float *__restrict__ part,
+                                                           float *__restrict__ Y, const T *__restrict__ w, float eps,
+                                                           T *__restrict__ out) {
+  extern __shared__ float row_sh[];   // [N]
+  __shared__ float red[16];
+  const int m = blockIdx.x;
+  float *y = Y + (long)m * N;
+  float ss = 0.f;
+  for (int n = threadIdx.x * 4; n < N; n += blockDim.x * 4) {
+    float4 a = sum_splits(part + (long)m * N + n, (long)M * N, splits);
+    if (EPI == EPI_ADD_F32) {
+      const float4 r = *reinterpret_cast<const float4 *>(y + n);
+      a = make_float4(r.x + a.x, r.y + a.y, r.z + a.z, r.w + a.w);
+    }
+    *reinterpret_cast<float4 *>(y + n) = a;
+    *reinterpret_cast<float4 *>(row_sh + n) = a;
+    ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+  }
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)N + eps);
+  T *o = out + (long)m * N;
+  for (int n = threadIdx.x * 4; n < N; n += blockDim.x * 4) {
+    const float4 a = *reinterpret_cast<const float4 *>(row_sh + n);
+    Elem<T>::store(o, n, a.x * inv * Elem<T>::load(w, n));
+    Elem<T>::store(o, n + 1, a.y * inv * Elem<T>::load(w, n + 1));
+    Elem<T>::store(o, n + 2, a.z * inv * Elem<T>::load(w, n + 2));
+    Elem<T>::store(o, n + 3, a.w * inv * Elem<T>::load(w, n + 3));
+  }
+}
+
 // ------------------------------------------------------------------ float32
 struct GemmF {
   const float *X, *W;
@@ -375,9 +411,9 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
   return p;
 }
 
-void launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, const void *X, int ldx, const void *W,
-                 void *Y, long ldy, float *part, hipStream_t s, RowStat *tile_stats, float inv_t) {
-  if (M <= 0) return;
+int launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, const void *X, int ldx, const void *W,
+                void *Y, long ldy, float *part, hipStream_t s, RowStat *tile_stats, float inv_t, bool defer_reduce) {
+  if (M <= 0) return 1;
   if (dtype == GM_BF16) {
     const GemmPlan p = plan_gemm(dtype, epi, M, N, K);
     GemmS g{(const uint16_t *)X, (const uint16_t *)W, Y, part, ldy, M, N, K, ldx, p.Nw, p.n_tiles, p.m_tiles,
@@ -392,6 +428,7 @@ void launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, cons
         case EPI_STATS: launch_stream_shape<EPI_STATS>(p.shape, g, s); break;
       }
     }
+    if (p.splits > 1 && defer_reduce) return p.splits;
     if (p.splits > 1) {
       TraceScope ts("gemm_split_reduce", s);
       const long total = (long)M * (N / 4);
@@ -403,6 +440,7 @@ void launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, cons
         case EPI_SWIGLU: hipLaunchKernelGGL(gemm_reduce_kernel<EPI_SWIGLU>, dim3(blocks), dim3(256), 0, s, g); break;
       }
     }
+    return 1;
   } else {
     GemmF g{(const float *)X, (const float *)W, (float *)Y, ldy, M, N, K, ldx};
     const dim3 grid((N + 63) / 64, (M + 15) / 16), block(256);
@@ -412,7 +450,7 @@ void launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, cons
         hipLaunchKernelGGL(gemm_f32_kernel<EPI_STORE_F32>, grid, block, 0, s, g);
       }
       launch_tile_stats((const float *)Y, ldy, M, N, inv_t, tile_stats, s);
-      return;
+      return 1;
     }
     TraceScope ts(name, s);
     switch (epi) {
@@ -421,6 +459,32 @@ void launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, cons
       case EPI_STORE_ACT: hipLaunchKernelGGL(gemm_f32_kernel<EPI_STORE_ACT>, grid, block, 0, s, g); break;
       case EPI_SWIGLU: hipLaunchKernelGGL(gemm_f32_kernel<EPI_SWIGLU>, grid, block, 0, s, g); break;
     }
+  }
+  return 1;
+}
+
+void launch_reduce_norm(int dtype, int epi, int M, int N, int splits, const float *part, float *Y, const void *norm_w,
+                        float eps, void *out, hipStream_t s) {
+  if (M <= 0) return;
+  TraceScope ts("reduce_norm", s);
+  int threads = ((N / 4 + 63) / 64) * 64;   // one float4 column group per thread when N <= 4096
+  if (threads > 1024) threads = 1024;
+  const dim3 grid(M), block(threads);
+  const size_t lds = (size_t)N * sizeof(float);
+  if (dtype == GM_BF16) {
+    if (epi == EPI_ADD_F32)
+      hipLaunchKernelGGL((reduce_norm_kernel<bf16, EPI_ADD_F32>), grid, block, lds, s, M, N, splits, part, Y,
+                         (const bf16 *)norm_w, eps, (bf16 *)out);
+    else
+      hipLaunchKernelGGL((reduce_norm_kernel<bf16, EPI_STORE_F32>), grid, block, lds, s, M, N, splits, part, Y,
+                         (const bf16 *)norm_w, eps, (bf16 *)out);
+  } else {
+    if (epi == EPI_ADD_F32)
+      hipLaunchKernelGGL((reduce_norm_kernel<float, EPI_ADD_F32>), grid, block, lds, s, M, N, splits, part, Y,
+                         (const float *)norm_w, eps, (float *)out);
+    else
+      hipLaunchKernelGGL((reduce_norm_kernel<float, EPI_STORE_F32>), grid, block, lds, s, M, N, splits, part, Y,
+                         (const float *)norm_w, eps, (float *)out);
   }
 }
 

@@ -27,6 +27,31 @@ __global__ __launch_bounds__(256) void embed_kernel(int H, int V, const int32_t 
   for (int c = threadIdx.x; c < H; c += blockDim.x) xr[c] = Elem<T>::load(er, c);
 }
 
+// the embedding rows (float32 residual stream) and their RMSNorm in one pass
+template <typename T>
+__global__ __launch_bounds__(256) void embed_norm_kernel(int H, int V, const int32_t *__restrict__ tok,
+                                                         const T *__restrict__ E, float *__restrict__ x,
+                                                         const T *__restrict__ w, float eps, T *__restrict__ out,
+                                                         int32_t *dev_err) {
+  __shared__ float red[16];
+  const int r = blockIdx.x;
+  const int t = tok[r];
+  const bool ok = t >= 0 && t < V;
+  if (!ok && threadIdx.x == 0) raise_dev_err(dev_err, GM_DEVERR_TOKEN);
+  const T *er = E + (long)(ok ? t : 0) * H;
+  float *xr = x + (long)r * H;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < H; c += blockDim.x) {
+    const float v = ok ? Elem<T>::load(er, c) : 0.f;
+    xr[c] = v;
+    ss += v * v;
+  }
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)H + eps);
+  T *o = out + (long)r * H;
+  for (int c = threadIdx.x; c < H; c += blockDim.x) Elem<T>::store(o, c, xr[c] * inv * Elem<T>::load(w, c));
+}
+
 // one wave per row, four channels per lane and step (H % 4 == 0)
 template <typename T>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(int M, int H, float eps, const float *__restrict__ x,
@@ -111,16 +136,28 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
       s_in = off & 15;
     }
   }
-  const float *src_row = a.qkv + (long)row * nh * D;
+  // the projected row staged in LDS: qkv itself, or the sum of the GEMM's K-split
+  // partials (split order), read as float4 column groups by the whole block
+  extern __shared__ float row_sh[];   // [nh * D]
+  {
+    const int W = nh * D;
+    const long row_off = (long)row * W;
+    for (int c = threadIdx.x * 4; c < W; c += blockDim.x * 4) {
+      const float4 v = a.splits > 1 ? sum_splits(a.part + row_off + c, (long)a.M * W, a.splits)
+                                    : *reinterpret_cast<const float4 *>(a.qkv + row_off + c);
+      *reinterpret_cast<float4 *>(row_sh + c) = v;
+    }
+  }
+  __syncthreads();
+  auto ld = [&](int col) -> float { return row_sh[col]; };
   const T *qn = (const T *)a.q_norm, *kn = (const T *)a.k_norm;
   // the rotation of pair `lane` at this position, shared by every head of the row
   double sn = 0.0, cs = 1.0;
   if (lane < half) sincos(pos * pow((double)a.rope_base, -2.0 * lane / D), &sn, &cs);
   for (int hh = w; hh < nh; hh += 4) {
-    const float *src = src_row + hh * D;
     const int kind = hh < a.n_heads ? 0 : (hh < a.n_heads + a.n_kv ? 1 : 2);
     const bool act = lane < half;
-    float x1 = act ? src[lane] : 0.f, x2 = act ? src[lane + half] : 0.f;
+    float x1 = act ? ld(hh * D + lane) : 0.f, x2 = act ? ld(hh * D + lane + half) : 0.f;
     if (kind < 2 && qn) {
       const T *nw = kind == 0 ? qn : kn;
       const float ss = wave_sum(x1 * x1 + x2 * x2);
@@ -177,6 +214,18 @@ void launch_embed(int dtype, int M, int H, int V, const int32_t *tokens, const v
     hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, H, V, tokens, (const float *)E, x, dev_err);
 }
 
+void launch_embed_norm(int dtype, int M, int H, int V, const int32_t *tokens, const void *E, float *x,
+                       const void *norm_w, float eps, void *out, int32_t *dev_err, hipStream_t s) {
+  if (M <= 0) return;
+  TraceScope ts("embed_norm", s);
+  if (dtype == GM_BF16)
+    hipLaunchKernelGGL(embed_norm_kernel<bf16>, dim3(M), dim3(256), 0, s, H, V, tokens, (const bf16 *)E, x,
+                       (const bf16 *)norm_w, eps, (bf16 *)out, dev_err);
+  else
+    hipLaunchKernelGGL(embed_norm_kernel<float>, dim3(M), dim3(256), 0, s, H, V, tokens, (const float *)E, x,
+                       (const float *)norm_w, eps, (float *)out, dev_err);
+}
+
 void launch_rmsnorm(int dtype, int M, int H, float eps, const float *x, const void *w, void *out, hipStream_t s) {
   if (M <= 0) return;
   TraceScope ts("rmsnorm", s);
@@ -190,8 +239,9 @@ void launch_rmsnorm(int dtype, int M, int H, float eps, const float *x, const vo
 void launch_rope_append(const RopeArgs &a, hipStream_t s) {
   if (a.M <= 0) return;
   TraceScope ts("rope_append", s);
-  if (a.dtype == GM_BF16) hipLaunchKernelGGL(rope_append_kernel<bf16>, dim3(a.M), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(rope_append_kernel<float>, dim3(a.M), dim3(256), 0, s, a);
+  const size_t lds = (size_t)(a.n_heads + 2 * a.n_kv) * a.head_dim * sizeof(float);
+  if (a.dtype == GM_BF16) hipLaunchKernelGGL(rope_append_kernel<bf16>, dim3(a.M), dim3(256), lds, s, a);
+  else hipLaunchKernelGGL(rope_append_kernel<float>, dim3(a.M), dim3(256), lds, s, a);
 }
 
 void launch_mtp_input(int dtype, int M, int H, int V, float eps, const float *h, const int32_t *tok, int tok_stride,

@@ -67,7 +67,8 @@ typedef enum {
  * (App. "Models and Draft Heads").  Limits of this build: head_dim 128 for
  * GM_BF16 (64 or 128 for GM_F32), n_heads a multiple of n_kv_heads with
  * (n_heads / n_kv_heads) * (k + 1) <= 64, hidden and ffn multiples of 64,
- * hidden and (n_heads + 2 n_kv_heads) * head_dim at most 16384;
+ * hidden and (n_heads + 2 n_kv_heads) * head_dim at most 16384, vocab at
+ * most 524288 (also the limit of gm_spec_accept's V);
  * GM_BF16 needs vocab a multiple of 128 and hidden, ffn and
  * n_heads * head_dim multiples of 256. */
 typedef struct {

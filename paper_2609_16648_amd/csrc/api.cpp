@@ -62,6 +62,7 @@ gm_status check_config(const gm_model_config *cfg, int B, int k) {
   if (G * (k + 1) > kAttnMaxRows)
     return fail(GM_ERR_UNSUPPORTED, "(n_heads / n_kv_heads) * (k + 1) = %d exceeds %d", G * (k + 1), kAttnMaxRows);
   if (cfg->hidden % 64 || cfg->ffn % 64) return fail(GM_ERR_UNSUPPORTED, "hidden and ffn must be multiples of 64");
+  if (cfg->vocab > kMaxVocab) return fail(GM_ERR_UNSUPPORTED, "vocab %d exceeds %d", cfg->vocab, kMaxVocab);
   // row kernels stage one hidden row or one projected q/k/v row in 64 KiB of LDS
   if (cfg->hidden > kMaxRowFloats || (cfg->n_heads + 2 * cfg->n_kv_heads) * cfg->head_dim > kMaxRowFloats)
     return fail(GM_ERR_UNSUPPORTED, "hidden and (n_heads + 2 n_kv_heads) * head_dim must be at most %d", kMaxRowFloats);
@@ -139,6 +140,7 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
                                     const float *u_final, int32_t *n_accept, int32_t *out_tokens, void *ws,
                                     size_t ws_bytes, void *stream) {
   if (B < 0 || k < 0 || k > kMaxK || V < 1) return fail(GM_ERR_INVALID_ARG, "bad B=%d k=%d V=%d", B, k, V);
+  if (V > kMaxVocab) return fail(GM_ERR_UNSUPPORTED, "vocab %d exceeds %d", V, kMaxVocab);
   if (mode != GM_GREEDY && mode != GM_SAMPLE) return fail(GM_ERR_INVALID_ARG, "unknown accept mode %d", mode);
   if (!(temperature > 0.f)) return fail(GM_ERR_INVALID_ARG, "temperature must be > 0");
   if (B == 0) return GM_OK;

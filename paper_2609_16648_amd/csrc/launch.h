@@ -48,6 +48,7 @@ inline int scan_chunks(int V) { return (V + kScanChunk - 1) / kScanChunk; }
 // form the LM-head GEMM epilogue emits; a draw from such a row needs no
 // further pass over the vocabulary.
 constexpr int kTileIds = 128;
+constexpr int kMaxVocab = 4096 * kTileIds;   // the draw stages a row's tile statistics in 64 KiB of LDS
 inline int vocab_tiles(int V) { return (V + kTileIds - 1) / kTileIds; }
 // tile statistics by a pass over rows of logits (paths without the GEMM epilogue)
 void launch_tile_stats(const float *logits, long row_stride, int n_rows, int V, float inv_t, RowStat *tiles,

@@ -113,84 +113,136 @@ __device__ __forceinline__ void combine_stats(const RowStat *st, int nch, double
 }
 
 // ------------------------------------------------------------------ 2. accept decision
-__global__ void accept_decide_kernel(int B, int k, int V, int mode, float inv_t,
-                                     const float *__restrict__ tlog, const float *__restrict__ dlog,
-                                     const RowStat *__restrict__ tstat, const RowStat *__restrict__ dstat,
-                                     int nch, const int32_t *__restrict__ drafts,
-                                     const float *__restrict__ u_acc, const float *__restrict__ u_fin,
-                                     int32_t *__restrict__ n_out, int32_t *__restrict__ out_tokens,
-                                     RowSel *__restrict__ sel) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= B) return;
+// One wave per sequence.  Lane r <= k combines the chunk statistics of target
+// row r, lane k + 1 + r those of draft row r; lane i < k then evaluates the
+// test for draft i (all in parallel), and the first failing lane is the first
+// rejection (the rule stops there, so later tests are not looked at).
+__global__ __launch_bounds__(64) void accept_decide_kernel(int B, int k, int V, int mode, float inv_t,
+                                                           const float *__restrict__ tlog,
+                                                           const float *__restrict__ dlog,
+                                                           const RowStat *__restrict__ tstat,
+                                                           const RowStat *__restrict__ dstat, int nch,
+                                                           const int32_t *__restrict__ drafts,
+                                                           const float *__restrict__ u_acc,
+                                                           const float *__restrict__ u_fin,
+                                                           int32_t *__restrict__ n_out, int32_t *__restrict__ out_tokens,
+                                                           RowSel *__restrict__ sel) {
+  const int b = blockIdx.x, lane = threadIdx.x;
   const int k1 = k + 1;
-  int n = 0;
-  RowSel rs;
-  rs.active = 0;
-  rs.q_row = nullptr;
-  rs.mq = 0.0;
-  rs.sq = 1.0;
-  rs.pad = 0;
-  if (mode == GM_GREEDY) {
-    double M, S;
-    int am = 0;
-    for (; n < k; ++n) {
-      combine_stats(tstat + (long)(b * k1 + n) * nch, nch, M, S, am);
-      if (drafts[b * k + n] != am) break;
-    }
-    if (n == k) combine_stats(tstat + (long)(b * k1 + k) * nch, nch, M, S, am);
-    out_tokens[b * k1 + n] = am;
-  } else {
-    for (; n < k; ++n) {
-      const int d = drafts[b * k + n];
-      if (d < 0 || d >= V) break;
-      double Mt, St, Mq, Sq;
-      int am;
-      combine_stats(tstat + (long)(b * k1 + n) * nch, nch, Mt, St, am);
-      combine_stats(dstat + (long)(b * k + n) * nch, nch, Mq, Sq, am);
-      const double zt = (double)(tlog[(long)(b * k1 + n) * V + d] * inv_t);
-      const double zq = (double)(dlog[(long)(b * k + n) * V + d] * inv_t);
-      const double p = exp(zt - Mt) / St;
+  // this lane's row: target rows 0..k, then draft rows 0..k-1 (sampling only)
+  const bool is_t = lane < k1, is_d = mode != GM_GREEDY && lane >= k1 && lane < k1 + k;
+  double M = 0.0, S = 1.0;
+  int am = 0;
+  if (is_t || is_d) {
+    const RowStat *st = is_t ? tstat + (long)(b * k1 + lane) * nch : dstat + (long)(b * k + lane - k1) * nch;
+    combine_stats(st, nch, M, S, am);
+  }
+  // the draft row statistics moved to the lane of the same position
+  const double Mq = __shfl(M, k1 + lane < 64 ? k1 + lane : lane, kWave);
+  const double Sq = __shfl(S, k1 + lane < 64 ? k1 + lane : lane, kWave);
+  bool ok = false;   // lane i < k: draft i passes its test
+  int d = -1;
+  if (lane < k) {
+    d = drafts[b * k + lane];
+    if (mode == GM_GREEDY) {
+      ok = d == am;
+    } else if (d >= 0 && d < V) {
+      const double zt = (double)(tlog[(long)(b * k1 + lane) * V + d] * inv_t);
+      const double zq = (double)(dlog[(long)(b * k + lane) * V + d] * inv_t);
+      const double p = exp(zt - M) / S;
       const double q = exp(zq - Mq) / Sq;
       const float ratio = q > 0.0 ? (float)(p / q) : INFINITY;
-      if (!(u_acc[b * k + n] < ratio)) break;
+      ok = u_acc[b * k + lane] < ratio;
     }
-    int am;
-    rs.p_row = tlog + (long)(b * k1 + n) * V;
-    combine_stats(tstat + (long)(b * k1 + n) * nch, nch, rs.mp, rs.sp, am);
-    if (n < k) {
-      rs.q_row = dlog + (long)(b * k + n) * V;
-      combine_stats(dstat + (long)(b * k + n) * nch, nch, rs.mq, rs.sq, am);
-    }
-    rs.u = (double)u_fin[b];
-    rs.dst = out_tokens + b * k1 + n;
-    rs.active = 1;
   }
-  for (int i = 0; i < n; ++i) out_tokens[b * k1 + i] = drafts[b * k + i];
-  for (int i = n + 1; i < k1; ++i) out_tokens[b * k1 + i] = -1;
-  n_out[b] = n;
-  sel[b] = rs;
+  const unsigned long long fail = __ballot(lane < k && !ok);
+  const int n = fail ? __ffsll((long long)fail) - 1 : k;
+  // lane n holds the statistics of target row n (and of draft row n, n < k)
+  const double mp = __shfl(M, n, kWave), sp = __shfl(S, n, kWave);
+  const double mq = __shfl(Mq, n, kWave), sq = __shfl(Sq, n, kWave);
+  const int am_n = __shfl(am, n, kWave);
+  if (lane < k1) {
+    int tok = -1;
+    if (lane < n) tok = d;
+    else if (lane == n && mode == GM_GREEDY) tok = am_n;
+    if (lane != n || mode == GM_GREEDY) out_tokens[b * k1 + lane] = tok;
+  }
+  if (lane == 0) {
+    n_out[b] = n;
+    RowSel rs;
+    rs.active = 0;
+    rs.q_row = nullptr;
+    rs.mq = 0.0;
+    rs.sq = 1.0;
+    rs.pad = 0;
+    rs.p_row = tlog + (long)(b * k1 + n) * V;
+    rs.mp = mp;
+    rs.sp = sp;
+    rs.u = 0.0;
+    rs.dst = out_tokens + b * k1 + n;
+    if (mode != GM_GREEDY) {
+      if (n < k) {
+        rs.q_row = dlog + (long)(b * k + n) * V;
+        rs.mq = mq;
+        rs.sq = sq;
+      }
+      rs.u = (double)u_fin[b];
+      rs.active = 1;
+    }
+    sel[b] = rs;
+  }
 }
 
 void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const float *tlog,
                           const float *dlog, const RowStat *tstat, const RowStat *dstat,
                           const int32_t *drafts, const float *u_accept, const float *u_final,
                           int32_t *n_accept, int32_t *out_tokens, RowSel *sel, hipStream_t s) {
+  if (B <= 0) return;
   TraceScope ts("accept_decide", s);
-  hipLaunchKernelGGL(accept_decide_kernel, dim3((B + 63) / 64), dim3(64), 0, s, B, k, V, mode, inv_t,
-                     tlog, dlog, tstat, dstat, stat_chunks(V), drafts, u_accept, u_final, n_accept,
-                     out_tokens, sel);
+  hipLaunchKernelGGL(accept_decide_kernel, dim3(B), dim3(64), 0, s, B, k, V, mode, inv_t, tlog, dlog, tstat, dstat,
+                     stat_chunks(V), drafts, u_accept, u_final, n_accept, out_tokens, sel);
 }
 
 // ------------------------------------------------------------------ 3. inverse-CDF draw
-// weight of id x: max(0, p(x) - q(x)) with q, p(x) without.  Each exponential is a
+// Weight of id x: max(0, p(x) - q(x)) with q, p(x) without.  Each exponential is a
 // float32 expf of z / T - max (both float32); scaling by the float64 normaliser
 // and every sum are float64.
-__device__ __forceinline__ double draw_weight(const RowSel &s, int x, float inv_t, bool use_p, double isp,
-                                              double isq) {
-  const double p = (double)expf(s.p_row[x] * inv_t - (float)s.mp) * isp;
-  if (use_p || s.q_row == nullptr) return p;
-  const double q = (double)expf(s.q_row[x] * inv_t - (float)s.mq) * isq;
-  return fmax(p - q, 0.0);
+// z / T - max for kScanPer consecutive ids of one row (float4 loads when the row allows)
+__device__ __forceinline__ void load_run(const float *row, int x0, int V, float inv_t, float mx,
+                                         float (&z)[kScanPer]) {
+  if ((V & 3) == 0 && x0 + kScanPer <= V) {
+#pragma unroll
+    for (int j = 0; j < kScanPer; j += 4) {
+      const float4 f = *reinterpret_cast<const float4 *>(row + x0 + j);
+      z[j] = f.x * inv_t - mx;
+      z[j + 1] = f.y * inv_t - mx;
+      z[j + 2] = f.z * inv_t - mx;
+      z[j + 3] = f.w * inv_t - mx;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) z[j] = x0 + j < V ? row[x0 + j] * inv_t - mx : -INFINITY;
+  }
+}
+
+// the kScanPer draw weights of one thread's run (max(0, p - q), or p alone) and their p
+__device__ __forceinline__ void run_weights(const RowSel &s, int x0, int V, float inv_t, bool use_p, double isp,
+                                            double isq, double (&w)[kScanPer], double &psum) {
+  float zp[kScanPer], zq[kScanPer];
+  load_run(s.p_row, x0, V, inv_t, (float)s.mp, zp);
+  const bool with_q = !use_p && s.q_row != nullptr;
+  if (with_q) load_run(s.q_row, x0, V, inv_t, (float)s.mq, zq);
+  psum = 0.0;
+#pragma unroll
+  for (int j = 0; j < kScanPer; ++j) {
+    const double px = x0 + j < V ? (double)expf(zp[j]) * isp : 0.0;
+    psum += px;
+    w[j] = px;
+    if (with_q) {
+      const double qx = x0 + j < V ? (double)expf(zq[j]) * isq : 0.0;
+      w[j] = fmax(px - qx, 0.0);
+    }
+  }
 }
 
 // per-thread sums over kScanPer consecutive ids, then a serial sum over the
@@ -205,16 +257,11 @@ __global__ __launch_bounds__(kScanThreads) void residual_chunk_kernel(int V, flo
   if (!s.active) return;
   const int x0 = c * kScanChunk + tid * kScanPer;
   const double isp = 1.0 / s.sp, isq = 1.0 / s.sq;
-  double w = 0.0, p = 0.0;
-  for (int j = 0; j < kScanPer; ++j) {
-    const int x = x0 + j;
-    if (x < V) {
-      const double px = (double)expf(s.p_row[x] * inv_t - (float)s.mp) * isp;
-      const double qx = s.q_row ? (double)expf(s.q_row[x] * inv_t - (float)s.mq) * isq : 0.0;
-      w += s.q_row ? fmax(px - qx, 0.0) : px;
-      p += px;
-    }
-  }
+  double wv[kScanPer], p = 0.0;
+  run_weights(s, x0, V, inv_t, false, isp, isq, wv, p);
+  double w = 0.0;
+#pragma unroll
+  for (int j = 0; j < kScanPer; ++j) w += wv[j];
   sw[tid] = w;
   sp[tid] = p;
   __syncthreads();
@@ -230,20 +277,26 @@ __global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, floa
                                                                      const RowSel *__restrict__ sel, int nch,
                                                                      const double *__restrict__ wsum,
                                                                      const double *__restrict__ psum) {
+  extern __shared__ double chunk_sh[];   // [2 nch]: residual masses, then p masses
   __shared__ double st[kScanThreads];
   __shared__ double sh_t, sh_base;
   __shared__ int sh_chunk, sh_thread, sh_use_p, sh_found;
   const int b = blockIdx.x, tid = threadIdx.x;
   const RowSel s = sel[b];
   if (!s.active) return;
+  for (int c = tid; c < nch; c += kScanThreads) {   // all chunk masses in flight at once
+    chunk_sh[c] = wsum[(long)b * nch + c];
+    chunk_sh[nch + c] = psum[(long)b * nch + c];
+  }
+  __syncthreads();
   if (tid == 0) {
-    const double *W = wsum + (long)b * nch;
+    const double *W = chunk_sh;
     double Z = 0.0;
     for (int c = 0; c < nch; ++c) Z += W[c];
     int use_p = 0;
     if (!(Z > 0.0)) {          // no residual mass: draw from p
       use_p = 1;
-      W = psum + (long)b * nch;
+      W = chunk_sh + nch;
       Z = 0.0;
       for (int c = 0; c < nch; ++c) Z += W[c];
     }
@@ -271,9 +324,11 @@ __global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, floa
   const bool use_p = sh_use_p != 0;
   const double isp = 1.0 / s.sp, isq = 1.0 / s.sq;
   const int x0 = cs * kScanChunk + tid * kScanPer;
+  double wv[kScanPer], pdummy;
+  run_weights(s, x0, V, inv_t, use_p, isp, isq, wv, pdummy);
   double w = 0.0;
-  for (int j = 0; j < kScanPer; ++j)
-    if (x0 + j < V) w += draw_weight(s, x0 + j, inv_t, use_p, isp, isq);
+#pragma unroll
+  for (int j = 0; j < kScanPer; ++j) w += wv[j];
   st[tid] = w;
   __syncthreads();
   if (tid == 0) {
@@ -293,13 +348,14 @@ __global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, floa
   if (tid == sh_thread) {
     double acc = sh_base;
     int x_last = -1, x_hit = -1;
+#pragma unroll
     for (int j = 0; j < kScanPer; ++j) {
       const int x = x0 + j;
-      if (x >= V) break;
-      const double wx = draw_weight(s, x, inv_t, use_p, isp, isq);
-      if (wx > 0.0) x_last = x;
-      acc += wx;
-      if (sh_found && x_hit < 0 && acc > sh_t) x_hit = x;
+      if (x < V) {
+        if (wv[j] > 0.0) x_last = x;
+        acc += wv[j];
+        if (sh_found && x_hit < 0 && acc > sh_t) x_hit = x;
+      }
     }
     *s.dst = x_hit >= 0 ? x_hit : (x_last >= 0 ? x_last : (x0 < V ? x0 : V - 1));
   }
@@ -315,8 +371,8 @@ void launch_residual_draw(const char *chunk_name, const char *scan_name, int B, 
   }
   {
     TraceScope ts(scan_name, s);
-    hipLaunchKernelGGL(residual_scan_kernel, dim3(B), dim3(kScanThreads), 0, s, V, inv_t, sel, nch, wsum,
-                       psum);
+    hipLaunchKernelGGL(residual_scan_kernel, dim3(B), dim3(kScanThreads), 2 * nch * sizeof(double), s, V, inv_t,
+                       sel, nch, wsum, psum);
   }
 }
 
@@ -392,27 +448,60 @@ void launch_tile_stats(const float *logits, long row_stride, int n_rows, int V, 
                      nt, tiles);
 }
 
-// One block per row.  The row's max and arg-max come from its tile statistics;
-// a sampled draw accumulates the tile masses s_t exp(m_t - M) in float64 in
-// ascending tile order to find the tile holding u * S, then one wave scans
+// Inclusive prefix sum of one double per thread over the block (256 threads).
+__device__ __forceinline__ double block_incl_scan(double v, double *wsum /* >= 4 */) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double n = __shfl_up(v, o, kWave);
+    if (lane >= o) v += n;
+  }
+  if (lane == 63) wsum[wid] = v;
+  __syncthreads();
+  double off = 0.0;
+  for (int w = 0; w < wid; ++w) off += wsum[w];
+  return off + v;
+}
+
+// One block per row.  The row's max and arg-max come from its tile statistics
+// (staged in LDS, all loads in flight at once); a sampled draw takes the tile
+// masses s_t exp(m_t - M) in float64, contiguous runs of them per thread, a
+// block-wide prefix sum over the runs, and the first run whose prefix passes
+// u * S is walked tile by tile to the tile holding u * S.  One wave then scans
 // that tile's 128 ids (the same per-id terms exp(z / T - m_t) the tile sums
 // were made of, scaled in float64) for the first running sum above u * S.
 __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float inv_t, const float *__restrict__ logits,
                                                         long row_stride, const RowStat *__restrict__ tiles,
                                                         int n_tiles, const float *__restrict__ u, int u_stride,
                                                         int32_t *__restrict__ dst, int dst_stride) {
-  __shared__ double seg[256];
+  extern __shared__ uint4 st_raw[];   // [n_tiles] RowStat
+  RowStat *st = reinterpret_cast<RowStat *>(st_raw);
   __shared__ float red_m[4];
   __shared__ int red_a[4];
+  __shared__ double wsum[4];
   __shared__ double sh_base, sh_t;
-  __shared__ int sh_tile;
+  __shared__ int sh_tile, sh_hit, sh_last;
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const RowStat *st = tiles + (long)b * n_tiles;
+  const uint4 *src = reinterpret_cast<const uint4 *>(tiles + (long)b * n_tiles);
   float m = -INFINITY;
   int a = 0x7fffffff;
-  for (int t = tid; t < n_tiles; t += 256) {
-    const RowStat s = st[t];
-    if (s.max > m || (s.max == m && s.argmax < a)) { m = s.max; a = s.argmax; }
+  for (int t0 = tid; t0 < n_tiles; t0 += 256 * 8) {
+    uint4 v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int t = t0 + 256 * q;
+      v[q] = t < n_tiles ? src[t] : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int t = t0 + 256 * q;
+      if (t < n_tiles) {
+        st_raw[t] = v[q];
+        const float tm = __uint_as_float(v[q].x);
+        const int ta = (int)v[q].y;
+        if (tm > m || (tm == m && ta < a)) { m = tm; a = ta; }
+      }
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -421,6 +510,7 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
     if (om > m || (om == m && oa < a)) { m = om; a = oa; }
   }
   if (lane == 0) { red_m[wid] = m; red_a[wid] = a; }
+  if (tid == 0) { sh_hit = 256; sh_last = -1; }
   __syncthreads();
   m = red_m[0];
   a = red_a[0];
@@ -434,32 +524,23 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
   const int per = (n_tiles + 255) / 256, t0 = tid * per, t1 = min(n_tiles, t0 + per);
   double w = 0.0;
   for (int t = t0; t < t1; ++t) w += st[t].sum * exp((double)st[t].max - M);
-  seg[tid] = w;
+  const double incl = block_incl_scan(w, wsum);
+  const double S = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+  const double target = (double)u[(long)b * u_stride] * S;
+  if (incl > target) atomicMin(&sh_hit, tid);   // first run whose prefix passes u * S
+  if (w > 0.0) atomicMax(&sh_last, tid);       // last run with mass (rounding fallback)
   __syncthreads();
-  if (tid == 0) {
-    double S = 0.0;
-    for (int i = 0; i < 256; ++i) S += seg[i];
-    const double target = (double)u[(long)b * u_stride] * S;
-    double acc = 0.0;
-    int tile = -1, last = 0;
-    for (int i = 0; i < 256 && tile < 0; ++i) {
-      if (seg[i] > 0.0) last = i;
-      if (acc + seg[i] > target) {
-        for (int t = i * per; t < min(n_tiles, (i + 1) * per); ++t) {
-          const double W = st[t].sum * exp((double)st[t].max - M);
-          if (acc + W > target) { tile = t; break; }
-          acc += W;
-        }
-        if (tile < 0) tile = min(n_tiles, (i + 1) * per) - 1;   // rounding: end of this segment
-      } else {
-        acc += seg[i];
-      }
+  const int hit = sh_hit, th = hit < 256 ? hit : (sh_last >= 0 ? sh_last : 255);
+  if (tid == th) {
+    double acc = incl - w;
+    int tile = -1;
+    for (int t = t0; t < t1; ++t) {
+      const double W = st[t].sum * exp((double)st[t].max - M);
+      if (hit < 256 && acc + W > target) { tile = t; break; }
+      if (hit >= 256 && t == t1 - 1) { tile = t; break; }   // past the end: last tile of the last run
+      acc += W;
     }
-    if (tile < 0) {   // rounding put u * S past the end: last tile of the last segment with mass
-      tile = min(n_tiles, (last + 1) * per) - 1;
-      acc = 0.0;
-      for (int t = 0; t < tile; ++t) acc += st[t].sum * exp((double)st[t].max - M);
-    }
+    if (tile < 0) { tile = t1 > t0 ? t1 - 1 : n_tiles - 1; }   // rounding inside the run: its last tile
     sh_tile = tile;
     sh_base = acc;
     sh_t = target;
@@ -473,19 +554,19 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
   const int xa = tile * kTileIds + 2 * lane, xb = xa + 1;
   const double ea = xa < V ? (double)expf(row[xa] * inv_t - mt) * scale : 0.0;
   const double eb = xb < V ? (double)expf(row[xb] * inv_t - mt) * scale : 0.0;
-  double incl = ea + eb;
+  double incl2 = ea + eb;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
-    const double n = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += n;
+    const double n = __shfl_up(incl2, o, kWave);
+    if (lane >= o) incl2 += n;
   }
-  double excl = __shfl_up(incl, 1, kWave);
+  double excl = __shfl_up(incl2, 1, kWave);
   if (lane == 0) excl = 0.0;
   const double acc_a = sh_base + excl + ea, acc_b = acc_a + eb;
-  const unsigned long long hit = __ballot(acc_a > sh_t || acc_b > sh_t);
+  const unsigned long long hitm = __ballot(acc_a > sh_t || acc_b > sh_t);
   const unsigned long long nz = __ballot(ea > 0.0 || eb > 0.0);
   // the first hit lane decides between its two ids (running sums grow along lanes)
-  const int first = hit ? __ffsll((long long)hit) - 1 : -1;
+  const int first = hitm ? __ffsll((long long)hitm) - 1 : -1;
   const int lastnz = nz ? 63 - __clzll((long long)nz) : -1;
   if (first >= 0 && lane == first) dst[(long)b * dst_stride] = acc_a > sh_t ? xa : xb;
   if (first < 0 && lastnz >= 0 && lane == lastnz) dst[(long)b * dst_stride] = eb > 0.0 ? xb : xa;
@@ -496,8 +577,8 @@ void launch_tile_draw(int B, int V, int mode, float inv_t, const float *logits, 
                       const float *u, int u_stride, int32_t *dst, int dst_stride, hipStream_t s) {
   if (B <= 0) return;
   TraceScope ts("draft_draw", s);
-  hipLaunchKernelGGL(tile_draw_kernel, dim3(B), dim3(256), 0, s, V, mode, inv_t, logits, row_stride, tiles,
-                     vocab_tiles(V), u, u_stride, dst, dst_stride);
+  hipLaunchKernelGGL(tile_draw_kernel, dim3(B), dim3(256), (size_t)vocab_tiles(V) * sizeof(RowStat), s, V, mode,
+                     inv_t, logits, row_stride, tiles, vocab_tiles(V), u, u_stride, dst, dst_stride);
 }
 
 }  // namespace gm

@@ -32,11 +32,18 @@ struct GemmS {
   long ldy;
   int M, N, K, ldx;   // N: output columns (features for SwiGLU); Nw: weight rows
   int Nw, n_tiles, m_tiles, splits, k_iters;
-  RowStat *stats;     // EPI_STATS: [M][Nw / 128] tile statistics of Y / T
+  RowStat *stats;     // EPI_STATS: [M][Nw / kTileIds] tile statistics of Y / T
   float inv_t;
 };
 
 __device__ __forceinline__ float silu(float x) { return x / (1.f + expf(-x)); }
+
+constexpr int kGemmThreads = 5 * kWave;   // four compute waves and one A-staging wave
+constexpr int kGemmBufs = 3;              // A chunks in LDS (the loader runs two ahead)
+// s_waitcnt immediates (gfx9 encoding: vmcnt bits 3:0 and 15:14, expcnt 6:4,
+// lgkmcnt 11:8; the other counters left at their maximum, i.e. not waited on)
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int kVmcnt0 = waitcnt_vm(0);
 
 // logical tile index of workgroup `bid`: workgroups are dealt round-robin to
 // the 8 XCDs; consecutive logical indices (same weight strip) share an XCD
@@ -45,21 +52,29 @@ __device__ __forceinline__ int xcd_remap(int bid, int T) {
   return x * q + (x < rem ? x : rem) + slot;
 }
 
-// MT: 16-row tiles per wave; NT: 16-column strips per wave; WM: waves along M (1 or 2)
+// MT: 16-row tiles per compute wave; NT: 16-column strips per compute wave;
+// WM: compute waves along M (1 or 2).  Waves 0-3 compute; wave 4 only stages
+// the A chunks in LDS.  The wait counter of loads is per wave, so the loader's
+// waits for A never drain the compute waves' weight ring.
 template <int MT, int NT, int WM, int EPI>
-__global__ __launch_bounds__(256) void gemm_stream_kernel(GemmS g) {
+__global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
   constexpr int WN = 4 / WM;
   constexpr int BM = 16 * MT * WM;            // rows per workgroup
-  constexpr int BKA = 16384 / BM;             // k per LDS chunk of A (32 KiB)
+  constexpr int BKA = 8192 / BM;              // k per LDS chunk of A (16 KiB)
   constexpr int SPC = BKA / 32;               // k32 steps per chunk
   constexpr int D = NT >= 4 ? 4 : 8;          // W prefetch depth (k32 steps)
+  static_assert(EPI != EPI_STATS || 16 * NT * WN == kTileIds, "tile statistics cover one workgroup's columns");
   constexpr int ITER = D > SPC ? D : SPC;     // k32 steps per unrolled iteration
-  constexpr int LDA = BKA + 8;
-  constexpr int AL = BM * BKA / 8 / 256;      // 16-byte A loads per thread per chunk
+  constexpr int CB = BKA / 8;                 // 16-byte column blocks per A row of a chunk
+  constexpr int SWZ = CB < 16 ? CB - 1 : 15;  // XOR swizzle of the column block by the row
+  constexpr int AL = BM * BKA / 8 / kWave;    // 1 KiB direct-to-LDS loads per chunk
+  constexpr int kVmcntAL = waitcnt_vm(AL);
   static_assert(ITER % SPC == 0 && ITER % D == 0, "unroll must cover whole chunks and ring turns");
-  __shared__ uint16_t As[2][BM * LDA];
+  // A chunk: row r, column block p of LDS holds X[r][8 (p ^ (r & SWZ)) ...]
+  __shared__ uint16_t As[kGemmBufs][BM * BKA];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // 4: the loader wave
   const int wm = w % WM, wn = w / WM;
   const int j = lane & 15, g4 = lane >> 4;
   const int T = g.n_tiles * g.m_tiles * g.splits;
@@ -67,10 +82,11 @@ __global__ __launch_bounds__(256) void gemm_stream_kernel(GemmS g) {
   const int mt = L % g.m_tiles, rest = L / g.m_tiles;
   const int ks = rest % g.splits, nt = rest / g.splits;
   const int m0 = mt * BM;
-  // this split's k range, in whole unrolled iterations
+  // this split's k range, in whole unrolled iterations (at least one)
   const int it0 = (int)((long)g.k_iters * ks / g.splits), it1 = (int)((long)g.k_iters * (ks + 1) / g.splits);
   const int k_begin = it0 * ITER * 32, k_end = it1 * ITER * 32;
   const int nsteps = (k_end - k_begin) / 32;
+  const int nchunks = nsteps / SPC;
 
   // weight strips of this wave: strip index (16-row groups of W)
   int strip[NT];
@@ -84,28 +100,6 @@ __global__ __launch_bounds__(256) void gemm_stream_kernel(GemmS g) {
       strip[t] = (nt * WN + wn) * NT + t;
     }
   }
-  const int kt_total = g.K / 32;
-  const uint16_t *wbase[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) wbase[t] = g.W + ((long)strip[t] * kt_total + k_begin / 32) * 512 + lane * 8;
-
-  // A chunk loader
-  uint4 ra[AL];
-  auto load_a = [&](int chunk_k) {
-#pragma unroll
-    for (int u = 0; u < AL; ++u) {
-      const int c = tid + 256 * u, row = c / (BKA / 8), col = (c % (BKA / 8)) * 8;
-      ra[u] = (m0 + row < g.M) ? *reinterpret_cast<const uint4 *>(g.X + (long)(m0 + row) * g.ldx + chunk_k + col)
-                               : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto store_a = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < AL; ++u) {
-      const int c = tid + 256 * u, row = c / (BKA / 8), col = (c % (BKA / 8)) * 8;
-      *reinterpret_cast<uint4 *>(&As[buf][row * LDA + col]) = ra[u];
-    }
-  };
 
   floatx4_t acc[MT][NT];
 #pragma unroll
@@ -113,52 +107,82 @@ __global__ __launch_bounds__(256) void gemm_stream_kernel(GemmS g) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[a][t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  // prime the weight ring and the first A chunk
-  uint4 ring[D][NT];
+  // Barrier c (c = 0 .. nchunks) closes "loader stored chunk c" and "compute
+  // finished chunk c - 1".  Chunk c lives in As[c % 3]; the buffer was last used
+  // by chunk c - 3, finished before barrier c - 2, so the loader starts chunk c
+  // right after barrier c - 2 and has two chunks of compute time to land it.
+  if (w == 4) {
+    // Direct-to-LDS loads: lane l of load u fills the 16 bytes at u KiB + 16 l of the
+    // chunk, i.e. row e / CB, block e % CB (e = 64 u + l); the lane fetches the
+    // global block that the swizzle puts there.  No registers hold A, and this
+    // wave's own waits (before each barrier) are the only ones A costs.
+    auto issue = [&](int c) {
+      const int chunk_k = k_begin + c * BKA;
+      uint16_t *dst = &As[c % kGemmBufs][0];
 #pragma unroll
-  for (int s = 0; s < D; ++s)
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-      ring[s][t] = s < nsteps ? *reinterpret_cast<const uint4 *>(wbase[t] + (long)s * 512) : make_uint4(0, 0, 0, 0);
-  if (nsteps > 0) {
-    load_a(k_begin);
-    store_a(0);
-    __syncthreads();
-    if (SPC < nsteps) load_a(k_begin + BKA);
-  }
-
-  for (int s0 = 0; s0 < nsteps; s0 += ITER) {
-#pragma unroll
-    for (int u = 0; u < ITER; ++u) {
-      const int s = s0 + u;                 // global k32 step
-      const int buf = (s / SPC) & 1;
-      const int ko = (u % SPC) * 32;        // offset inside the chunk
-      uint4 wv[NT];
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        wv[t] = ring[u % D][t];
-        if (s + D < nsteps) ring[u % D][t] = *reinterpret_cast<const uint4 *>(wbase[t] + (long)(s + D) * 512);
+      for (int u = 0; u < AL; ++u) {   // rows past M re-read row M - 1 (never stored)
+        const int e = lane + kWave * u, row = e / CB, p = e % CB;
+        const uint16_t *src = g.X + (long)min(m0 + row, g.M - 1) * g.ldx + chunk_k + 8 * (p ^ (row & SWZ));
+        __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)(dst + u * 512), 16, 0, 0);
       }
-      bf16x8_t af[MT];
+    };
+    issue(0);
+    if (nchunks > 1) issue(1);
+    for (int c = 0; c < nchunks; ++c) {
+      // chunk c landed: at most the AL loads of chunk c + 1 still in flight
+      if (c + 1 < nchunks) __builtin_amdgcn_s_waitcnt(kVmcntAL);
+      else __builtin_amdgcn_s_waitcnt(kVmcnt0);
+      __builtin_amdgcn_s_barrier();   // barrier c
+      if (c + 2 < nchunks) issue(c + 2);
+    }
+    __builtin_amdgcn_s_barrier();     // barrier nchunks
+  } else {
+    // The weight ring is loaded unconditionally (indices clamped to the last
+    // step, a re-read near the end), so the loop is one straight path: every
+    // wait counts exactly the loads still in flight and the ring stays full
+    // across iterations and chunk barriers.
+    const int kt_total = g.K / 32;
+    const uint16_t *wbase[NT];
 #pragma unroll
-      for (int a = 0; a < MT; ++a)
-        af[a] = as_bf16x8(*reinterpret_cast<const uint4 *>(&As[buf][(wm * 16 * MT + 16 * a + j) * LDA + ko + 8 * g4]));
+    for (int t = 0; t < NT; ++t) wbase[t] = g.W + ((long)strip[t] * kt_total + k_begin / 32) * 512 + lane * 8;
+    uint4 ring[D][NT];
 #pragma unroll
-      for (int a = 0; a < MT; ++a)
+    for (int s = 0; s < D; ++s)
 #pragma unroll
-        for (int t = 0; t < NT; ++t)
-          acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], as_bf16x8(wv[t]), acc[a][t], 0, 0, 0);
-      if ((u % SPC) == SPC - 1) {           // end of an A chunk: rotate the double buffer
-        const int next = s + 1;             // first step of the next chunk
-        if (next < nsteps) {
-          store_a(buf ^ 1);
-          __syncthreads();
-          if (next + SPC < nsteps) load_a(k_begin + (next + SPC) * 32);
+      for (int t = 0; t < NT; ++t)
+        ring[s][t] = *reinterpret_cast<const uint4 *>(wbase[t] + (long)min(s, nsteps - 1) * 512);
+    __syncthreads();     // barrier 0
+
+    for (int s0 = 0; s0 < nsteps; s0 += ITER) {
+#pragma unroll
+      for (int u = 0; u < ITER; ++u) {
+        const int s = s0 + u;                 // global k32 step
+        const int buf = (s / SPC) % kGemmBufs;
+        const int ko = (u % SPC) * 32;        // offset inside the chunk
+        uint4 wv[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          wv[t] = ring[u % D][t];
+          ring[u % D][t] = *reinterpret_cast<const uint4 *>(wbase[t] + (long)min(s + D, nsteps - 1) * 512);
         }
+        bf16x8_t af[MT];
+#pragma unroll
+        for (int a = 0; a < MT; ++a) {
+          const int rr = wm * 16 * MT + 16 * a + j;
+          const int p = ((ko >> 3) + g4) ^ (rr & SWZ);
+          af[a] = as_bf16x8(*reinterpret_cast<const uint4 *>(&As[buf][rr * BKA + 8 * p]));
+        }
+#pragma unroll
+        for (int a = 0; a < MT; ++a)
+#pragma unroll
+          for (int t = 0; t < NT; ++t)
+            acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], as_bf16x8(wv[t]), acc[a][t], 0, 0, 0);
+        if ((u % SPC) == SPC - 1) __syncthreads();   // barrier s / SPC + 1: done with this chunk
       }
     }
   }
 
+  if (w < 4) {
   // lane holds C[row 16a + 4 g4 + r][col 16t + j] of the wave tile
 #pragma unroll
   for (int a = 0; a < MT; ++a) {
@@ -188,12 +212,15 @@ __global__ __launch_bounds__(256) void gemm_stream_kernel(GemmS g) {
     }
   }
 
+  }
+
   if (EPI == EPI_STATS) {
-    // softmax statistics of this workgroup's 128 columns, per row: every wave
+    // softmax statistics of this workgroup's kTileIds columns, per row: every wave
     // reduces its own columns over the 16 lanes of a row, the waves of a row
     // meet in LDS (A's buffers are free once the K loop is done)
     __syncthreads();
     float *sm = reinterpret_cast<float *>(&As[0][0]);          // [BM][WN][3]
+    if (w < 4) {
 #pragma unroll
     for (int a = 0; a < MT; ++a) {
 #pragma unroll
@@ -225,8 +252,9 @@ __global__ __launch_bounds__(256) void gemm_stream_kernel(GemmS g) {
         }
       }
     }
+    }
     __syncthreads();
-    for (int rl = tid; rl < BM; rl += 256) {
+    for (int rl = tid; rl < BM; rl += 4 * kWave) {
       const int m = m0 + rl;
       if (m >= g.M) continue;
       const float *e = sm + rl * WN * 3;
@@ -245,7 +273,7 @@ __global__ __launch_bounds__(256) void gemm_stream_kernel(GemmS g) {
       o.max = M;
       o.argmax = arg;
       o.sum = S;
-      g.stats[(long)m * (g.Nw / 128) + nt] = o;
+      g.stats[(long)m * (g.Nw / kTileIds) + nt] = o;
     }
   }
 }
@@ -367,14 +395,19 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF g) {
 
 template <int MT, int NT, int WM, int EPI>
 void launch_stream(const GemmS &g, hipStream_t s) {
-  hipLaunchKernelGGL((gemm_stream_kernel<MT, NT, WM, EPI>), dim3(g.n_tiles * g.m_tiles * g.splits), dim3(256), 0, s, g);
+  hipLaunchKernelGGL((gemm_stream_kernel<MT, NT, WM, EPI>), dim3(g.n_tiles * g.m_tiles * g.splits), dim3(kGemmThreads),
+                     0, s, g);
 }
 
 template <int EPI>
 void launch_stream_shape(int shape, const GemmS &g, hipStream_t s) {
-  switch (shape) {
-    case 0: launch_stream<4, 2, 1, EPI>(g, s); break;   // 64 x 128 tiles
-    default: launch_stream<8, 2, 1, EPI>(g, s); break;  // 128 x 128 tiles
+  if constexpr (EPI == EPI_STATS) {
+    launch_stream<4, 2, 1, EPI>(g, s);                  // 64 x 128 tiles: one tile-statistics block each
+  } else {
+    switch (shape) {
+      case 0: launch_stream<4, 2, 1, EPI>(g, s); break;   // 64 x 128 tiles
+      default: launch_stream<8, 2, 1, EPI>(g, s); break;  // 128 x 128 tiles
+    }
   }
 }
 }  // namespace
@@ -396,8 +429,9 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
   p.Nw = epi == EPI_SWIGLU ? 2 * N : N;
   p.n_tiles = p.Nw / cols;
   const int target = 256;                           // workgroups that keep every CU streaming
-  p.shape = (M > 64 && M <= 128 && p.n_tiles >= target) ? 1 : 0;
-  const int BM = p.shape == 0 ? 64 : 128;
+  // tile statistics (kTileIds = 128 columns per workgroup) take the 64 x 128 tiles
+  p.shape = (epi != EPI_STATS && M > 64 && M <= 128 && p.n_tiles >= target) ? 1 : 0;
+  const int BM = p.shape == 1 ? 128 : 64;
   const int ITER = 8;                               // k32 steps per unrolled iteration (see kernel)
   p.m_tiles = (M + BM - 1) / BM;
   p.k_iters = K / (ITER * 32);

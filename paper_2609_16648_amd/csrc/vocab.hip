@@ -411,7 +411,9 @@ void launch_kv_commit(int B, int k, int page_size, int max_pages, const int32_t 
 // ------------------------------------------------------------------ tile statistics and tile draws
 namespace gm {
 
-// one wave per 128-id tile: max of z / T, the lowest id attaining it, sum exp(z / T - max)
+// one wave per 128-id tile (two ids per lane): max of z / T, the lowest id attaining
+// it, sum exp(z / T - max)
+static_assert(kTileIds == 2 * kWave, "a tile is two ids per lane");
 __global__ __launch_bounds__(256) void tile_stats_kernel(const float *__restrict__ logits, long row_stride, int V,
                                                          float inv_t, int n_tiles, RowStat *__restrict__ out) {
   const int r = blockIdx.x, t = blockIdx.y * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -551,7 +553,7 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
   const float mt = st[tile].max;
   const double scale = exp((double)mt - M);
   const float *row = logits + (long)b * row_stride;
-  const int xa = tile * kTileIds + 2 * lane, xb = xa + 1;
+  const int xa = tile * kTileIds + 2 * lane, xb = xa + 1;   // two consecutive ids per lane
   const double ea = xa < V ? (double)expf(row[xa] * inv_t - mt) * scale : 0.0;
   const double eb = xb < V ? (double)expf(row[xb] * inv_t - mt) * scale : 0.0;
   double incl2 = ea + eb;

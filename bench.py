@@ -256,14 +256,37 @@ def cpu_baseline(wl, mode, budget_s, weights=None):
     per_seq = max(t1, 1e-3)
     nseq = int(max(1, min(wl.batch, budget_s / per_seq)))
     t, c = run(nseq) if nseq > 1 else (t1, c1)
+    reps = 1
+    while nseq == wl.batch and t < 10.0 and reps < 4:   # a whole batch in under 10 s: repeat it
+        t2, c2 = run(nseq)
+        t, c, reps = t + t2, c + c2, reps + 1
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     return {"value": c / t, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": "%d of %d sequences of the %s workload, one full step (verify forward in the bf16 "
+            "sample": "%d of %d sequences of the %s workload, %d full step%s (verify forward in the bf16 "
                       "rounding-contract mode, accept, commit%s) in %.1f s, %d committed tokens"
-                      % (nseq, wl.batch, wl.name, ", MTP draft" if wl.with_mtp else "", t, c)}
+                      % (nseq, wl.batch, wl.name, reps, "s" if reps > 1 else "", ", MTP draft" if wl.with_mtp else "",
+                         t, c)}
 
 
 # ----------------------------------------------------------------------------- main
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter record
+    (profiles/hbm_traffic_<kernel>.json), or None when there is none for this
+    workload or a source file it was taken from has changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_%s.json" % kernel)
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel") != kernel or rec.get("workload") != workload:
+        return None
+    for rel, digest in rec.get("sources_sha256", {}).items():
+        f = os.path.join(ROOT, rel)
+        if not os.path.exists(f) or hashlib.sha256(open(f, "rb").read()).hexdigest() != digest:
+            return None
+    return int(rec["traffic_bytes_per_launch"])
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -345,7 +368,10 @@ def main():
             roof = {"bound": "hbm", "achieved": round(per_launch_bytes / (dom_ms * 1e-3) / 1e9, 1),
                     "peak": HBM_GBS, "unit": "GB/s"}
         roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-        roof["traffic"] = None
+        roof["traffic"] = measured_traffic(dominant, args.workload)
+        if roof["traffic"] is not None:
+            roof["traffic_unit"] = "bytes/launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
+            roof["traffic_vs_algorithmic"] = round(roof["traffic"] / per_launch_bytes, 3)
         roof["kernel"] = dominant
         roof["avg_launch_ms"] = round(dom_ms, 4)
         roof["launches"] = dom[0]

@@ -24,10 +24,13 @@ CFLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH, "-Wall", "-Wno
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-I" + os.path.join(ROOT, "include")]
 
-# Per-source extra flags.  attention.hip: keep MFMA accumulators in ordinary
-# VGPRs (the online-softmax rescale multiplies them with vector ALU ops, which
-# would otherwise copy them out of and back into accumulation registers).
-EXTRA_FLAGS = {"attention.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form"]}
+# Per-source extra flags: keep MFMA accumulators in ordinary VGPRs.  In
+# attention.hip the online-softmax rescale multiplies them with vector ALU ops,
+# which would otherwise copy them out of and back into accumulation registers;
+# in gemm.hip the register rings otherwise lose their fixed registers across
+# loop turns (the accumulators get shuffled through copies every iteration).
+EXTRA_FLAGS = {"attention.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form"],
+               "gemm.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form"]}
 
 
 def hipcc() -> str:

@@ -140,7 +140,7 @@ MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx) {
   p.attn_chain = plan_attention(cfg, B, 1, max_ctx + 2 * k);
   p.attn_ws = c.take(p.attn_ext.total > p.attn_chain.total ? p.attn_ext.total : p.attn_chain.total);
   const int V = cfg.vocab;
-  p.stat = c.take(sizeof(RowStat) * (size_t)B * vocab_tiles(V));
+  p.stat = c.take(sizeof(RowStat) * (size_t)B * plan_lm_head(cfg.dtype, B, V, cfg.hidden).tiles);
   const size_t pe = part_bytes(cfg, (int)Me, true), pb = part_bytes(cfg, B, true);
   p.part = c.take(pe > pb ? pe : pb);
   p.total = c.off;
@@ -174,11 +174,12 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
     launch_gemm("mtp_gemm_gate_up", dt, EPI_SWIGLU, B, F, H, nbuf, H, L.w_gate_up, act, F, part, s);
     gemm_norm("mtp_gemm_down", dt, EPI_ADD_F32, B, H, F, act, F, L.w_down, x1, part, mtp.final_norm, eps, nbuf, s);
     float *zl = draft_logits + (long)j * V;
-    // the LM head emits the logits and their softmax statistics per 128-id tile; the draw
+    // the LM head emits the logits and their softmax statistics per tile of ids; the draw
     // then reads only the tile statistics and one tile of logits per sequence
     launch_gemm("mtp_gemm_lm_head", dt, EPI_STATS, B, V, H, nbuf, H, shared.lm_head, zl, (long)k * V, part, s, tiles,
                 inv_t);
-    launch_tile_draw(B, V, mode, inv_t, zl, (long)k * V, tiles, u_draft ? u_draft + j : nullptr, k, drafts + j, k, s);
+    launch_tile_draw(B, V, mode, inv_t, zl, (long)k * V, plan_lm_head(dt, B, V, H), tiles, u_draft ? u_draft + j : nullptr,
+                     k, drafts + j, k, s);
   };
 
   // ---- extend: rows (h_{m+i}, x_{m+i+1}), i = 0..n_b, at slots m_b + i

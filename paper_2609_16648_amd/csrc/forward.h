@@ -66,6 +66,9 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K);
 int launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, const void *X, int ldx,
                 const void *W, void *Y, long ldy, float *part, hipStream_t s,
                 RowStat *tile_stats = nullptr, float inv_t = 1.f, bool defer_reduce = false);
+// tile geometry of the softmax statistics an EPI_STATS launch at M rows emits (the draw reads it);
+// *strips_kernel: whether the persistent strip-range kernel runs
+TileGeom plan_lm_head(int dtype, int M, int V, int K, bool *strips_kernel = nullptr);
 // Y[M][N] (+)= sum of `splits` partials, then out = RMSNorm(Y) * norm_w (epi: STORE_F32 or ADD_F32)
 void launch_reduce_norm(int dtype, int epi, int M, int N, int splits, const float *part, float *Y,
                         const void *norm_w, float eps, void *out, hipStream_t s);

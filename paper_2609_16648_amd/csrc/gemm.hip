@@ -19,6 +19,8 @@
 //    model dtype, SwiGLU (gate and up strips of the same features sit in the
 //    same wave, so silu(gate) * up is formed in registers).
 // float32 path: a plain LDS-tiled FMA kernel on row-major weights.
+#include <atomic>
+
 #include "common.h"
 #include "forward.h"
 
@@ -32,13 +34,14 @@ struct GemmS {
   long ldy;
   int M, N, K, ldx;   // N: output columns (features for SwiGLU); Nw: weight rows
   int Nw, n_tiles, m_tiles, splits, k_iters;
-  RowStat *stats;     // EPI_STATS: [M][Nw / kTileIds] tile statistics of Y / T
+  RowStat *stats;     // EPI_STATS: [M][Nw / kStatCols] tile statistics of Y / T
   float inv_t;
 };
 
 __device__ __forceinline__ float silu(float x) { return x / (1.f + expf(-x)); }
 
 constexpr int kGemmThreads = 5 * kWave;   // four compute waves and one A-staging wave
+constexpr int kStatCols = kMaxTileStrips * kStripIds;   // columns per statistics tile of the tiled GEMM
 constexpr int kGemmBufs = 3;              // A chunks in LDS (the loader runs two ahead)
 // s_waitcnt immediates (gfx9 encoding: vmcnt bits 3:0 and 15:14, expcnt 6:4,
 // lgkmcnt 11:8; the other counters left at their maximum, i.e. not waited on)
@@ -63,7 +66,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
   constexpr int BKA = 8192 / BM;              // k per LDS chunk of A (16 KiB)
   constexpr int SPC = BKA / 32;               // k32 steps per chunk
   constexpr int D = NT >= 4 ? 4 : 8;          // W prefetch depth (k32 steps)
-  static_assert(EPI != EPI_STATS || 16 * NT * WN == kTileIds, "tile statistics cover one workgroup's columns");
+  static_assert(EPI != EPI_STATS || 16 * NT * WN == kStatCols, "tile statistics cover one workgroup's columns");
   constexpr int ITER = D > SPC ? D : SPC;     // k32 steps per unrolled iteration
   constexpr int CB = BKA / 8;                 // 16-byte column blocks per A row of a chunk
   constexpr int SWZ = CB < 16 ? CB - 1 : 15;  // XOR swizzle of the column block by the row
@@ -215,7 +218,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
   }
 
   if (EPI == EPI_STATS) {
-    // softmax statistics of this workgroup's kTileIds columns, per row: every wave
+    // softmax statistics of this workgroup's kStatCols columns, per row: every wave
     // reduces its own columns over the 16 lanes of a row, the waves of a row
     // meet in LDS (A's buffers are free once the K loop is done)
     __syncthreads();
@@ -273,7 +276,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
       o.max = M;
       o.argmax = arg;
       o.sum = S;
-      g.stats[(long)m * (g.Nw / kTileIds) + nt] = o;
+      g.stats[(long)m * (g.Nw / kStatCols) + nt] = o;
     }
   }
 }
@@ -393,6 +396,141 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF g) {
   }
 }
 
+// ------------------------------------------------------------------ LM head, M <= 64
+// Persistent strip ranges: as many waves as the chip holds, each owning a
+// contiguous range of 16-column weight strips (at most kLmStrips, balanced to
+// within one strip over all waves) over the whole K.  Every wave is on its own:
+// the weight tiles and the activation fragments (64 rows, read from L2 in the
+// A-operand order) stream through a kLmRing-step register ring with
+// unconditional loads, and there is no LDS and no barrier, so no wave ever
+// waits for another.  EPI_STATS: the softmax statistics of Y / T are taken per
+// row over the wave's own range (float32 terms, float64 sums), one RowStat per
+// (row, wave): the tiles of the draw are the waves' ranges.
+constexpr int kLmStrips = 10;
+constexpr int kLmRing = 4;
+
+struct GemmL {
+  const uint16_t *X, *W;
+  float *Y;
+  long ldy;
+  int M, K, ldx;
+  TileGeom geo;       // strips = N / 16, tiles = waves
+  RowStat *stats;     // EPI_STATS: [M][waves]
+  float inv_t;
+};
+
+template <int EPI>
+__global__ __launch_bounds__(256) void lm_strips_kernel(GemmL g) {
+  const int lane = threadIdx.x & 63, j = lane & 15, g4 = lane >> 4;
+  const int wid = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
+  if (wid >= g.geo.tiles) return;
+  const int s0 = tile_first_strip(g.geo, wid), n = tile_first_strip(g.geo, wid + 1) - s0;   // 1 .. kLmStrips
+  const int ksteps = g.K / 32;   // a multiple of kLmRing
+  const uint16_t *wb[kLmStrips];
+#pragma unroll
+  for (int t = 0; t < kLmStrips; ++t) wb[t] = g.W + (long)(s0 + min(t, n - 1)) * ksteps * 512 + lane * 8;
+  const uint16_t *ab[4];   // A fragment of row tile a: row 16 a + j (rows past M re-read row M - 1), k 8 g4 ..
+#pragma unroll
+  for (int a = 0; a < 4; ++a) ab[a] = g.X + (long)min(16 * a + j, g.M - 1) * g.ldx + 8 * g4;
+
+  floatx4_t acc[4][kLmStrips];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int t = 0; t < kLmStrips; ++t) acc[a][t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  uint4 ra[kLmRing][4], rw[kLmRing][kLmStrips];
+  auto load = [&](int slot, int step) {
+#pragma unroll
+    for (int t = 0; t < kLmStrips; ++t) rw[slot][t] = *reinterpret_cast<const uint4 *>(wb[t] + (long)step * 512);
+#pragma unroll
+    for (int a = 0; a < 4; ++a) ra[slot][a] = *reinterpret_cast<const uint4 *>(ab[a] + step * 32);
+  };
+#pragma unroll
+  for (int d = 0; d < kLmRing - 1; ++d) {   // in slot order: the ring's waits count on it
+    __builtin_amdgcn_sched_barrier(0);
+    load(d, d);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  for (int s0k = 0; s0k < ksteps; s0k += kLmRing) {
+#pragma unroll
+    for (int d = 0; d < kLmRing; ++d) {
+      // refill the slot consumed last step (a re-read of the last step near the end)
+      __builtin_amdgcn_sched_barrier(0);
+      load((d + kLmRing - 1) % kLmRing, min(s0k + d + kLmRing - 1, ksteps - 1));
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int t = 0; t < kLmStrips; ++t)
+          acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ra[d][a]), as_bf16x8(rw[d][t]), acc[a][t], 0,
+                                                              0, 0);
+    }
+  }
+
+  // lane holds C[row 16 a + 4 g4 + r][col 16 (s0 + t) + j]
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = 16 * a + 4 * g4 + r;
+      const bool row_ok = m < g.M;
+      if (row_ok) {
+        float *y = g.Y + (long)m * g.ldy + (long)s0 * 16 + j;
+#pragma unroll
+        for (int t = 0; t < kLmStrips; ++t)
+          if (t < n) y[16 * t] = acc[a][t][r];
+      }
+      if (EPI == EPI_STATS) {
+        float vmax = -INFINITY;
+        int varg = 0x7fffffff;
+#pragma unroll
+        for (int t = 0; t < kLmStrips; ++t) {
+          const float v = acc[a][t][r] * g.inv_t;
+          if (t < n && v > vmax) { vmax = v; varg = (s0 + t) * 16 + j; }   // ascending ids per lane
+        }
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) {
+          const float om = __shfl_xor(vmax, o, kWave);
+          const int oa = __shfl_xor(varg, o, kWave);
+          if (om > vmax || (om == vmax && oa < varg)) { vmax = om; varg = oa; }
+        }
+        double sum = 0.0;
+#pragma unroll
+        for (int t = 0; t < kLmStrips; ++t)
+          if (t < n) sum += (double)expf(acc[a][t][r] * g.inv_t - vmax);
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) sum += __shfl_xor(sum, o, kWave);
+        if (row_ok && j == 0) {
+          RowStat st;
+          st.max = vmax;
+          st.argmax = varg;
+          st.sum = sum;
+          g.stats[(long)m * g.geo.tiles + wid] = st;
+        }
+      }
+    }
+  }
+}
+
+// waves of lm_strips_kernel the device holds at once (queried once per device)
+int lm_resident_waves() {
+  static std::atomic<int> cache[16];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 16) return 1024;
+  int v = cache[dev].load();
+  if (v > 0) return v;
+  int per_cu = 0, cus = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, lm_strips_kernel<EPI_STATS>, 256, 0) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || per_cu < 1 || cus < 1) {
+    (void)hipGetLastError();
+    return 1024;
+  }
+  v = per_cu * cus * 4;
+  cache[dev].store(v);
+  return v;
+}
+
 template <int MT, int NT, int WM, int EPI>
 void launch_stream(const GemmS &g, hipStream_t s) {
   hipLaunchKernelGGL((gemm_stream_kernel<MT, NT, WM, EPI>), dim3(g.n_tiles * g.m_tiles * g.splits), dim3(kGemmThreads),
@@ -429,7 +567,7 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
   p.Nw = epi == EPI_SWIGLU ? 2 * N : N;
   p.n_tiles = p.Nw / cols;
   const int target = 256;                           // workgroups that keep every CU streaming
-  // tile statistics (kTileIds = 128 columns per workgroup) take the 64 x 128 tiles
+  // tile statistics (kStatCols = 128 columns per workgroup) take the 64 x 128 tiles
   p.shape = (epi != EPI_STATS && M > 64 && M <= 128 && p.n_tiles >= target) ? 1 : 0;
   const int BM = p.shape == 1 ? 128 : 64;
   const int ITER = 8;                               // k32 steps per unrolled iteration (see kernel)
@@ -445,9 +583,33 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
   return p;
 }
 
+// Tile geometry of the LM head's softmax statistics at M rows: the strip-range
+// kernel's waves (bf16, M <= 64), else tiles of 8 strips (128 ids).
+TileGeom plan_lm_head(int dtype, int M, int V, int K, bool *strips_kernel) {
+  if (strips_kernel) *strips_kernel = false;
+  if (dtype != GM_BF16 || M > 64 || V % kStripIds || K % (32 * kLmRing)) return fixed_tiles(V);
+  const int S = V / kStripIds;
+  int waves = lm_resident_waves();
+  if (waves > S) waves = S;
+  if (waves < (S + kLmStrips - 1) / kLmStrips) waves = (S + kLmStrips - 1) / kLmStrips;
+  if (waves > kMaxTiles) return fixed_tiles(V);
+  if (strips_kernel) *strips_kernel = true;
+  return TileGeom{S, waves};
+}
+
 int launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, const void *X, int ldx, const void *W,
                 void *Y, long ldy, float *part, hipStream_t s, RowStat *tile_stats, float inv_t, bool defer_reduce) {
   if (M <= 0) return 1;
+  if (dtype == GM_BF16 && epi == EPI_STATS) {
+    bool strips = false;
+    const TileGeom geo = plan_lm_head(dtype, M, N, K, &strips);
+    if (strips) {
+      GemmL l{(const uint16_t *)X, (const uint16_t *)W, (float *)Y, ldy, M, K, ldx, geo, tile_stats, inv_t};
+      TraceScope ts(name, s);
+      hipLaunchKernelGGL(lm_strips_kernel<EPI_STATS>, dim3((geo.tiles + 3) / 4), dim3(256), 0, s, l);
+      return 1;
+    }
+  }
   if (dtype == GM_BF16) {
     const GemmPlan p = plan_gemm(dtype, epi, M, N, K);
     GemmS g{(const uint16_t *)X, (const uint16_t *)W, Y, part, ldy, M, N, K, ldx, p.Nw, p.n_tiles, p.m_tiles,
@@ -483,7 +645,7 @@ int launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, const
         TraceScope ts(name, s);
         hipLaunchKernelGGL(gemm_f32_kernel<EPI_STORE_F32>, grid, block, 0, s, g);
       }
-      launch_tile_stats((const float *)Y, ldy, M, N, inv_t, tile_stats, s);
+      launch_tile_stats((const float *)Y, ldy, M, N, inv_t, plan_lm_head(dtype, M, N, K), tile_stats, s);
       return 1;
     }
     TraceScope ts(name, s);

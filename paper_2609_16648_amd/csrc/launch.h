@@ -44,18 +44,30 @@ constexpr int kScanChunk = kScanThreads * kScanPer;           // 4096 ids per ch
 inline int stat_chunks(int V) { return (V + kStatChunk - 1) / kStatChunk; }
 inline int scan_chunks(int V) { return (V + kScanChunk - 1) / kScanChunk; }
 
-// Softmax statistics per 128-id tile of a logits row (RowStat per tile), the
-// form the LM-head GEMM epilogue emits; a draw from such a row needs no
-// further pass over the vocabulary.
-constexpr int kTileIds = 128;
-constexpr int kMaxVocab = 4096 * kTileIds;   // the draw stages a row's tile statistics in 64 KiB of LDS
-inline int vocab_tiles(int V) { return (V + kTileIds - 1) / kTileIds; }
+// Softmax statistics per tile of a logits row (RowStat per tile), the form the
+// LM-head GEMM epilogue emits; a draw from such a row needs no further pass over
+// the vocabulary.  The row's ids are cut into `strips` strips of 16 and the
+// strips into `tiles` tiles: tile t holds strips [t S / T, (t + 1) S / T)
+// (integer division), at most kMaxTileStrips of them.
+constexpr int kStripIds = 16;
+constexpr int kMaxTileStrips = 8;              // 128 ids
+constexpr int kMaxTiles = 4096;                // the draw stages a row's tile statistics in 64 KiB of LDS
+constexpr int kMaxVocab = kMaxTiles * kMaxTileStrips * kStripIds;
+struct TileGeom {
+  int strips, tiles;
+};
+__host__ __device__ inline int tile_first_strip(const TileGeom &g, int t) { return (int)((long)t * g.strips / g.tiles); }
+// tiles of 8 strips (128 ids; the last may be shorter)
+inline TileGeom fixed_tiles(int V) {
+  const int S = (V + kStripIds - 1) / kStripIds;
+  return TileGeom{S, (S + kMaxTileStrips - 1) / kMaxTileStrips};
+}
 // tile statistics by a pass over rows of logits (paths without the GEMM epilogue)
-void launch_tile_stats(const float *logits, long row_stride, int n_rows, int V, float inv_t, RowStat *tiles,
-                       hipStream_t s);
+void launch_tile_stats(const float *logits, long row_stride, int n_rows, int V, float inv_t, TileGeom geo,
+                       RowStat *tiles, hipStream_t s);
 // one draw per row from softmax(z / T) given its tile statistics: argmax (greedy) or the
 // inverse-CDF draw with u[b * u_stride]; writes dst[b * dst_stride]
-void launch_tile_draw(int B, int V, int mode, float inv_t, const float *logits, long row_stride,
+void launch_tile_draw(int B, int V, int mode, float inv_t, const float *logits, long row_stride, TileGeom geo,
                       const RowStat *tiles, const float *u, int u_stride, int32_t *dst, int dst_stride,
                       hipStream_t s);
 

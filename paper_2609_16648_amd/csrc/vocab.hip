@@ -14,7 +14,7 @@
 //     order (per-id exponentials in float32, normalisers, differences and
 //     running sums in float64), first as chunk masses, then a scan inside the
 //     chunk that holds u * Z.
-//  4. tile_stats / tile_draw: per 128-id tile statistics (also emitted by
+//  4. tile_stats / tile_draw: per-tile statistics (tiles of at most 128 ids; also emitted by
 //     the LM-head GEMM epilogue) and a draw that needs no pass over the row.
 #include <float.h>
 
@@ -411,18 +411,19 @@ void launch_kv_commit(int B, int k, int page_size, int max_pages, const int32_t 
 // ------------------------------------------------------------------ tile statistics and tile draws
 namespace gm {
 
-// one wave per 128-id tile (two ids per lane): max of z / T, the lowest id attaining
-// it, sum exp(z / T - max)
-static_assert(kTileIds == 2 * kWave, "a tile is two ids per lane");
+// one wave per tile (at most 128 ids, two per lane): max of z / T, the lowest id
+// attaining it, sum exp(z / T - max) (float32 terms, float64 sum)
+static_assert(kMaxTileStrips * kStripIds <= 2 * kWave, "a tile is at most two ids per lane");
 __global__ __launch_bounds__(256) void tile_stats_kernel(const float *__restrict__ logits, long row_stride, int V,
-                                                         float inv_t, int n_tiles, RowStat *__restrict__ out) {
+                                                         float inv_t, TileGeom geo, RowStat *__restrict__ out) {
   const int r = blockIdx.x, t = blockIdx.y * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (t >= n_tiles) return;
+  if (t >= geo.tiles) return;
   const float *row = logits + (long)r * row_stride;
-  const int x0 = t * kTileIds + lane, x1 = x0 + 64;
-  const float v0 = x0 < V ? row[x0] * inv_t : -INFINITY, v1 = x1 < V ? row[x1] * inv_t : -INFINITY;
+  const int lo = tile_first_strip(geo, t) * kStripIds, hi = min(V, tile_first_strip(geo, t + 1) * kStripIds);
+  const int x0 = lo + lane, x1 = x0 + 64;
+  const float v0 = x0 < hi ? row[x0] * inv_t : -INFINITY, v1 = x1 < hi ? row[x1] * inv_t : -INFINITY;
   float m = v0;
-  int a = x0 < V ? x0 : 0x7fffffff;
+  int a = x0 < hi ? x0 : 0x7fffffff;
   if (v1 > m) { m = v1; a = x1; }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -430,24 +431,23 @@ __global__ __launch_bounds__(256) void tile_stats_kernel(const float *__restrict
     const int oa = __shfl_xor(a, o, kWave);
     if (om > m || (om == m && oa < a)) { m = om; a = oa; }
   }
-  float s = expf(v0 - m) + expf(v1 - m);
+  double s = (x0 < hi ? (double)expf(v0 - m) : 0.0) + (x1 < hi ? (double)expf(v1 - m) : 0.0);
   s = wave_sum(s);
   if (lane == 0) {
     RowStat o;
     o.max = m;
     o.argmax = a;
-    o.sum = (double)s;
-    out[(long)r * n_tiles + t] = o;
+    o.sum = s;
+    out[(long)r * geo.tiles + t] = o;
   }
 }
 
-void launch_tile_stats(const float *logits, long row_stride, int n_rows, int V, float inv_t, RowStat *tiles,
-                       hipStream_t s) {
+void launch_tile_stats(const float *logits, long row_stride, int n_rows, int V, float inv_t, TileGeom geo,
+                       RowStat *tiles, hipStream_t s) {
   if (n_rows <= 0) return;
   TraceScope ts("draft_tile_stats", s);
-  const int nt = vocab_tiles(V);
-  hipLaunchKernelGGL(tile_stats_kernel, dim3(n_rows, (nt + 3) / 4), dim3(256), 0, s, logits, row_stride, V, inv_t,
-                     nt, tiles);
+  hipLaunchKernelGGL(tile_stats_kernel, dim3(n_rows, (geo.tiles + 3) / 4), dim3(256), 0, s, logits, row_stride, V,
+                     inv_t, geo, tiles);
 }
 
 // Inclusive prefix sum of one double per thread over the block (256 threads).
@@ -470,12 +470,13 @@ __device__ __forceinline__ double block_incl_scan(double v, double *wsum /* >= 4
 // masses s_t exp(m_t - M) in float64, contiguous runs of them per thread, a
 // block-wide prefix sum over the runs, and the first run whose prefix passes
 // u * S is walked tile by tile to the tile holding u * S.  One wave then scans
-// that tile's 128 ids (the same per-id terms exp(z / T - m_t) the tile sums
+// that tile's ids (at most 128; the same per-id terms exp(z / T - m_t) the tile sums
 // were made of, scaled in float64) for the first running sum above u * S.
 __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float inv_t, const float *__restrict__ logits,
                                                         long row_stride, const RowStat *__restrict__ tiles,
-                                                        int n_tiles, const float *__restrict__ u, int u_stride,
+                                                        TileGeom geo, const float *__restrict__ u, int u_stride,
                                                         int32_t *__restrict__ dst, int dst_stride) {
+  const int n_tiles = geo.tiles;
   extern __shared__ uint4 st_raw[];   // [n_tiles] RowStat
   RowStat *st = reinterpret_cast<RowStat *>(st_raw);
   __shared__ float red_m[4];
@@ -553,9 +554,10 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
   const float mt = st[tile].max;
   const double scale = exp((double)mt - M);
   const float *row = logits + (long)b * row_stride;
-  const int xa = tile * kTileIds + 2 * lane, xb = xa + 1;   // two consecutive ids per lane
-  const double ea = xa < V ? (double)expf(row[xa] * inv_t - mt) * scale : 0.0;
-  const double eb = xb < V ? (double)expf(row[xb] * inv_t - mt) * scale : 0.0;
+  const int lo = tile_first_strip(geo, tile) * kStripIds, hi = min(V, tile_first_strip(geo, tile + 1) * kStripIds);
+  const int xa = lo + 2 * lane, xb = xa + 1;   // two consecutive ids per lane
+  const double ea = xa < hi ? (double)expf(row[xa] * inv_t - mt) * scale : 0.0;
+  const double eb = xb < hi ? (double)expf(row[xb] * inv_t - mt) * scale : 0.0;
   double incl2 = ea + eb;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
@@ -575,12 +577,12 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
   if (first < 0 && lastnz < 0 && lane == 0) dst[(long)b * dst_stride] = a;
 }
 
-void launch_tile_draw(int B, int V, int mode, float inv_t, const float *logits, long row_stride, const RowStat *tiles,
-                      const float *u, int u_stride, int32_t *dst, int dst_stride, hipStream_t s) {
+void launch_tile_draw(int B, int V, int mode, float inv_t, const float *logits, long row_stride, TileGeom geo,
+                      const RowStat *tiles, const float *u, int u_stride, int32_t *dst, int dst_stride, hipStream_t s) {
   if (B <= 0) return;
   TraceScope ts("draft_draw", s);
-  hipLaunchKernelGGL(tile_draw_kernel, dim3(B), dim3(256), (size_t)vocab_tiles(V) * sizeof(RowStat), s, V, mode,
-                     inv_t, logits, row_stride, tiles, vocab_tiles(V), u, u_stride, dst, dst_stride);
+  hipLaunchKernelGGL(tile_draw_kernel, dim3(B), dim3(256), (size_t)geo.tiles * sizeof(RowStat), s, V, mode, inv_t,
+                     logits, row_stride, tiles, geo, u, u_stride, dst, dst_stride);
 }
 
 }  // namespace gm

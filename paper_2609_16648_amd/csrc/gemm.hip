@@ -7,8 +7,9 @@
 //    v_mfma_f32_16x16x32_bf16.  A wave streams its strips of 16 rows along K
 //    as consecutive 1 KiB tiles, straight from HBM into registers, through a
 //    prefetch ring several k-steps deep; W never touches LDS.
-//  * Activations (small, L2-resident) are staged in LDS in 32 KiB chunks,
-//    double-buffered, one barrier per chunk, shared by the 4 waves.
+//  * Activations (small, L2-resident) are staged in LDS in 16 or 32 KiB
+//    chunks, three deep, by a fifth wave of direct-to-LDS loads, one barrier
+//    per chunk, shared by the 4 compute waves.
 //  * Small N is split along K (deterministic two-pass reduction: float32
 //    partials, then a reduce kernel that sums the splits in order and applies
 //    the epilogue) so that a launch fills the 256 CUs.
@@ -27,6 +28,20 @@
 namespace gm {
 
 namespace {
+// Weight tiles read by one workgroup only are loaded non-temporally: they then
+// do not evict the activations, which every workgroup re-reads from L2
+// (measured: 5-6% off the M <= 64 LM head).  Weight strips re-read by the M
+// tiles of a launch take ordinary loads, as that re-read is meant to hit L2.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+template <bool STREAM>
+__device__ __forceinline__ uint4 load_w(const uint16_t *p) {
+  if (STREAM) {
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+  }
+  return *reinterpret_cast<const uint4 *>(p);
+}
+
 struct GemmS {
   const uint16_t *X, *W;
   void *Y;
@@ -56,14 +71,15 @@ __device__ __forceinline__ int xcd_remap(int bid, int T) {
 }
 
 // MT: 16-row tiles per compute wave; NT: 16-column strips per compute wave;
-// WM: compute waves along M (1 or 2).  Waves 0-3 compute; wave 4 only stages
+// WM: compute waves along M (1 or 2); SW: weights loaded non-temporally (one M
+// tile).  Waves 0-3 compute; wave 4 only stages
 // the A chunks in LDS.  The wait counter of loads is per wave, so the loader's
 // waits for A never drain the compute waves' weight ring.
-template <int MT, int NT, int WM, int EPI>
+template <int MT, int NT, int WM, int EPI, bool SW>
 __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
   constexpr int WN = 4 / WM;
   constexpr int BM = 16 * MT * WM;            // rows per workgroup
-  constexpr int BKA = 8192 / BM;              // k per LDS chunk of A (16 KiB)
+  constexpr int BKA = (BM >= 256 ? 16384 : 8192) / BM;   // k per LDS chunk of A (16 KiB; 32 KiB at 256 rows)
   constexpr int SPC = BKA / 32;               // k32 steps per chunk
   constexpr int D = NT >= 4 ? 4 : 8;          // W prefetch depth (k32 steps)
   static_assert(EPI != EPI_STATS || 16 * NT * WN == kStatCols, "tile statistics cover one workgroup's columns");
@@ -73,6 +89,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
   constexpr int AL = BM * BKA / 8 / kWave;    // 1 KiB direct-to-LDS loads per chunk
   constexpr int kVmcntAL = waitcnt_vm(AL);
   static_assert(ITER % SPC == 0 && ITER % D == 0, "unroll must cover whole chunks and ring turns");
+  static_assert(ITER == 8, "plan_gemm counts K in iterations of 8 k32 steps");
   // A chunk: row r, column block p of LDS holds X[r][8 (p ^ (r & SWZ)) ...]
   __shared__ uint16_t As[kGemmBufs][BM * BKA];
 
@@ -153,7 +170,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
     for (int s = 0; s < D; ++s)
 #pragma unroll
       for (int t = 0; t < NT; ++t)
-        ring[s][t] = *reinterpret_cast<const uint4 *>(wbase[t] + (long)min(s, nsteps - 1) * 512);
+        ring[s][t] = load_w<SW>(wbase[t] + (long)min(s, nsteps - 1) * 512);
     __syncthreads();     // barrier 0
 
     for (int s0 = 0; s0 < nsteps; s0 += ITER) {
@@ -166,7 +183,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
           wv[t] = ring[u % D][t];
-          ring[u % D][t] = *reinterpret_cast<const uint4 *>(wbase[t] + (long)min(s + D, nsteps - 1) * 512);
+          ring[u % D][t] = load_w<SW>(wbase[t] + (long)min(s + D, nsteps - 1) * 512);
         }
         bf16x8_t af[MT];
 #pragma unroll
@@ -442,7 +459,7 @@ __global__ __launch_bounds__(256) void lm_strips_kernel(GemmL g) {
   uint4 ra[kLmRing][4], rw[kLmRing][kLmStrips];
   auto load = [&](int slot, int step) {
 #pragma unroll
-    for (int t = 0; t < kLmStrips; ++t) rw[slot][t] = *reinterpret_cast<const uint4 *>(wb[t] + (long)step * 512);
+    for (int t = 0; t < kLmStrips; ++t) rw[slot][t] = load_w<true>(wb[t] + (long)step * 512);
 #pragma unroll
     for (int a = 0; a < 4; ++a) ra[slot][a] = *reinterpret_cast<const uint4 *>(ab[a] + step * 32);
   };
@@ -533,8 +550,9 @@ int lm_resident_waves() {
 
 template <int MT, int NT, int WM, int EPI>
 void launch_stream(const GemmS &g, hipStream_t s) {
-  hipLaunchKernelGGL((gemm_stream_kernel<MT, NT, WM, EPI>), dim3(g.n_tiles * g.m_tiles * g.splits), dim3(kGemmThreads),
-                     0, s, g);
+  const dim3 grid(g.n_tiles * g.m_tiles * g.splits);
+  if (g.m_tiles == 1) hipLaunchKernelGGL((gemm_stream_kernel<MT, NT, WM, EPI, true>), grid, dim3(kGemmThreads), 0, s, g);
+  else hipLaunchKernelGGL((gemm_stream_kernel<MT, NT, WM, EPI, false>), grid, dim3(kGemmThreads), 0, s, g);
 }
 
 template <int EPI>
@@ -543,8 +561,9 @@ void launch_stream_shape(int shape, const GemmS &g, hipStream_t s) {
     launch_stream<4, 2, 1, EPI>(g, s);                  // 64 x 128 tiles: one tile-statistics block each
   } else {
     switch (shape) {
-      case 0: launch_stream<4, 2, 1, EPI>(g, s); break;   // 64 x 128 tiles
-      default: launch_stream<8, 2, 1, EPI>(g, s); break;  // 128 x 128 tiles
+      case 0: launch_stream<4, 2, 1, EPI>(g, s); break;    // 64 x 128 tiles
+      case 1: launch_stream<8, 2, 1, EPI>(g, s); break;    // 128 x 128 tiles
+      default: launch_stream<16, 2, 1, EPI>(g, s); break;  // 256 x 128 tiles
     }
   }
 }
@@ -553,11 +572,11 @@ void launch_stream_shape(int shape, const GemmS &g, hipStream_t s) {
 // Tile shape and K split.  Every launch streams each weight byte from HBM
 // once; the choices trade workgroup count (to keep the CUs streaming) against
 // extra traffic:
-//  * wide outputs (>= 256 column tiles, e.g. the LM head) with 65..128 rows
-//    take 128-row tiles, so each weight strip is fetched once;
+//  * wide outputs (>= 256 column tiles, e.g. the LM head) with 65..256 rows
+//    take 128- or 256-row tiles, so each weight strip is fetched once (at 256
+//    rows measured 270 us against 330 us with four 64-row tiles per strip);
 //  * everything else uses 64-row tiles: the M tiles of one strip run on the
-//    same XCD and re-read it from that XCD's L2 (measured faster than
-//    256-row tiles at 256 rows: more workgroups in flight per strip), plus,
+//    same XCD and re-read it from that XCD's L2, plus,
 //    for narrow outputs, a K split capped so that the float32 partials move
 //    at most half as many bytes as the weights.
 GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
@@ -568,8 +587,8 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
   p.n_tiles = p.Nw / cols;
   const int target = 256;                           // workgroups that keep every CU streaming
   // tile statistics (kStatCols = 128 columns per workgroup) take the 64 x 128 tiles
-  p.shape = (epi != EPI_STATS && M > 64 && M <= 128 && p.n_tiles >= target) ? 1 : 0;
-  const int BM = p.shape == 1 ? 128 : 64;
+  p.shape = (epi != EPI_STATS && M > 64 && p.n_tiles >= target) ? (M <= 128 ? 1 : 2) : 0;
+  const int BM = p.shape == 2 ? 256 : p.shape == 1 ? 128 : 64;
   const int ITER = 8;                               // k32 steps per unrolled iteration (see kernel)
   p.m_tiles = (M + BM - 1) / BM;
   p.k_iters = K / (ITER * 32);

@@ -42,6 +42,14 @@ typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+// 16-byte load marked non-temporal: data read once per launch (weights, KV) then does
+// not displace what the launch re-reads from the caches
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_nt(const void *p) {
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 __device__ __forceinline__ bf16x4_t as_bf16x4(uint2 v) { return __builtin_bit_cast(bf16x4_t, v); }
 
 // ----------------------------------------------------------------- reductions

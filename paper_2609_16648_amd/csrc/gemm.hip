@@ -32,13 +32,9 @@ namespace {
 // do not evict the activations, which every workgroup re-reads from L2
 // (measured: 5-6% off the M <= 64 LM head).  Weight strips re-read by the M
 // tiles of a launch take ordinary loads, as that re-read is meant to hit L2.
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 template <bool STREAM>
 __device__ __forceinline__ uint4 load_w(const uint16_t *p) {
-  if (STREAM) {
-    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
-    return make_uint4(v.x, v.y, v.z, v.w);
-  }
+  if (STREAM) return load_nt(p);
   return *reinterpret_cast<const uint4 *>(p);
 }
 
@@ -165,12 +161,18 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
     const uint16_t *wbase[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) wbase[t] = g.W + ((long)strip[t] * kt_total + k_begin / 32) * 512 + lane * 8;
+    // Slot d of the ring holds step d mod D.  Each step first refills the slot
+    // consumed by the step before (its registers are dead), then consumes its
+    // own: a load never targets a register still waiting for its reader, so the
+    // ring keeps fixed registers across loop turns and no wait drains it.
     uint4 ring[D][NT];
 #pragma unroll
-    for (int s = 0; s < D; ++s)
+    for (int s = 0; s < D - 1; ++s) {
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
-        ring[s][t] = load_w<SW>(wbase[t] + (long)min(s, nsteps - 1) * 512);
+      for (int t = 0; t < NT; ++t) ring[s][t] = load_w<SW>(wbase[t] + (long)min(s, nsteps - 1) * 512);
+    }
+    __builtin_amdgcn_sched_barrier(0);
     __syncthreads();     // barrier 0
 
     for (int s0 = 0; s0 < nsteps; s0 += ITER) {
@@ -179,12 +181,12 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
         const int s = s0 + u;                 // global k32 step
         const int buf = (s / SPC) % kGemmBufs;
         const int ko = (u % SPC) * 32;        // offset inside the chunk
-        uint4 wv[NT];
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          wv[t] = ring[u % D][t];
-          ring[u % D][t] = load_w<SW>(wbase[t] + (long)min(s + D, nsteps - 1) * 512);
-        }
+        for (int t = 0; t < NT; ++t)
+          ring[(u + D - 1) % D][t] = load_w<SW>(wbase[t] + (long)min(s + D - 1, nsteps - 1) * 512);
+        __builtin_amdgcn_sched_barrier(0);
+        const uint4 (&wv)[NT] = ring[u % D];
         bf16x8_t af[MT];
 #pragma unroll
         for (int a = 0; a < MT; ++a) {

@@ -157,14 +157,29 @@ def layer_weights(s: ModelShape, seed: int, prefix: str) -> Dict[str, np.ndarray
     return w
 
 
-def model_weights(s: ModelShape, seed: int = SEED_WEIGHTS) -> Dict[str, object]:
-    """Backbone weights, all row-major [out, in] as nn.Linear stores them."""
+def model_weights(s: ModelShape, seed: int = SEED_WEIGHTS, threads: int = 1) -> Dict[str, object]:
+    """Backbone weights, all row-major [out, in] as nn.Linear stores them.
+
+    threads > 1 draws the tensors concurrently; every tensor has its own
+    stream, so the values do not depend on it."""
+    def job(i):
+        if i == s.n_layers:
+            return _linear(seed, "embed", s.vocab, s.hidden, s.dtype)
+        if i == s.n_layers + 1:
+            return None if s.tie_embed else _linear(seed, "lm_head", s.vocab, s.hidden, s.dtype)
+        return layer_weights(s, seed, "layer%d." % i)
+    if threads > 1:
+        import concurrent.futures
+        with concurrent.futures.ThreadPoolExecutor(threads) as ex:
+            parts = list(ex.map(job, range(s.n_layers + 2)))
+    else:
+        parts = [job(i) for i in range(s.n_layers + 2)]
     w: Dict[str, object] = {
-        "embed": _linear(seed, "embed", s.vocab, s.hidden, s.dtype),
+        "embed": parts[s.n_layers],
         "final_norm": _ones(s.hidden, s.dtype),
-        "layers": [layer_weights(s, seed, "layer%d." % i) for i in range(s.n_layers)],
+        "layers": parts[:s.n_layers],
     }
-    w["lm_head"] = w["embed"] if s.tie_embed else _linear(seed, "lm_head", s.vocab, s.hidden, s.dtype)
+    w["lm_head"] = w["embed"] if s.tie_embed else parts[s.n_layers + 1]
     return w
 
 

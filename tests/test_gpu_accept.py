@@ -47,7 +47,8 @@ def _compare(name, ref, n, out):
         assert 0 <= n[b] <= out.shape[1] - 1 and (out[b, n[b] + 1:] == -1).all()
 
 
-@pytest.mark.parametrize("B,k,V", [(64, 3, 151936), (32, 7, 151936), (4, 3, 1024), (257, 2, 1000), (3, 0, 5000)])
+@pytest.mark.parametrize("B,k,V", [(64, 3, 151936), (32, 7, 151936), (256, 3, 151936), (128, 1, 151680),
+                                   (4, 3, 1024), (257, 2, 1000), (3, 0, 5000)])
 def test_sample_accept_matches_oracle(B, k, V):
     need_gpu()
     zt = synth.normal_logits((B, k + 1, V), 3, "t", B, k, V)

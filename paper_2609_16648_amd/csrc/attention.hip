@@ -6,8 +6,9 @@
 // holds at once; workgroup (p, head group) takes range p for its heads, so
 // every wave streams the same number of tiles whatever the length mix, and a
 // range that crosses sequences yields one partial per sequence.  A combine
-// kernel merges the partials of each sequence.  One 64-lane wave per (KV head,
-// 16-row query tile):
+// kernel merges the partials of each sequence.  One 64-lane wave per KV head and
+// one or two 16-row query tiles (two: the k = 7 block, 32 rows, streams each KV
+// tile once for both):
 //  * GQA packing: the (n_heads / n_kv_heads) query heads of one KV head times
 //    the block rows form the rows of 16-row matrix-core tiles, so each K/V
 //    byte streamed from HBM serves every query that reads it;
@@ -50,7 +51,7 @@ struct AttnK {
   int32_t *cum;         // [B + 1] tiles before sequence b (written by workgroup (0, 0))
   int32_t *dev_err;
   int B, base_off, blen_add, R, G, n_heads, n_kv, page_size, max_pages, num_pages, rows_pad;
-  int parts, heads_per_group, row_tiles;
+  int parts, heads_per_group, row_tiles, waves_per_head;
   float scale_log2;
 };
 
@@ -167,16 +168,19 @@ __device__ __forceinline__ void attn_tile(int tb, int L, int g, float scale_log2
   }
 }
 
-// STREAM: every KV tile has exactly one reader (one 16-row query tile per KV head), so
-// its loads are marked non-temporal and do not displace the lines other waves re-read;
-// with two or more row tiles the waves of one head read the same tiles, and the second
-// read is meant to hit the cache (measured: non-temporal loads there cost 20%).
-template <bool STREAM>
+// RT: 16-row query tiles per wave.  A wave streams the KV tiles of its head once and
+// runs the score / softmax / PV products of its RT query tiles on each of them; the
+// waves_per_head = row_tiles / RT waves of one head split its query tiles.
+// STREAM: every KV tile has exactly one reader (one wave per KV head), so its loads are
+// marked non-temporal and do not displace the lines other waves re-read; where two waves
+// read the same tiles the second read is meant to hit the cache (measured: non-temporal
+// loads there cost 20%).
+template <bool STREAM, int RT>
 __global__ __launch_bounds__(64 * kAttnWavesPerGroup) void attn_mfma_kernel(AttnK a) {
   const int part = blockIdx.x, grp = blockIdx.y;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave index, uniform per wave
   const int lane = threadIdx.x & 63, j = lane & 15, g = lane >> 4;
-  const int kvh = grp * a.heads_per_group + w / a.row_tiles, rt = w % a.row_tiles;
+  const int kvh = grp * a.heads_per_group + w / a.waves_per_head, rt0 = (w % a.waves_per_head) * RT;
   const bool wave_ok = kvh < a.n_kv;
   const int rows = a.G * a.R;
 
@@ -270,25 +274,29 @@ __global__ __launch_bounds__(64 * kAttnWavesPerGroup) void attn_mfma_kernel(Attn
       tend = max(t0, (p0 + bad) * a.page_size);
     }
 
-    bf16x8_t qf[4];
-    int vis = 0;
-    {
-      const int r = rt * 16 + j;
+    bf16x8_t qf[RT][4];
+    int vis[RT];
+    float m[RT], l[RT];
+    floatx4_t O[RT][8];
+#pragma unroll
+    for (int u = 0; u < RT; ++u) {
+      const int r = (rt0 + u) * 16 + j;
+      vis[u] = 0;
       if (r < rows) {
         const int hl = r / a.R, i = r % a.R;
         const uint16_t *qrow = a.q + (((long)b * a.R + i) * a.n_heads + kvh * a.G + hl) * 128;
 #pragma unroll
-        for (int ii = 0; ii < 4; ++ii) qf[ii] = as_bf16x8(*reinterpret_cast<const uint4 *>(qrow + 32 * ii + 8 * g));
-        vis = i < blen ? m0 + i + 1 : 0;
+        for (int ii = 0; ii < 4; ++ii) qf[u][ii] = as_bf16x8(*reinterpret_cast<const uint4 *>(qrow + 32 * ii + 8 * g));
+        vis[u] = i < blen ? m0 + i + 1 : 0;
       } else {
 #pragma unroll
-        for (int ii = 0; ii < 4; ++ii) qf[ii] = as_bf16x8(make_uint4(0, 0, 0, 0));
+        for (int ii = 0; ii < 4; ++ii) qf[u][ii] = as_bf16x8(make_uint4(0, 0, 0, 0));
       }
-    }
-    float m = -INFINITY, l = 0.f;
-    floatx4_t O[8];
+      m[u] = -INFINITY;
+      l[u] = 0.f;
 #pragma unroll
-    for (int mm = 0; mm < 8; ++mm) O[mm] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+      for (int mm = 0; mm < 8; ++mm) O[u][mm] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    }
 
     auto tile_off = [&](int tb) -> long {
       const int page = page_sh[tb / a.page_size - p0];
@@ -323,28 +331,41 @@ __global__ __launch_bounds__(64 * kAttnWavesPerGroup) void attn_mfma_kernel(Attn
           __builtin_amdgcn_sched_barrier(0);
           load_tile(tile_off(t0 + 16 * min(i + d + kAttnRing - 1, n - 1)), ring[(d + kAttnRing - 1) % kAttnRing]);
           __builtin_amdgcn_sched_barrier(0);
-          attn_tile<false>(t0 + 16 * (i + d), L, g, a.scale_log2, ring[d], qf, vis, m, l, O);
+#pragma unroll
+          for (int u = 0; u < RT; ++u)
+            attn_tile<false>(t0 + 16 * (i + d), L, g, a.scale_log2, ring[d], qf[u], vis[u], m[u], l[u], O[u]);
         }
       }
 #pragma unroll
       for (int d = 0; d < kAttnRing - 1; ++d)
-        if (n_pipe + d < n) attn_tile<false>(t0 + 16 * (n_pipe + d), L, g, a.scale_log2, ring[d], qf, vis, m, l, O);
+        if (n_pipe + d < n) {
+#pragma unroll
+          for (int u = 0; u < RT; ++u)
+            attn_tile<false>(t0 + 16 * (n_pipe + d), L, g, a.scale_log2, ring[d], qf[u], vis[u], m[u], l[u], O[u]);
+        }
     }
-    // the causal diagonal and the partial tile at the end of the context
+    // the causal diagonal and the partial tile at the end of the context (the mask zeroes
+    // the V entries past the context in place: applying it again is a no-op)
     for (int tb = t0 + 16 * n; tb < tend; tb += 16) {
       TileBuf t;
       load_tile(tile_off(tb), t);
-      attn_tile<true>(tb, L, g, a.scale_log2, t, qf, vis, m, l, O);
+#pragma unroll
+      for (int u = 0; u < RT; ++u) attn_tile<true>(tb, L, g, a.scale_log2, t, qf[u], vis[u], m[u], l[u], O[u]);
     }
 
-    l += __shfl_xor(l, 16, kWave);
-    l += __shfl_xor(l, 32, kWave);
-    const long prow = ((long)(part + b) * a.n_kv + kvh) * a.rows_pad + rt * 16 + j;
-    if (g == 0) a.part_ml[prow] = make_float2(m, l);
-    float *po = a.part_o + prow * 128;
 #pragma unroll
-    for (int mm = 0; mm < 8; ++mm)
-      *reinterpret_cast<float4 *>(po + 16 * mm + 4 * g) = make_float4(O[mm][0], O[mm][1], O[mm][2], O[mm][3]);
+    for (int u = 0; u < RT; ++u) {
+      float lu = l[u];
+      lu += __shfl_xor(lu, 16, kWave);
+      lu += __shfl_xor(lu, 32, kWave);
+      const long prow = ((long)(part + b) * a.n_kv + kvh) * a.rows_pad + (rt0 + u) * 16 + j;
+      if (g == 0) a.part_ml[prow] = make_float2(m[u], lu);
+      float *po = a.part_o + prow * 128;
+#pragma unroll
+      for (int mm = 0; mm < 8; ++mm)
+        *reinterpret_cast<float4 *>(po + 16 * mm + 4 * g) =
+            make_float4(O[u][mm][0], O[u][mm][1], O[u][mm][2], O[u][mm][3]);
+    }
   }
 }
 
@@ -475,16 +496,18 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnF a) {
 
 // Geometry of the bf16 launch: row tiles per KV head, heads per workgroup, groups.
 struct AttnGeom {
-  int row_tiles, heads_per_group, groups, block;
+  int row_tiles, rt_per_wave, waves_per_head, heads_per_group, groups, block;
 };
 AttnGeom attn_geom(const gm_model_config &cfg, int rows_pad) {
   AttnGeom g;
   g.row_tiles = rows_pad / 16;
-  g.heads_per_group = kAttnWavesPerGroup / g.row_tiles;
+  g.rt_per_wave = g.row_tiles >= 2 ? 2 : 1;
+  g.waves_per_head = g.row_tiles / g.rt_per_wave;
+  g.heads_per_group = kAttnWavesPerGroup / g.waves_per_head;
   if (g.heads_per_group > cfg.n_kv_heads) g.heads_per_group = cfg.n_kv_heads;
   if (g.heads_per_group < 1) g.heads_per_group = 1;
   g.groups = (cfg.n_kv_heads + g.heads_per_group - 1) / g.heads_per_group;
-  g.block = 64 * g.heads_per_group * g.row_tiles;
+  g.block = 64 * g.heads_per_group * g.waves_per_head;
   return g;
 }
 
@@ -499,11 +522,12 @@ int resident_groups(int block) {
   int v = cache[dev][wv].load();
   if (v > 0) return v;
   int per_cu = 0, cus = 0;
-  if (hipFuncSetAttribute((const void *)attn_mfma_kernel<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                          kAttnLdsReserve) != hipSuccess ||
-      hipFuncSetAttribute((const void *)attn_mfma_kernel<false>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                          kAttnLdsReserve) != hipSuccess ||
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_mfma_kernel<false>, block, kAttnLdsReserve) != hipSuccess ||
+  const void *kernels[] = {(const void *)attn_mfma_kernel<true, 1>, (const void *)attn_mfma_kernel<true, 2>,
+                           (const void *)attn_mfma_kernel<false, 2>};
+  bool ok = true;
+  for (const void *f : kernels)
+    ok = ok && hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, kAttnLdsReserve) == hipSuccess;
+  if (!ok || hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_mfma_kernel<true, 2>, block, kAttnLdsReserve) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || per_cu < 1 || cus < 1) {
     (void)hipGetLastError();
     return 256;
@@ -595,13 +619,17 @@ void run_attention(const AttnArgs &a, const AttnPlan &p, char *ws, hipStream_t s
     k.parts = p.parts;
     k.heads_per_group = geo.heads_per_group;
     k.row_tiles = geo.row_tiles;
+    k.waves_per_head = geo.waves_per_head;
     k.scale_log2 = a.scale * 1.4426950408889634f;
     {
       TraceScope ts(a.trace, s);
-      if (geo.row_tiles == 1)
-        hipLaunchKernelGGL(attn_mfma_kernel<true>, dim3(p.parts, geo.groups), dim3(geo.block), kAttnLdsReserve, s, k);
+      const dim3 grid(p.parts, geo.groups), block(geo.block);
+      if (geo.rt_per_wave == 1)
+        hipLaunchKernelGGL((attn_mfma_kernel<true, 1>), grid, block, kAttnLdsReserve, s, k);
+      else if (geo.waves_per_head == 1)
+        hipLaunchKernelGGL((attn_mfma_kernel<true, 2>), grid, block, kAttnLdsReserve, s, k);
       else
-        hipLaunchKernelGGL(attn_mfma_kernel<false>, dim3(p.parts, geo.groups), dim3(geo.block), kAttnLdsReserve, s, k);
+        hipLaunchKernelGGL((attn_mfma_kernel<false, 2>), grid, block, kAttnLdsReserve, s, k);
     }
     TraceScope ts(a.trace_combine, s);
     const int items = a.n_kv * G * a.R * 32;

@@ -578,9 +578,15 @@ void launch_stream_shape(int shape, const GemmS &g, hipStream_t s) {
 //    take 128- or 256-row tiles, so each weight strip is fetched once (at 256
 //    rows measured 270 us against 330 us with four 64-row tiles per strip);
 //  * everything else uses 64-row tiles: the M tiles of one strip run on the
-//    same XCD and re-read it from that XCD's L2, plus,
-//    for narrow outputs, a K split capped so that the float32 partials move
-//    at most half as many bytes as the weights.
+//    same XCD and re-read it from that XCD's L2, plus, for narrow outputs, a
+//    K split.  The split takes the most workgroups that still fit one per CU:
+//    a CU that gets a second workgroup streams twice the bytes and holds up
+//    the launch (measured at 64 rows: down projection 19 us with 13 splits,
+//    260 workgroups; 14 us with 10).  It is capped so that the float32
+//    partials (written, then read) move at most half as many bytes as the
+//    weights at one M tile, as many at several (where each workgroup carries
+//    more fixed cost per weight byte: 256 rows, o projection 17 us with 3
+//    splits, 19 us with 2).
 GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
   GemmPlan p{};
   if (dtype != GM_BF16 || M <= 0) return p;
@@ -594,8 +600,9 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
   const int ITER = 8;                               // k32 steps per unrolled iteration (see kernel)
   p.m_tiles = (M + BM - 1) / BM;
   p.k_iters = K / (ITER * 32);
-  int splits = (target + p.n_tiles * p.m_tiles - 1) / (p.n_tiles * p.m_tiles);
-  const int cap = K / (8 * M);                      // 2 * S * M * Nw * 4 <= Nw * K * 2 / 2
+  int splits = target / (p.n_tiles * p.m_tiles);
+  // 2 * S * M * Nw * 4 <= Nw * K * 2 / 2 (one M tile), <= Nw * K * 2 (several)
+  const int cap = p.m_tiles > 1 ? K / (4 * M) : K / (8 * M);
   if (splits > cap) splits = cap;
   if (splits > p.k_iters) splits = p.k_iters;
   if (splits < 1 || epi == EPI_STATS) splits = 1;   // tile statistics need whole dot products

@@ -427,6 +427,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF g) {
 // (row, wave): the tiles of the draw are the waves' ranges.
 constexpr int kLmStrips = 10;
 constexpr int kLmRing = 4;
+static_assert(kLmStrips * kStripIds <= kMaxDrawTileIds, "the draw scans a whole strip range");
 
 struct GemmL {
   const uint16_t *X, *W;

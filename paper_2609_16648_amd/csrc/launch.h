@@ -48,9 +48,14 @@ inline int scan_chunks(int V) { return (V + kScanChunk - 1) / kScanChunk; }
 // LM-head GEMM epilogue emits; a draw from such a row needs no further pass over
 // the vocabulary.  The row's ids are cut into `strips` strips of 16 and the
 // strips into `tiles` tiles: tile t holds strips [t S / T, (t + 1) S / T)
-// (integer division), at most kMaxTileStrips of them.
+// (integer division).
 constexpr int kStripIds = 16;
-constexpr int kMaxTileStrips = 8;              // 128 ids
+constexpr int kMaxTileStrips = 8;              // 128 ids (fixed tiles and the tiled GEMM's statistics)
+// The draw scans the ids of one tile with kDrawRun consecutive ids per lane of a
+// wave, so it takes tiles of up to kMaxDrawTileIds ids (the strip ranges of the
+// draft head's LM head hold up to 160).
+constexpr int kDrawRun = 3;
+constexpr int kMaxDrawTileIds = kDrawRun * 64;
 constexpr int kMaxTiles = 4096;                // the draw stages a row's tile statistics in 64 KiB of LDS
 constexpr int kMaxVocab = kMaxTiles * kMaxTileStrips * kStripIds;
 struct TileGeom {

@@ -470,8 +470,9 @@ __device__ __forceinline__ double block_incl_scan(double v, double *wsum /* >= 4
 // masses s_t exp(m_t - M) in float64, contiguous runs of them per thread, a
 // block-wide prefix sum over the runs, and the first run whose prefix passes
 // u * S is walked tile by tile to the tile holding u * S.  One wave then scans
-// that tile's ids (at most 128; the same per-id terms exp(z / T - m_t) the tile sums
-// were made of, scaled in float64) for the first running sum above u * S.
+// that tile's ids (at most kMaxDrawTileIds, kDrawRun consecutive ids per lane; the
+// same per-id terms exp(z / T - m_t) the tile sums were made of, scaled in float64)
+// for the first running sum above u * S.
 __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float inv_t, const float *__restrict__ logits,
                                                         long row_stride, const RowStat *__restrict__ tiles,
                                                         TileGeom geo, const float *__restrict__ u, int u_stride,
@@ -555,10 +556,14 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
   const double scale = exp((double)mt - M);
   const float *row = logits + (long)b * row_stride;
   const int lo = tile_first_strip(geo, tile) * kStripIds, hi = min(V, tile_first_strip(geo, tile + 1) * kStripIds);
-  const int xa = lo + 2 * lane, xb = xa + 1;   // two consecutive ids per lane
-  const double ea = xa < hi ? (double)expf(row[xa] * inv_t - mt) * scale : 0.0;
-  const double eb = xb < hi ? (double)expf(row[xb] * inv_t - mt) * scale : 0.0;
-  double incl2 = ea + eb;
+  const int x0 = lo + kDrawRun * lane;   // kDrawRun consecutive ids per lane
+  double e[kDrawRun], run = 0.0;
+#pragma unroll
+  for (int q = 0; q < kDrawRun; ++q) {
+    e[q] = x0 + q < hi ? (double)expf(row[x0 + q] * inv_t - mt) * scale : 0.0;
+    run += e[q];
+  }
+  double incl2 = run;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     const double n = __shfl_up(incl2, o, kWave);
@@ -566,14 +571,22 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
   }
   double excl = __shfl_up(incl2, 1, kWave);
   if (lane == 0) excl = 0.0;
-  const double acc_a = sh_base + excl + ea, acc_b = acc_a + eb;
-  const unsigned long long hitm = __ballot(acc_a > sh_t || acc_b > sh_t);
-  const unsigned long long nz = __ballot(ea > 0.0 || eb > 0.0);
-  // the first hit lane decides between its two ids (running sums grow along lanes)
+  // running sum after each of this lane's ids; the first id whose sum passes u * S
+  double c = sh_base + excl;
+  int pick = -1, lastq = -1;
+#pragma unroll
+  for (int q = 0; q < kDrawRun; ++q) {
+    c += e[q];
+    if (pick < 0 && c > sh_t) pick = q;
+    if (e[q] > 0.0) lastq = q;
+  }
+  const unsigned long long hitm = __ballot(pick >= 0);
+  const unsigned long long nz = __ballot(lastq >= 0);
+  // running sums grow along lanes: the first hit lane holds the drawn id
   const int first = hitm ? __ffsll((long long)hitm) - 1 : -1;
   const int lastnz = nz ? 63 - __clzll((long long)nz) : -1;
-  if (first >= 0 && lane == first) dst[(long)b * dst_stride] = acc_a > sh_t ? xa : xb;
-  if (first < 0 && lastnz >= 0 && lane == lastnz) dst[(long)b * dst_stride] = eb > 0.0 ? xb : xa;
+  if (first >= 0 && lane == first) dst[(long)b * dst_stride] = x0 + pick;
+  if (first < 0 && lastnz >= 0 && lane == lastnz) dst[(long)b * dst_stride] = x0 + lastq;
   if (first < 0 && lastnz < 0 && lane == 0) dst[(long)b * dst_stride] = a;
 }
 

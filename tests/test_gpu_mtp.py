@@ -129,6 +129,47 @@ def test_qwen_layer_bf16_mtp_sample_logits(qwen_mtp):
     assert ((got >= 0) & (got < shape.vocab)).all()
 
 
+@pytest.mark.parametrize("temperature", [1.0, 0.7])
+def test_qwen_layer_bf16_mtp_sample_draw_from_own_logits(qwen_mtp, temperature):
+    # Each sampled draft is the inverse-CDF draw from softmax(z / T) of the logits the
+    # head itself wrote (Sec. 2.2: drafts are samples of q).  For every row, u * Z must
+    # fall in the drawn id's CDF interval [C(x - 1), C(x)) of those logits, widened by
+    # 1e-6 Z for the float32 terms (the window of the float32 large-vocabulary draws).  The LM
+    # head's statistics tiles here are strip ranges of up to 160 ids, so a draw that
+    # reached only part of a tile lands intervals away and fails within a few rows.
+    need_gpu()
+    shape, W, Wm = qwen_mtp
+    k = 3
+    lens, caches, hidden, n, out, u = _inputs(shape, 64, k, 1, 3000, 6)
+    B = len(lens)
+    model, mtp = gm.DeviceModel(shape, W), gm.DeviceMtp(shape, Wm)
+    cache = device_cache(shape, caches, lens, 2 * k + 2)
+    drafts = torch.zeros((B, k), dtype=torch.int32, device="cuda")
+    dlog = torch.zeros((B, k, shape.vocab), dtype=torch.float32, device="cuda")
+    gm.mtp_draft(model, mtp, cache, k, gm.GM_SAMPLE, t32(hidden), i32(n), i32(out), t32(u), drafts, dlog,
+                 gm.Workspace(), temperature=temperature)
+    torch.cuda.synchronize()
+    z = dlog.cpu().numpy()
+    got = drafts.cpu().numpy()
+    inv_t = float(np.float32(1.0 / temperature))
+    exact, in_tail = 0, 0
+    strips = shape.vocab // 16
+    first = (np.arange(1025) * strips) // 1024   # first strip of each range when the chip holds 1024 waves
+    for b in range(B):
+        for j in range(k):
+            c = np.cumsum(oracle.softmax(z[b, j].astype(np.float64) * inv_t))
+            t, x = float(u[b, j]) * c[-1], int(got[b, j])
+            assert 0 <= x < shape.vocab
+            lo = c[x - 1] if x > 0 else 0.0
+            assert lo - 1e-6 * c[-1] <= t < c[x] + 1e-6 * c[-1], (b, j, x, (t - lo) / c[-1], (c[x] - t) / c[-1])
+            ref = oracle.inverse_cdf(oracle.softmax(z[b, j].astype(np.float64) * inv_t), u[b, j])[0]
+            exact += int(ref == x)
+            r = int(np.searchsorted(first, ref // 16, side="right")) - 1
+            in_tail += int(ref - 16 * first[r] >= 128)
+    print("[mtp bf16 draw T=%.1f] %d draws, %d identical to the oracle's, %d past the 128th id of their range"
+          % (temperature, B * k, exact, in_tail), flush=True)
+
+
 def test_f32_mtp_large_vocab_sample():
     # sampled drafts over a 151936-id vocabulary: float32 logits agree with the oracle to ~1e-6
     # relative, so a draw is compared outside a 1e-6 window around the CDF edges

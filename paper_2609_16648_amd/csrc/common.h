@@ -53,6 +53,15 @@ __device__ __forceinline__ uint4 load_nt(const void *p) {
 __device__ __forceinline__ bf16x4_t as_bf16x4(uint2 v) { return __builtin_bit_cast(bf16x4_t, v); }
 
 // ----------------------------------------------------------------- reductions
+// Orders this wave's LDS writes before its later LDS reads by other lanes (a
+// wave's LDS operations complete in order; this keeps the compiler from moving
+// them across and waits for the writes).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);

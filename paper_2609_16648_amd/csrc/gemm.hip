@@ -423,8 +423,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF g) {
 // A-operand order) stream through a kLmRing-step register ring with
 // unconditional loads, and there is no LDS and no barrier, so no wave ever
 // waits for another.  EPI_STATS: the softmax statistics of Y / T are taken per
-// row over the wave's own range (float32 terms, float64 sums), one RowStat per
-// (row, wave): the tiles of the draw are the waves' ranges.
+// row over the wave's own range (float32 terms, summed per lane in float32, the
+// 16 lane sums of a row in float64), one RowStat per (row, wave): the tiles of
+// the draw are the waves' ranges.
 constexpr int kLmStrips = 10;
 constexpr int kLmRing = 4;
 static_assert(kLmStrips * kStripIds <= kMaxDrawTileIds, "the draw scans a whole strip range");
@@ -494,14 +495,32 @@ __global__ __launch_bounds__(256) void lm_strips_kernel(GemmL g) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int m = 16 * a + 4 * g4 + r;
-      const bool row_ok = m < g.M;
-      if (row_ok) {
+      if (m < g.M) {
         float *y = g.Y + (long)m * g.ldy + (long)s0 * 16 + j;
 #pragma unroll
         for (int t = 0; t < kLmStrips; ++t)
           if (t < n) y[16 * t] = acc[a][t][r];
       }
-      if (EPI == EPI_STATS) {
+    }
+  }
+  if (EPI == EPI_STATS) {
+    // Softmax statistics of the range per row.  A row's values sit in the 16 lanes
+    // of one lane group (j) times the range's strips.  Each lane's per-row partials
+    // go through this wave's slice of LDS, where lane L then owns row L: the
+    // partial maxima (and lowest ids) meet there, the row maxima go back to the
+    // lanes, and their partial sums of exp(z / T - max) (float32, at most
+    // kLmStrips terms) meet again and are added in float64.  No cross-lane
+    // shuffles and no branches on the lane.
+    __shared__ float sh_part[4][64 * 17];   // [row][lane group j], padded
+    __shared__ int sh_arg[4][64 * 17];
+    __shared__ float sh_rmax[4][64];
+    const int wv = threadIdx.x >> 6;
+    float *pf = sh_part[wv], *rmax = sh_rmax[wv];
+    int *pa = sh_arg[wv];
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
         float vmax = -INFINITY;
         int varg = 0x7fffffff;
 #pragma unroll
@@ -509,26 +528,45 @@ __global__ __launch_bounds__(256) void lm_strips_kernel(GemmL g) {
           const float v = acc[a][t][r] * g.inv_t;
           if (t < n && v > vmax) { vmax = v; varg = (s0 + t) * 16 + j; }   // ascending ids per lane
         }
+        const int row = 16 * a + 4 * g4 + r;
+        pf[row * 17 + j] = vmax;
+        pa[row * 17 + j] = varg;
+      }
+    }
+    wave_lds_sync();
+    float M = -INFINITY;
+    int A = 0x7fffffff;
 #pragma unroll
-        for (int o = 1; o < 16; o <<= 1) {
-          const float om = __shfl_xor(vmax, o, kWave);
-          const int oa = __shfl_xor(varg, o, kWave);
-          if (om > vmax || (om == vmax && oa < varg)) { vmax = om; varg = oa; }
-        }
-        double sum = 0.0;
+    for (int q = 0; q < 16; ++q) {
+      const float mq = pf[lane * 17 + q];
+      const int aq = pa[lane * 17 + q];
+      if (mq > M || (mq == M && aq < A)) { M = mq; A = aq; }
+    }
+    rmax[lane] = M;
+    wave_lds_sync();
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * a + 4 * g4 + r;
+        const float mr = rmax[row];
+        float sum = 0.f;
 #pragma unroll
         for (int t = 0; t < kLmStrips; ++t)
-          if (t < n) sum += (double)expf(acc[a][t][r] * g.inv_t - vmax);
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) sum += __shfl_xor(sum, o, kWave);
-        if (row_ok && j == 0) {
-          RowStat st;
-          st.max = vmax;
-          st.argmax = varg;
-          st.sum = sum;
-          g.stats[(long)m * g.geo.tiles + wid] = st;
-        }
+          if (t < n) sum += expf(acc[a][t][r] * g.inv_t - mr);
+        pf[row * 17 + j] = sum;
       }
+    }
+    wave_lds_sync();
+    double S = 0.0;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) S += (double)pf[lane * 17 + q];
+    if (lane < g.M) {
+      RowStat st;
+      st.max = M;
+      st.argmax = A;
+      st.sum = S;
+      g.stats[(long)lane * g.geo.tiles + wid] = st;
     }
   }
 }

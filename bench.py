@@ -79,7 +79,8 @@ def accounting(wl, lens):
         put("gemm_down", gemm(M, H, F, 4, add=True), L)
         put("gemm_lm_head", gemm(M, V, H, 4), 1)
     put("attn_verify", (attn_flops, kv_bytes + 2.0 * 2 * M * qd), L)
-    put("accept_row_stats", (0.0, 4.0 * B * (2 * k + 1) * V), 1)
+    # the target rows; the draft rows' statistics come from the draft head when it runs in the step
+    put("accept_row_stats", (0.0, 4.0 * B * ((k + 1) if wl.with_mtp else (2 * k + 1)) * V), 1)
     if wl.with_mtp:
         mkv = float((lens.astype(np.float64) * nkv * d * 2 * 2).sum())
         put("mtp_gemm_lm_head", gemm(B, V, H, 4), k)
@@ -143,6 +144,15 @@ class Step:
             self.logits = torch.empty((B, k + 1, V), dtype=torch.float32, device=device)
             self.hidden = torch.empty((B, k + 1, s.hidden), dtype=torch.float32, device=device)
             if wl.with_mtp:
+                # zq stands in for the draft logits the previous step's head wrote; the head
+                # also hands the accept their softmax statistics, so those come with them
+                zq = self.zq.cpu().numpy()
+                st = np.zeros((B, k), dtype=[("max", "<f4"), ("argmax", "<i4"), ("sum", "<f8")])
+                st["max"] = zq.max(-1)
+                st["argmax"] = zq.argmax(-1)
+                st["sum"] = np.exp(zq.astype(np.float64) - st["max"][..., None].astype(np.float64)).sum(-1)
+                self.zq_stats = torch.from_numpy(st.view(np.uint8).reshape(B, k, gm.ROW_STATS_BYTES).copy()).to(device)
+                self.next_stats = gm.new_row_stats(B, k, device)
                 self.Wm = synth.mtp_weights(s)
                 self.mtp = gm.DeviceMtp(s, self.Wm, device)
                 self.mcache = gm.PagedCache(s, 1, self.lens, cap, page_size=wl.page_size, fill="empty")
@@ -182,12 +192,13 @@ class Step:
             gm.kv_commit(self.cache, k, self.n, self.slots)
             return
         gm.verify_forward(self.model, self.cache, self.tokens, self.logits, self.hidden, self.ws_v)
-        gm.spec_accept(self.logits, self.zq, self.drafts, self.ua, self.uf, self.n, self.out, self.mode, self.ws_a)
+        gm.spec_accept(self.logits, self.zq, self.drafts, self.ua, self.uf, self.n, self.out, self.mode, self.ws_a,
+                       draft_stats=self.zq_stats if wl.with_mtp else None)
         gm.kv_commit(self.cache, k, self.n, self.slots)
         if wl.with_mtp:
             self.mcache.seq_lens.copy_(self.lens0)
             gm.mtp_draft(self.model, self.mtp, self.mcache, k, self.mode, self.hidden, self.n, self.out, self.ud,
-                         self.next_drafts, self.dlog, self.ws_m)
+                         self.next_drafts, self.dlog, self.ws_m, draft_stats=self.next_stats)
 
 
 # ----------------------------------------------------------------------------- CPU baseline

@@ -142,6 +142,16 @@ typedef struct {
   int max_ctx;                 /* host: an upper bound on every seq_lens[b] */
 } gm_kv_cache;
 
+/* Softmax statistics of one logits row z at temperature T: the max of z / T,
+ * the lowest id attaining it, and sum over ids of exp(z / T - max).
+ * gm_mtp_draft can emit them for its draft logits; gm_spec_accept can take them
+ * in place of its own pass over those rows (q's normaliser, Sec. 2.2). */
+typedef struct {
+  float max;
+  int32_t argmax;
+  double sum;
+} gm_row_stats;
+
 /* Bytes of workspace the given call needs (0 on invalid arguments).
  * `max_ctx` is the bound that the call's gm_kv_cache carries. */
 size_t gm_workspace_size(int op, const gm_model_config *cfg, int B, int k, int max_ctx);
@@ -180,11 +190,16 @@ gm_status gm_verify_attention(const gm_model_config *cfg, const gm_kv_cache *cac
  *   w = p_k (bonus token) if n = k.
  * GM_GREEDY: d_i is accepted iff it is the argmax of target_logits[b][i]
  *   (lowest id on ties); the final token is the argmax of row n.
- *   draft_logits, u_accept and u_final may be NULL.
+ *   draft_logits, draft_stats, u_accept and u_final may be NULL.
+ * draft_stats [B][k] (may be NULL; read in GM_SAMPLE mode only): the statistics
+ *   of softmax(draft_logits[b][i] / T) at this temperature, as gm_mtp_draft
+ *   writes them.  Given, they stand in for a pass over the draft rows; the
+ *   caller guarantees that they describe these draft_logits.
  * Outputs: n_accept [B] in [0, k]; out_tokens [B][k+1] = d_0..d_{n-1}, final, -1 pad.
  * The logits rows are read in place; no probability matrix is written. */
 gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature,
                          const float *target_logits, const float *draft_logits,
+                         const gm_row_stats *draft_stats,
                          const int32_t *draft_tokens, const float *u_accept, const float *u_final,
                          int32_t *n_accept, int32_t *out_tokens, void *ws, size_t ws_bytes,
                          void *stream);
@@ -211,14 +226,17 @@ gm_status gm_kv_commit(const gm_kv_cache *cache, int B, int k, const int32_t *n_
  * past the committed length and are overwritten by the next extend.
  * Drafts are argmax (GM_GREEDY) or inverse-CDF draws with u_draft[b][j]
  * (GM_SAMPLE) from softmax(z / T).  Outputs: drafts [B][k],
- * draft_logits [B][k][vocab] float32.  Errors: GM_ERR_CAPACITY if
- * max_ctx + 2k + 1 > max_pages_per_seq * page_size of the head's cache. */
+ * draft_logits [B][k][vocab] float32, and (if draft_stats is not NULL)
+ * draft_stats [B][k], the softmax statistics of each draft_logits row at T
+ * (the draw's own; gm_spec_accept takes them for the same rows and T).
+ * Errors: GM_ERR_CAPACITY if max_ctx + 2k + 1 > max_pages_per_seq * page_size
+ * of the head's cache. */
 gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weights *mtp,
                        const gm_model_weights *shared, const gm_kv_cache *mtp_cache, int B, int k,
                        int mode, float temperature, const float *verify_hidden,
                        const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft,
-                       int32_t *drafts, float *draft_logits, void *ws, size_t ws_bytes,
-                       int32_t *dev_err, void *stream);
+                       int32_t *drafts, float *draft_logits, gm_row_stats *draft_stats, void *ws,
+                       size_t ws_bytes, int32_t *dev_err, void *stream);
 
 /* Thread-local message describing the last non-OK status of this thread. */
 const char *gm_last_error(void);

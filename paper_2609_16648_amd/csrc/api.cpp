@@ -2,6 +2,7 @@
 // Every entry point validates on the host, then enqueues on the caller's
 // stream and returns without synchronising.
 #include <stdarg.h>
+#include <stddef.h>
 #include <stdio.h>
 
 #include <string>
@@ -135,8 +136,14 @@ extern "C" size_t gm_workspace_size(int op, const gm_model_config *cfg, int B, i
 }
 
 // ---------------------------------------------------------------- gm_spec_accept
+static_assert(sizeof(gm_row_stats) == sizeof(RowStat) && offsetof(gm_row_stats, max) == offsetof(RowStat, max) &&
+                  offsetof(gm_row_stats, argmax) == offsetof(RowStat, argmax) &&
+                  offsetof(gm_row_stats, sum) == offsetof(RowStat, sum),
+              "gm_row_stats is the device's RowStat");
+
 extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature, const float *target_logits,
-                                    const float *draft_logits, const int32_t *draft_tokens, const float *u_accept,
+                                    const float *draft_logits, const gm_row_stats *draft_stats,
+                                    const int32_t *draft_tokens, const float *u_accept,
                                     const float *u_final, int32_t *n_accept, int32_t *out_tokens, void *ws,
                                     size_t ws_bytes, void *stream) {
   if (B < 0 || k < 0 || k > kMaxK || V < 1) return fail(GM_ERR_INVALID_ARG, "bad B=%d k=%d V=%d", B, k, V);
@@ -159,8 +166,17 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
   RowSel *sel = (RowSel *)(w + p.sel);
   const float inv_t = 1.0f / temperature;
   launch_row_stats("accept_row_stats", target_logits, V, B * (k + 1), V, inv_t, tstat, s);
-  if (mode == GM_SAMPLE && k > 0) launch_row_stats("accept_row_stats", draft_logits, V, B * k, V, inv_t, dstat, s);
-  launch_accept_decide(B, k, V, mode, inv_t, target_logits, draft_logits, tstat, dstat, draft_tokens, u_accept,
+  // q's statistics: the draft head's own (one per row) when the caller has them, else a pass over the rows
+  int nch_d = stat_chunks(V);
+  if (mode == GM_SAMPLE && k > 0) {
+    if (draft_stats) {
+      dstat = (RowStat *)draft_stats;
+      nch_d = 1;
+    } else {
+      launch_row_stats("accept_row_stats", draft_logits, V, B * k, V, inv_t, dstat, s);
+    }
+  }
+  launch_accept_decide(B, k, V, mode, inv_t, target_logits, draft_logits, tstat, dstat, nch_d, draft_tokens, u_accept,
                        u_final, n_accept, out_tokens, sel, s);
   if (mode == GM_SAMPLE) launch_residual_draw("accept_residual_chunk", "accept_residual_scan", B, V, inv_t, sel, (double *)(w + p.wsum), (double *)(w + p.psum), s);
   return check_launch("gm_spec_accept");
@@ -228,8 +244,9 @@ extern "C" gm_status gm_verify_forward(const gm_model_config *cfg, const gm_mode
 extern "C" gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weights *mtp, const gm_model_weights *shared,
                                   const gm_kv_cache *mtp_cache, int B, int k, int mode, float temperature,
                                   const float *verify_hidden, const int32_t *n_accept, const int32_t *out_tokens,
-                                  const float *u_draft, int32_t *drafts, float *draft_logits, void *ws,
-                                  size_t ws_bytes, int32_t *dev_err, void *stream) {
+                                  const float *u_draft, int32_t *drafts, float *draft_logits,
+                                  gm_row_stats *draft_stats, void *ws, size_t ws_bytes, int32_t *dev_err,
+                                  void *stream) {
   gm_status st = check_config(cfg, B, k);
   if (st != GM_OK) return st;
   if (k < 1) return fail(GM_ERR_INVALID_ARG, "gm_mtp_draft needs k >= 1");
@@ -248,6 +265,6 @@ extern "C" gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weigh
   st = check_ws(ws, ws_bytes, p.total);
   if (st != GM_OK) return st;
   run_mtp_draft(*cfg, *mtp, *shared, *mtp_cache, B, k, mode, 1.0f / temperature, verify_hidden, n_accept, out_tokens,
-                u_draft, drafts, draft_logits, p, (char *)ws, dev_err, (hipStream_t)stream);
+                u_draft, drafts, draft_logits, (RowStat *)draft_stats, p, (char *)ws, dev_err, (hipStream_t)stream);
   return check_launch("gm_mtp_draft");
 }

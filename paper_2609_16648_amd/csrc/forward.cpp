@@ -154,7 +154,8 @@ MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx) {
 void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const gm_model_weights &shared,
                    const gm_kv_cache &c, int B, int k, int mode, float inv_t, const float *verify_hidden,
                    const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft, int32_t *drafts,
-                   float *draft_logits, const MtpPlan &p, char *ws, int32_t *dev_err, hipStream_t s) {
+                   float *draft_logits, RowStat *draft_stats, const MtpPlan &p, char *ws, int32_t *dev_err,
+                   hipStream_t s) {
   const int R = k + 1, Me = B * R, H = cfg.hidden, F = cfg.ffn, V = cfg.vocab, dt = cfg.dtype;
   const int qd = cfg.n_heads * cfg.head_dim, qw = qkv_width(cfg);
   const size_t e = esize(dt);
@@ -179,7 +180,7 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
     launch_gemm("mtp_gemm_lm_head", dt, EPI_STATS, B, V, H, nbuf, H, shared.lm_head, zl, (long)k * V, part, s, tiles,
                 inv_t);
     launch_tile_draw(B, V, mode, inv_t, zl, (long)k * V, plan_lm_head(dt, B, V, H), tiles, u_draft ? u_draft + j : nullptr,
-                     k, drafts + j, k, s);
+                     k, drafts + j, k, draft_stats ? draft_stats + j : nullptr, k, s);
   };
 
   // ---- extend: rows (h_{m+i}, x_{m+i+1}), i = 0..n_b, at slots m_b + i

@@ -124,6 +124,7 @@ MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx);
 void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const gm_model_weights &shared,
                    const gm_kv_cache &c, int B, int k, int mode, float inv_t, const float *verify_hidden,
                    const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft, int32_t *drafts,
-                   float *draft_logits, const MtpPlan &p, char *ws, int32_t *dev_err, hipStream_t s);
+                   float *draft_logits, RowStat *draft_stats, const MtpPlan &p, char *ws, int32_t *dev_err,
+                   hipStream_t s);
 
 }  // namespace gm

@@ -72,14 +72,16 @@ void launch_tile_stats(const float *logits, long row_stride, int n_rows, int V, 
                        RowStat *tiles, hipStream_t s);
 // one draw per row from softmax(z / T) given its tile statistics: argmax (greedy) or the
 // inverse-CDF draw with u[b * u_stride]; writes dst[b * dst_stride]
+// row_out (may be null): the row's combined statistics at row_out[b * row_stride_out]
 void launch_tile_draw(int B, int V, int mode, float inv_t, const float *logits, long row_stride, TileGeom geo,
                       const RowStat *tiles, const float *u, int u_stride, int32_t *dst, int dst_stride,
-                      hipStream_t s);
+                      RowStat *row_out, int row_stride_out, hipStream_t s);
 
 void launch_row_stats(const char *name, const float *logits, long row_stride, int n_rows, int V, float inv_t,
                       RowStat *out, hipStream_t s);
+// dstat holds nch_d RowStats per draft row (chunk statistics, or one combined per row)
 void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const float *tlog,
-                          const float *dlog, const RowStat *tstat, const RowStat *dstat,
+                          const float *dlog, const RowStat *tstat, const RowStat *dstat, int nch_d,
                           const int32_t *drafts, const float *u_accept, const float *u_final,
                           int32_t *n_accept, int32_t *out_tokens, RowSel *sel, hipStream_t s);
 void launch_residual_draw(const char *chunk_name, const char *scan_name, int B, int V, float inv_t, const RowSel *sel, double *wsum,

@@ -121,7 +121,7 @@ __global__ __launch_bounds__(64) void accept_decide_kernel(int B, int k, int V, 
                                                            const float *__restrict__ tlog,
                                                            const float *__restrict__ dlog,
                                                            const RowStat *__restrict__ tstat,
-                                                           const RowStat *__restrict__ dstat, int nch,
+                                                           const RowStat *__restrict__ dstat, int nch, int nch_d,
                                                            const int32_t *__restrict__ drafts,
                                                            const float *__restrict__ u_acc,
                                                            const float *__restrict__ u_fin,
@@ -134,8 +134,8 @@ __global__ __launch_bounds__(64) void accept_decide_kernel(int B, int k, int V, 
   double M = 0.0, S = 1.0;
   int am = 0;
   if (is_t || is_d) {
-    const RowStat *st = is_t ? tstat + (long)(b * k1 + lane) * nch : dstat + (long)(b * k + lane - k1) * nch;
-    combine_stats(st, nch, M, S, am);
+    const RowStat *st = is_t ? tstat + (long)(b * k1 + lane) * nch : dstat + (long)(b * k + lane - k1) * nch_d;
+    combine_stats(st, is_t ? nch : nch_d, M, S, am);
   }
   // the draft row statistics moved to the lane of the same position
   const double Mq = __shfl(M, k1 + lane < 64 ? k1 + lane : lane, kWave);
@@ -194,13 +194,13 @@ __global__ __launch_bounds__(64) void accept_decide_kernel(int B, int k, int V, 
 }
 
 void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const float *tlog,
-                          const float *dlog, const RowStat *tstat, const RowStat *dstat,
+                          const float *dlog, const RowStat *tstat, const RowStat *dstat, int nch_d,
                           const int32_t *drafts, const float *u_accept, const float *u_final,
                           int32_t *n_accept, int32_t *out_tokens, RowSel *sel, hipStream_t s) {
   if (B <= 0) return;
   TraceScope ts("accept_decide", s);
   hipLaunchKernelGGL(accept_decide_kernel, dim3(B), dim3(64), 0, s, B, k, V, mode, inv_t, tlog, dlog, tstat, dstat,
-                     stat_chunks(V), drafts, u_accept, u_final, n_accept, out_tokens, sel);
+                     stat_chunks(V), nch_d, drafts, u_accept, u_final, n_accept, out_tokens, sel);
 }
 
 // ------------------------------------------------------------------ 3. inverse-CDF draw
@@ -476,7 +476,8 @@ __device__ __forceinline__ double block_incl_scan(double v, double *wsum /* >= 4
 __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float inv_t, const float *__restrict__ logits,
                                                         long row_stride, const RowStat *__restrict__ tiles,
                                                         TileGeom geo, const float *__restrict__ u, int u_stride,
-                                                        int32_t *__restrict__ dst, int dst_stride) {
+                                                        int32_t *__restrict__ dst, int dst_stride,
+                                                        RowStat *__restrict__ row_out, int row_stride_out) {
   const int n_tiles = geo.tiles;
   extern __shared__ uint4 st_raw[];   // [n_tiles] RowStat
   RowStat *st = reinterpret_cast<RowStat *>(st_raw);
@@ -520,7 +521,7 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
   a = red_a[0];
   for (int w = 1; w < 4; ++w)
     if (red_m[w] > m || (red_m[w] == m && red_a[w] < a)) { m = red_m[w]; a = red_a[w]; }
-  if (mode == GM_GREEDY) {
+  if (mode == GM_GREEDY && !row_out) {
     if (tid == 0) dst[(long)b * dst_stride] = a;
     return;
   }
@@ -530,6 +531,17 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
   for (int t = t0; t < t1; ++t) w += st[t].sum * exp((double)st[t].max - M);
   const double incl = block_incl_scan(w, wsum);
   const double S = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+  if (row_out && tid == 0) {   // the row's statistics, for the accept of this draft
+    RowStat o;
+    o.max = m;
+    o.argmax = a;
+    o.sum = S;
+    row_out[(long)b * row_stride_out] = o;
+  }
+  if (mode == GM_GREEDY) {
+    if (tid == 0) dst[(long)b * dst_stride] = a;
+    return;
+  }
   const double target = (double)u[(long)b * u_stride] * S;
   if (incl > target) atomicMin(&sh_hit, tid);   // first run whose prefix passes u * S
   if (w > 0.0) atomicMax(&sh_last, tid);       // last run with mass (rounding fallback)
@@ -591,11 +603,12 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
 }
 
 void launch_tile_draw(int B, int V, int mode, float inv_t, const float *logits, long row_stride, TileGeom geo,
-                      const RowStat *tiles, const float *u, int u_stride, int32_t *dst, int dst_stride, hipStream_t s) {
+                      const RowStat *tiles, const float *u, int u_stride, int32_t *dst, int dst_stride,
+                      RowStat *row_out, int row_stride_out, hipStream_t s) {
   if (B <= 0) return;
   TraceScope ts("draft_draw", s);
   hipLaunchKernelGGL(tile_draw_kernel, dim3(B), dim3(256), (size_t)geo.tiles * sizeof(RowStat), s, V, mode, inv_t,
-                     logits, row_stride, tiles, geo, u, u_stride, dst, dst_stride);
+                     logits, row_stride, tiles, geo, u, u_stride, dst, dst_stride, row_out, row_stride_out);
 }
 
 }  // namespace gm

@@ -86,13 +86,13 @@ def lib() -> ctypes.CDLL:
                                       c_void_p, c_size_t, c_void_p, c_void_p]
     L.gm_spec_accept.restype = c_int
     L.gm_spec_accept.argtypes = [c_int, c_int, c_int, c_int, c_float, c_void_p, c_void_p, c_void_p, c_void_p,
-                                 c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
+                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
     L.gm_kv_commit.restype = c_int
     L.gm_kv_commit.argtypes = [P(KVCacheDesc), c_int, c_int, c_void_p, c_void_p, c_void_p]
     L.gm_mtp_draft.restype = c_int
     L.gm_mtp_draft.argtypes = [P(ModelConfig), P(MtpWeights), P(ModelWeights), P(KVCacheDesc), c_int, c_int,
                                c_int, c_float, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
-                               c_void_p, c_size_t, c_void_p, c_void_p]
+                               c_void_p, c_void_p, c_size_t, c_void_p, c_void_p]
     L.gm_last_error.restype = ctypes.c_char_p
     L.gm_last_error.argtypes = []
     L.gm_trace_start.restype = c_int
@@ -323,9 +323,26 @@ def verify_attention(cfg: ModelConfig, cache: PagedCache, layer: int, q: torch.T
                                      _ptr(buf), buf.numel(), _ptr(dev_err), _stream(stream)))
 
 
+ROW_STATS_BYTES = 16   # gm_row_stats: float max, int32 argmax, double sum
+
+
+def new_row_stats(B: int, k: int, device="cuda") -> torch.Tensor:
+    """Storage for [B][k] gm_row_stats (as bytes)."""
+    return torch.zeros((B, k, ROW_STATS_BYTES), dtype=torch.uint8, device=device)
+
+
+def decode_row_stats(t: torch.Tensor):
+    """(max float32, argmax int32, sum float64) arrays of a gm_row_stats tensor."""
+    h = t.detach().cpu().contiguous()
+    return (h[..., 0:4].contiguous().view(torch.float32)[..., 0].numpy(),
+            h[..., 4:8].contiguous().view(torch.int32)[..., 0].numpy(),
+            h[..., 8:16].contiguous().view(torch.float64)[..., 0].numpy())
+
+
 def spec_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], draft_tokens: torch.Tensor,
                 u_accept: Optional[torch.Tensor], u_final: Optional[torch.Tensor], n_accept: torch.Tensor,
-                out_tokens: torch.Tensor, mode: int, ws: Workspace, temperature: float = 1.0, stream=None):
+                out_tokens: torch.Tensor, mode: int, ws: Workspace, temperature: float = 1.0, stream=None,
+                draft_stats: Optional[torch.Tensor] = None):
     B, k1, V = target_logits.shape
     k = k1 - 1
     _need(target_logits, torch.float32, (B, k1, V), "target_logits")
@@ -334,12 +351,14 @@ def spec_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor
     _need(draft_tokens, torch.int32, (B, k), "draft_tokens")
     _need(n_accept, torch.int32, (B,), "n_accept")
     _need(out_tokens, torch.int32, (B, k1), "out_tokens")
+    if draft_stats is not None:
+        _need(draft_stats, torch.uint8, (B, k, ROW_STATS_BYTES), "draft_stats")
     cfg = ModelConfig()
     cfg.vocab = V
     n = workspace_size(GM_OP_SPEC_ACCEPT, cfg, B, k, 0)
     buf = ws.get(n)
     _check(lib().gm_spec_accept(B, k, V, mode, float(temperature), _ptr(target_logits), _ptr(draft_logits),
-                                _ptr(draft_tokens), _ptr(u_accept), _ptr(u_final), _ptr(n_accept), _ptr(out_tokens),
+                                _ptr(draft_stats), _ptr(draft_tokens), _ptr(u_accept), _ptr(u_final), _ptr(n_accept), _ptr(out_tokens),
                                 _ptr(buf), buf.numel(), _stream(stream)))
 
 
@@ -352,18 +371,22 @@ def kv_commit(cache: PagedCache, k: int, n_accept: torch.Tensor, committed_slots
 def mtp_draft(model: DeviceModel, mtp: DeviceMtp, mtp_cache: PagedCache, k: int, mode: int,
               verify_hidden: torch.Tensor, n_accept: torch.Tensor, out_tokens: torch.Tensor,
               u_draft: Optional[torch.Tensor], drafts: torch.Tensor, draft_logits: torch.Tensor, ws: Workspace,
-              temperature: float = 1.0, dev_err: Optional[torch.Tensor] = None, stream=None):
+              temperature: float = 1.0, dev_err: Optional[torch.Tensor] = None, stream=None,
+              draft_stats: Optional[torch.Tensor] = None):
     B = mtp_cache.B
     s = model.shape
     _need(verify_hidden, torch.float32, (B, k + 1, s.hidden), "verify_hidden")
     _need(drafts, torch.int32, (B, k), "drafts")
     _need(draft_logits, torch.float32, (B, k, s.vocab), "draft_logits")
+    if draft_stats is not None:
+        _need(draft_stats, torch.uint8, (B, k, ROW_STATS_BYTES), "draft_stats")
     cs = mtp_cache.struct()
     n = workspace_size(GM_OP_MTP_DRAFT, model.cfg, B, k, mtp_cache.max_ctx)
     buf = ws.get(n)
     _check(lib().gm_mtp_draft(ctypes.byref(model.cfg), ctypes.byref(mtp.struct), ctypes.byref(model.struct),
                               ctypes.byref(cs), B, k, mode, float(temperature), _ptr(verify_hidden), _ptr(n_accept),
-                              _ptr(out_tokens), _ptr(u_draft), _ptr(drafts), _ptr(draft_logits), _ptr(buf),
+                              _ptr(out_tokens), _ptr(u_draft), _ptr(drafts), _ptr(draft_logits), _ptr(draft_stats),
+                              _ptr(buf),
                               buf.numel(), _ptr(dev_err), _stream(stream)))
 
 

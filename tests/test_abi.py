@@ -55,7 +55,7 @@ def test_spec_accept_rejects_bad_arguments():
                                   uf=FAKE, n=FAKE, out=FAKE, ws=ws, nbytes=1 << 30), **kw)
 
     def call(a):
-        return L.gm_spec_accept(a["B"], a["k"], a["V"], a["mode"], a["T"], a["tl"], a["dl"], a["dt"], a["ua"],
+        return L.gm_spec_accept(a["B"], a["k"], a["V"], a["mode"], a["T"], a["tl"], a["dl"], None, a["dt"], a["ua"],
                                 a["uf"], a["n"], a["out"], a["ws"], a["nbytes"], None)
 
     assert call(args(k=16)) == gm.GM_ERR_INVALID_ARG
@@ -114,11 +114,11 @@ def test_mtp_and_attention_reject_bad_arguments():
     mtp = gm.MtpWeights(FAKE, FAKE, FAKE, FAKE, gm.LayerWeights(*([FAKE] * 8)))
     c = _FakeCache(1, 100)
     st = L.gm_mtp_draft(ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(c.desc), 4, 3,
-                        gm.GM_SAMPLE, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, 1 << 30, None, None)
+                        gm.GM_SAMPLE, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, None, FAKE, 1 << 30, None, None)
     assert st == gm.GM_ERR_INVALID_ARG and "u_draft" in gm.last_error()
     c2 = _FakeCache(1, 150)                                         # 150 + 2k + 1 > 160
     st = L.gm_mtp_draft(ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(c2.desc), 4, 5,
-                        gm.GM_GREEDY, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, 1 << 30, None, None)
+                        gm.GM_GREEDY, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, None, FAKE, 1 << 30, None, None)
     assert st == gm.GM_ERR_CAPACITY
     st = L.gm_verify_attention(ctypes.byref(cfg), ctypes.byref(c.desc), 1, 4, 3, FAKE, FAKE, FAKE, 1 << 30, None, None)
     assert st == gm.GM_ERR_INVALID_ARG                              # layer out of range

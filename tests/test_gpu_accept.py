@@ -25,14 +25,26 @@ def _sampled_drafts(zq, u_draft):
     return d
 
 
-def _run(zt, zq, drafts, ua, uf, mode):
+def _host_row_stats(z, temperature=1.0):
+    """gm_row_stats of each row of z by their definition: max of z / T (float32
+    product), the lowest id attaining it, sum of exp(z / T - max) in float64."""
+    v = z.astype(np.float32) * np.float32(1.0 / temperature)
+    st = np.zeros(z.shape[:-1], dtype=[("max", "<f4"), ("argmax", "<i4"), ("sum", "<f8")])
+    st["max"] = v.max(-1)
+    st["argmax"] = v.argmax(-1)
+    st["sum"] = np.exp(v.astype(np.float64) - st["max"][..., None].astype(np.float64)).sum(-1)
+    return torch.from_numpy(st.view(np.uint8).reshape(z.shape[:-1] + (16,)).copy()).cuda()
+
+
+def _run(zt, zq, drafts, ua, uf, mode, draft_stats=None):
     B, k1, V = zt.shape
     k = k1 - 1
     n = torch.zeros(B, dtype=torch.int32, device="cuda")
     out = torch.zeros((B, k1), dtype=torch.int32, device="cuda")
     ws = gm.Workspace()
     gm.spec_accept(t32(zt), t32(zq) if zq is not None else None, i32(drafts),
-                   t32(ua) if ua is not None else None, t32(uf) if uf is not None else None, n, out, mode, ws)
+                   t32(ua) if ua is not None else None, t32(uf) if uf is not None else None, n, out, mode, ws,
+                   draft_stats=draft_stats)
     torch.cuda.synchronize()
     return n.cpu().numpy(), out.cpu().numpy()
 
@@ -59,6 +71,23 @@ def test_sample_accept_matches_oracle(B, k, V):
     n, out = _run(zt, zq, drafts, ua, uf, gm.GM_SAMPLE)
     _compare("sample B=%d k=%d V=%d" % (B, k, V), ref, n, out)
     assert ref.flagged.mean() < 0.05
+
+
+@pytest.mark.parametrize("B,k,V", [(64, 3, 151936), (33, 2, 1000)])
+def test_sample_accept_with_draft_stats(B, k, V):
+    # q's normaliser taken from given row statistics (as the draft head emits them)
+    # instead of a pass over the draft rows: same decisions as the oracle
+    need_gpu()
+    zt = synth.normal_logits((B, k + 1, V), 3, "ts", B, k, V)
+    zq = synth.normal_logits((B, k, V), 3, "qs", B, k, V)
+    ua, uf, ud = synth.uniforms(B, k, 4, "s", B, k, V)
+    drafts = _sampled_drafts(zq, ud)
+    ref = oracle.spec_accept(zt, zq, drafts, ua, uf, final_eps=FINAL_EPS)
+    n, out = _run(zt, zq, drafts, ua, uf, gm.GM_SAMPLE, draft_stats=_host_row_stats(zq))
+    _compare("sample with draft stats B=%d k=%d V=%d" % (B, k, V), ref, n, out)
+    n2, out2 = _run(zt, zq, drafts, ua, uf, gm.GM_SAMPLE)
+    np.testing.assert_array_equal(n, n2)
+    np.testing.assert_array_equal(out, out2)
 
 
 @pytest.mark.parametrize("B,k,V", [(64, 3, 151936), (16, 5, 1024)])

@@ -146,12 +146,20 @@ def test_qwen_layer_bf16_mtp_sample_draw_from_own_logits(qwen_mtp, temperature):
     cache = device_cache(shape, caches, lens, 2 * k + 2)
     drafts = torch.zeros((B, k), dtype=torch.int32, device="cuda")
     dlog = torch.zeros((B, k, shape.vocab), dtype=torch.float32, device="cuda")
+    stats = gm.new_row_stats(B, k)
     gm.mtp_draft(model, mtp, cache, k, gm.GM_SAMPLE, t32(hidden), i32(n), i32(out), t32(u), drafts, dlog,
-                 gm.Workspace(), temperature=temperature)
+                 gm.Workspace(), temperature=temperature, draft_stats=stats)
     torch.cuda.synchronize()
     z = dlog.cpu().numpy()
     got = drafts.cpu().numpy()
     inv_t = float(np.float32(1.0 / temperature))
+    # the row statistics handed to the accept: max of z / T, lowest arg-max, and the normaliser
+    smax, sarg, ssum = gm.decode_row_stats(stats)
+    v = z * np.float32(inv_t)
+    np.testing.assert_array_equal(smax, v.max(-1))
+    np.testing.assert_array_equal(sarg, v.argmax(-1))
+    ref_sum = np.exp(v.astype(np.float64) - v.max(-1, keepdims=True).astype(np.float64)).sum(-1)
+    assert np.abs(ssum / ref_sum - 1).max() < 1e-6
     exact, in_tail = 0, 0
     strips = shape.vocab // 16
     first = (np.arange(1025) * strips) // 1024   # first strip of each range when the chip holds 1024 waves

@@ -82,12 +82,16 @@ typedef struct {
 
 /* One decoder layer.  A linear weight W[out][in] (y = W x) is stored
  *  - GM_F32: row-major;
- *  - GM_BF16: tiled, in tiles of 16 rows x 32 columns: element (n, c) at
- *      ((n / 16) * (in / 32) + c / 32) * 512 + ((c % 32) / 8) * 128 + (n % 16) * 8 + c % 8,
- *    so that a 16-row strip of W is a run of 1 KiB tiles along `in`, each
- *    read by one 16-byte-per-lane load of a 64-lane wave in the operand order
- *    of the matrix cores.  (Row-major W converts to this layout by viewing it
- *    as [out/16][16][in/32][4][8] and permuting to [out/16][in/32][4][16][8].)
+ *  - GM_BF16: tiled, in tiles of 16 rows x 32 columns (out a multiple of 128):
+ *    element (n, c) at
+ *      (((n / 128) * (in / 32) + c / 32) * 8 + (n / 16) % 8) * 512
+ *        + ((c % 32) / 8) * 128 + (n % 16) * 8 + c % 8,
+ *    so that each 1 KiB tile is read by one 16-byte-per-lane load of a
+ *    64-lane wave in the operand order of the matrix cores, and the tiles of
+ *    8 consecutive 16-row strips at one 32-column step are consecutive (the
+ *    strips streamed together are one contiguous run per step).  (Row-major W
+ *    converts to this layout by viewing it as [out/128][8][16][in/32][4][8]
+ *    and permuting to [out/128][in/32][8][4][16][8].)
  * The tiled layout applies to w_qkv, w_o, w_gate_up, w_down, the MTP w_proj
  * and lm_head; embeddings and norm weights are plain vectors / row-major. */
 typedef struct {

@@ -117,6 +117,18 @@ __device__ __forceinline__ float4 sum_splits(const float *p, long stride, int sp
   return a;
 }
 
+// ----------------------------------------------------------------- weight tile layout
+// bf16 linear weights (gm.h): 1 KiB tiles of 16 rows (a strip) x 32 columns (a
+// k-step); the strips come in groups of 8, and inside a group the 8 tiles of
+// one k-step are consecutive, so the strips a wave or workgroup streams
+// together sit in one contiguous run per k-step.
+constexpr int kWGroup = 8;                      // strips per group
+constexpr int kWStep = kWGroup * 512;           // elements from k-step kt to kt + 1 of a strip
+// element offset of the tile (strip s, k-step kt) of a weight with `ksteps` k-steps
+__device__ __forceinline__ long w_tile(int s, int kt, int ksteps) {
+  return (((long)(s / kWGroup) * ksteps + kt) * kWGroup + s % kWGroup) * 512;
+}
+
 // ----------------------------------------------------------------- KV tile layout
 // Offsets inside the 16-token tile of one (page, kv head); see gm.h.
 __device__ __forceinline__ int k_tile_off(int s, int c) {

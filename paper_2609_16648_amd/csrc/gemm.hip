@@ -4,9 +4,10 @@
 // verify step: every weight byte is read once and used for all M rows).
 //  * Weights are stored pre-tiled (gm.h): tiles of 16 rows x 32 k (1 KiB)
 //    laid out so that one 16-byte-per-lane load of a wave is the B operand of
-//    v_mfma_f32_16x16x32_bf16.  A wave streams its strips of 16 rows along K
-//    as consecutive 1 KiB tiles, straight from HBM into registers, through a
-//    prefetch ring several k-steps deep; W never touches LDS.
+//    v_mfma_f32_16x16x32_bf16, with the tiles of 8 strips (16-row groups) of
+//    one k-step side by side.  A wave streams its strips along K, straight
+//    from HBM into registers, through a prefetch ring several k-steps deep;
+//    W never touches LDS.
 //  * Activations (small, L2-resident) are staged in LDS in 16 or 32 KiB
 //    chunks, three deep, by a fifth wave of direct-to-LDS loads, one barrier
 //    per chunk, shared by the 4 compute waves.
@@ -160,7 +161,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
     const int kt_total = g.K / 32;
     const uint16_t *wbase[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) wbase[t] = g.W + ((long)strip[t] * kt_total + k_begin / 32) * 512 + lane * 8;
+    for (int t = 0; t < NT; ++t) wbase[t] = g.W + w_tile(strip[t], k_begin / 32, kt_total) + lane * 8;
     // Slot d of the ring holds step d mod D.  Each step first refills the slot
     // consumed by the step before (its registers are dead), then consumes its
     // own: a load never targets a register still waiting for its reader, so the
@@ -170,7 +171,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
     for (int s = 0; s < D - 1; ++s) {
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int t = 0; t < NT; ++t) ring[s][t] = load_w<SW>(wbase[t] + (long)min(s, nsteps - 1) * 512);
+      for (int t = 0; t < NT; ++t) ring[s][t] = load_w<SW>(wbase[t] + (long)min(s, nsteps - 1) * kWStep);
     }
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();     // barrier 0
@@ -184,7 +185,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int t = 0; t < NT; ++t)
-          ring[(u + D - 1) % D][t] = load_w<SW>(wbase[t] + (long)min(s + D - 1, nsteps - 1) * 512);
+          ring[(u + D - 1) % D][t] = load_w<SW>(wbase[t] + (long)min(s + D - 1, nsteps - 1) * kWStep);
         __builtin_amdgcn_sched_barrier(0);
         const uint4 (&wv)[NT] = ring[u % D];
         bf16x8_t af[MT];
@@ -449,7 +450,7 @@ __global__ __launch_bounds__(256) void lm_strips_kernel(GemmL g) {
   const int ksteps = g.K / 32;   // a multiple of kLmRing
   const uint16_t *wb[kLmStrips];
 #pragma unroll
-  for (int t = 0; t < kLmStrips; ++t) wb[t] = g.W + (long)(s0 + min(t, n - 1)) * ksteps * 512 + lane * 8;
+  for (int t = 0; t < kLmStrips; ++t) wb[t] = g.W + w_tile(s0 + min(t, n - 1), 0, ksteps) + lane * 8;
   const uint16_t *ab[4];   // A fragment of row tile a: row 16 a + j (rows past M re-read row M - 1), k 8 g4 ..
 #pragma unroll
   for (int a = 0; a < 4; ++a) ab[a] = g.X + (long)min(16 * a + j, g.M - 1) * g.ldx + 8 * g4;
@@ -463,7 +464,7 @@ __global__ __launch_bounds__(256) void lm_strips_kernel(GemmL g) {
   uint4 ra[kLmRing][4], rw[kLmRing][kLmStrips];
   auto load = [&](int slot, int step) {
 #pragma unroll
-    for (int t = 0; t < kLmStrips; ++t) rw[slot][t] = load_w<true>(wb[t] + (long)step * 512);
+    for (int t = 0; t < kLmStrips; ++t) rw[slot][t] = load_w<true>(wb[t] + (long)step * kWStep);
 #pragma unroll
     for (int a = 0; a < 4; ++a) ra[slot][a] = *reinterpret_cast<const uint4 *>(ab[a] + step * 32);
   };

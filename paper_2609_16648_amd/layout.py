@@ -65,14 +65,16 @@ def block_table(pages_needed, max_pages: int, seed: int = 0):
 
 
 def tile_weight(w: np.ndarray) -> np.ndarray:
-    """Row-major W [out, in] -> the tiled bf16 weight layout of gm.h (tiles of
-    16 rows x 32 columns, element (n, c) of a tile at ((c % 32) // 8) * 128 +
-    (n % 16) * 8 + c % 8).  Returns a flat array."""
+    """Row-major W [out, in] -> the tiled bf16 weight layout of gm.h: tiles of
+    16 rows x 32 columns (element (n, c) of a tile at ((c % 32) // 8) * 128 +
+    (n % 16) * 8 + c % 8), the tile of strip s = n // 16 and k-step c // 32 at
+    ((s // 8) * (in / 32) + c // 32) * 8 + s % 8.  Returns a flat array."""
     n, k = w.shape
-    if n % 16 or k % 32:
-        raise ValueError("tiled weights need out % 16 == 0 and in % 32 == 0, got %s" % (w.shape,))
-    return np.ascontiguousarray(w.reshape(n // 16, 16, k // 32, 4, 8).transpose(0, 2, 3, 1, 4)).reshape(-1)
+    if n % 128 or k % 32:
+        raise ValueError("tiled weights need out % 128 == 0 and in % 32 == 0, got %s" % (w.shape,))
+    # [group][strip in group][row][kstep][col block][col] -> [group][kstep][strip][col block][row][col]
+    return np.ascontiguousarray(w.reshape(n // 128, 8, 16, k // 32, 4, 8).transpose(0, 3, 1, 4, 2, 5)).reshape(-1)
 
 
 def untile_weight(flat: np.ndarray, n: int, k: int) -> np.ndarray:
-    return np.ascontiguousarray(flat.reshape(n // 16, k // 32, 4, 16, 8).transpose(0, 3, 1, 2, 4)).reshape(n, k)
+    return np.ascontiguousarray(flat.reshape(n // 128, k // 32, 8, 4, 16, 8).transpose(0, 2, 4, 1, 3, 5)).reshape(n, k)

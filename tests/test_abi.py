@@ -166,11 +166,11 @@ def test_scatter_gather_round_trip():
 
 def test_weight_tiling_matches_header_formula():
     g = np.random.default_rng(1)
-    n, k = 48, 96
+    n, k = 256, 96
     w = g.standard_normal((n, k)).astype(np.float32)
     flat = layout.tile_weight(w)
     r, c = np.meshgrid(np.arange(n), np.arange(k), indexing="ij")
-    off = ((r // 16) * (k // 32) + c // 32) * 512 + ((c % 32) // 8) * 128 + (r % 16) * 8 + c % 8
+    off = (((r // 128) * (k // 32) + c // 32) * 8 + (r // 16) % 8) * 512 + ((c % 32) // 8) * 128 + (r % 16) * 8 + c % 8
     np.testing.assert_array_equal(flat[off], w)
     np.testing.assert_array_equal(layout.untile_weight(flat, n, k), w)
     # one 16-byte load per lane at lane * 8 of a tile: row lane % 16, columns 8 (lane // 16) .. +7

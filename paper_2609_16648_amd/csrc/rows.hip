@@ -137,13 +137,18 @@ __global__ __launch_bounds__(1024) void mtp_input_kernel(int H, int V, float eps
   }
 }
 
-// one block per row; wave w handles heads w, w+4, ...; lane c < d/2 handles the pair (c, c + d/2)
+// One wave per (row, head): block (row, y) holds heads 4 y .. 4 y + 3, and lane
+// c < d/2 handles the pair (c, c + d/2).  Each wave reads its head's columns
+// straight from the projection (or sums its K-split partials, in split order),
+// so a row's heads run on as many waves as it has heads.
 template <typename T>
 __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
   const int row = blockIdx.x, b = row / a.R, i = row % a.R;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
   const int D = a.head_dim, half = D / 2;
   const int nh = a.n_heads + 2 * a.n_kv;
+  const int hh = blockIdx.y * 4 + (threadIdx.x >> 6);
+  if (hh >= nh) return;
   int blen = a.R;
   if (a.blk_len) {
     blen = a.blk_len[b] + a.blk_len_add;
@@ -151,74 +156,78 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
   }
   const int slot = a.base_lens[b] + a.base_off + i;
   const double pos = (double)(slot + a.pos_off);
-  const bool write_kv = i < blen;
-  long kv_base = -1;
-  int s_in = 0;
-  if (write_kv) {
-    const int pi = slot / a.page_size;
-    const int page = pi < a.max_pages ? a.block_table[(long)b * a.max_pages + pi] : -1;
-    if (page < 0 || page >= a.num_pages) {
-      if (threadIdx.x == 0) raise_dev_err(a.dev_err, GM_DEVERR_PAGE);
+  const int kind = hh < a.n_heads ? 0 : (hh < a.n_heads + a.n_kv ? 1 : 2);
+  const bool act = lane < half;
+  // the pair's two columns (all loads of the splits issued before the sums)
+  float x1 = 0.f, x2 = 0.f;
+  if (act) {
+    const long W = (long)nh * D, off = (long)row * W + (long)hh * D + lane;
+    if (a.splits > 1) {
+      const long stride = (long)a.M * W;
+      for (int s0 = 0; s0 < a.splits; s0 += 8) {
+        float v1[8], v2[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const long sp = s0 + u < a.splits ? s0 + u : a.splits - 1;
+          v1[u] = a.part[sp * stride + off];
+          v2[u] = a.part[sp * stride + off + half];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (s0 + u < a.splits) {
+            x1 += v1[u];
+            x2 += v2[u];
+          }
+        }
+      }
     } else {
-      const int off = slot % a.page_size;
-      kv_base = (((long)page * a.n_kv) * a.page_size + (off & ~15)) * D;   // + head * page_size * D
-      s_in = off & 15;
+      x1 = a.qkv[off];
+      x2 = a.qkv[off + half];
     }
   }
-  // the projected row staged in LDS: qkv itself, or the sum of the GEMM's K-split
-  // partials (split order), read as float4 column groups by the whole block
-  extern __shared__ float row_sh[];   // [nh * D]
-  {
-    const int W = nh * D;
-    const long row_off = (long)row * W;
-    for (int c = threadIdx.x * 4; c < W; c += blockDim.x * 4) {
-      const float4 v = a.splits > 1 ? sum_splits(a.part + row_off + c, (long)a.M * W, a.splits)
-                                    : *reinterpret_cast<const float4 *>(a.qkv + row_off + c);
-      *reinterpret_cast<float4 *>(row_sh + c) = v;
-    }
-  }
-  __syncthreads();
-  auto ld = [&](int col) -> float { return row_sh[col]; };
-  const T *qn = (const T *)a.q_norm, *kn = (const T *)a.k_norm;
-  // the rotation of pair `lane` at this position, shared by every head of the row
+  // the rotation of pair `lane` at this position
   double sn = 0.0, cs = 1.0;
-  if (lane < half) sincos(pos * pow((double)a.rope_base, -2.0 * lane / D), &sn, &cs);
-  for (int hh = w; hh < nh; hh += 4) {
-    const int kind = hh < a.n_heads ? 0 : (hh < a.n_heads + a.n_kv ? 1 : 2);
-    const bool act = lane < half;
-    float x1 = act ? ld(hh * D + lane) : 0.f, x2 = act ? ld(hh * D + lane + half) : 0.f;
-    if (kind < 2 && qn) {
-      const T *nw = kind == 0 ? qn : kn;
-      const float ss = wave_sum(x1 * x1 + x2 * x2);
-      const float inv = 1.0f / sqrtf(ss / (float)D + a.eps);
-      if (act) {
-        x1 = x1 * inv * Elem<T>::load(nw, lane);
-        x2 = x2 * inv * Elem<T>::load(nw, lane + half);
-      }
+  if (kind < 2 && act) sincos(pos * pow((double)a.rope_base, -2.0 * lane / D), &sn, &cs);
+  const T *qn = (const T *)a.q_norm, *kn = (const T *)a.k_norm;
+  if (kind < 2 && qn) {
+    const T *nw = kind == 0 ? qn : kn;
+    const float ss = wave_sum(x1 * x1 + x2 * x2);
+    const float inv = 1.0f / sqrtf(ss / (float)D + a.eps);
+    if (act) {
+      x1 = x1 * inv * Elem<T>::load(nw, lane);
+      x2 = x2 * inv * Elem<T>::load(nw, lane + half);
     }
-    if (!act) continue;
-    float y1 = x1, y2 = x2;
-    if (kind < 2) {
-      y1 = (float)((double)x1 * cs - (double)x2 * sn);
-      y2 = (float)((double)x2 * cs + (double)x1 * sn);
-    }
-    if (kind == 0) {
-      T *q = (T *)a.q_out + ((long)row * a.n_heads + hh) * D;
-      Elem<T>::store(q, lane, y1);
-      Elem<T>::store(q, lane + half, y2);
-    } else if (kv_base >= 0) {
-      const int head = kind == 1 ? hh - a.n_heads : hh - a.n_heads - a.n_kv;
-      const long base = kv_base + (long)head * a.page_size * D;
-      if (kind == 1) {
-        T *kp = (T *)a.k_pages + base;
-        Elem<T>::store(kp, k_tile_off(s_in, lane), y1);
-        Elem<T>::store(kp, k_tile_off(s_in, lane + half), y2);
-      } else {
-        T *vp = (T *)a.v_pages + base;
-        Elem<T>::store(vp, v_tile_off(s_in, lane), y1);
-        Elem<T>::store(vp, v_tile_off(s_in, lane + half), y2);
-      }
-    }
+  }
+  if (!act) return;
+  float y1 = x1, y2 = x2;
+  if (kind < 2) {
+    y1 = (float)((double)x1 * cs - (double)x2 * sn);
+    y2 = (float)((double)x2 * cs + (double)x1 * sn);
+  }
+  if (kind == 0) {
+    T *q = (T *)a.q_out + ((long)row * a.n_heads + hh) * D;
+    Elem<T>::store(q, lane, y1);
+    Elem<T>::store(q, lane + half, y2);
+    return;
+  }
+  if (i >= blen) return;   // rows past the block's valid length append nothing
+  const int pi = slot / a.page_size;
+  const int page = pi < a.max_pages ? a.block_table[(long)b * a.max_pages + pi] : -1;
+  if (page < 0 || page >= a.num_pages) {
+    if (lane == 0) raise_dev_err(a.dev_err, GM_DEVERR_PAGE);
+    return;
+  }
+  const int off = slot % a.page_size, s_in = off & 15;
+  const int head = kind == 1 ? hh - a.n_heads : hh - a.n_heads - a.n_kv;
+  const long base = ((((long)page * a.n_kv) * a.page_size + (off & ~15)) * D) + (long)head * a.page_size * D;
+  if (kind == 1) {
+    T *kp = (T *)a.k_pages + base;
+    Elem<T>::store(kp, k_tile_off(s_in, lane), y1);
+    Elem<T>::store(kp, k_tile_off(s_in, lane + half), y2);
+  } else {
+    T *vp = (T *)a.v_pages + base;
+    Elem<T>::store(vp, v_tile_off(s_in, lane), y1);
+    Elem<T>::store(vp, v_tile_off(s_in, lane + half), y2);
   }
 }
 
@@ -268,9 +277,9 @@ void launch_rmsnorm(int dtype, int M, int H, float eps, const float *x, const vo
 void launch_rope_append(const RopeArgs &a, hipStream_t s) {
   if (a.M <= 0) return;
   TraceScope ts("rope_append", s);
-  const size_t lds = (size_t)(a.n_heads + 2 * a.n_kv) * a.head_dim * sizeof(float);
-  if (a.dtype == GM_BF16) hipLaunchKernelGGL(rope_append_kernel<bf16>, dim3(a.M), dim3(256), lds, s, a);
-  else hipLaunchKernelGGL(rope_append_kernel<float>, dim3(a.M), dim3(256), lds, s, a);
+  const dim3 grid(a.M, (a.n_heads + 2 * a.n_kv + 3) / 4);
+  if (a.dtype == GM_BF16) hipLaunchKernelGGL(rope_append_kernel<bf16>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(rope_append_kernel<float>, grid, dim3(256), 0, s, a);
 }
 
 void launch_mtp_input(int dtype, int M, int H, int V, float eps, const float *h, const int32_t *tok, int tok_stride,

@@ -93,10 +93,10 @@ __device__ __forceinline__ F block_sum(F v, F *smem /* >= 16 */) {
 
 // Sum, in split order, of `splits` float4 values stride floats apart (K-split
 // partials of one output element group); the loads of a batch are all issued
-// before the first add.
-__device__ __forceinline__ float4 sum_splits(const float *p, long stride, int splits) {
-  constexpr int kBatch = 8;
-  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+// before the first add (batches of 16 when there are more than 8 splits, so
+// that up to 16 take one round trip).
+template <int kBatch>
+__device__ __forceinline__ void sum_splits_batched(const float *p, long stride, int splits, float4 &a) {
   for (int s0 = 0; s0 < splits; s0 += kBatch) {
     float4 v[kBatch];
 #pragma unroll
@@ -114,6 +114,11 @@ __device__ __forceinline__ float4 sum_splits(const float *p, long stride, int sp
       }
     }
   }
+}
+__device__ __forceinline__ float4 sum_splits(const float *p, long stride, int splits) {
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (splits > 8) sum_splits_batched<16>(p, stride, splits, a);
+  else sum_splits_batched<8>(p, stride, splits, a);
   return a;
 }
 

@@ -245,13 +245,29 @@ __device__ __forceinline__ void run_weights(const RowSel &s, int x0, int V, floa
   }
 }
 
-// per-thread sums over kScanPer consecutive ids, then a serial sum over the
-// threads in ascending order (thread 0), so both kernels associate identically
+// Inclusive prefix sum of one double per thread over the block (256 threads).
+__device__ __forceinline__ double block_incl_scan(double v, double *wsum /* >= 4 */) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double n = __shfl_up(v, o, kWave);
+    if (lane >= o) v += n;
+  }
+  if (lane == 63) wsum[wid] = v;
+  __syncthreads();
+  double off = 0.0;
+  for (int w = 0; w < wid; ++w) off += wsum[w];
+  return off + v;
+}
+
+// per-thread sums over kScanPer consecutive ids, then a block-wide inclusive scan
+// over the threads (the same code in both kernels, so a chunk's mass is exactly
+// the last running sum of the scan inside it)
 __global__ __launch_bounds__(kScanThreads) void residual_chunk_kernel(int V, float inv_t,
                                                                       const RowSel *__restrict__ sel,
                                                                       int nch, double *__restrict__ wsum,
                                                                       double *__restrict__ psum) {
-  __shared__ double sw[kScanThreads], sp[kScanThreads];
+  __shared__ double sw[kScanThreads / kWave], sp[kScanThreads / kWave];
   const int b = blockIdx.x, c = blockIdx.y, tid = threadIdx.x;
   const RowSel s = sel[b];
   if (!s.active) return;
@@ -262,12 +278,9 @@ __global__ __launch_bounds__(kScanThreads) void residual_chunk_kernel(int V, flo
   double w = 0.0;
 #pragma unroll
   for (int j = 0; j < kScanPer; ++j) w += wv[j];
-  sw[tid] = w;
-  sp[tid] = p;
-  __syncthreads();
-  if (tid == 0) {
-    double tw = 0.0, tp = 0.0;
-    for (int i = 0; i < kScanThreads; ++i) { tw += sw[i]; tp += sp[i]; }
+  const double tw = block_incl_scan(w, sw);
+  const double tp = block_incl_scan(p, sp);
+  if (tid == kScanThreads - 1) {
     wsum[(long)b * nch + c] = tw;
     psum[(long)b * nch + c] = tp;
   }
@@ -278,9 +291,9 @@ __global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, floa
                                                                      const double *__restrict__ wsum,
                                                                      const double *__restrict__ psum) {
   extern __shared__ double chunk_sh[];   // [2 nch]: residual masses, then p masses
-  __shared__ double st[kScanThreads];
+  __shared__ double st[kScanThreads / kWave];
   __shared__ double sh_t, sh_base;
-  __shared__ int sh_chunk, sh_thread, sh_use_p, sh_found;
+  __shared__ int sh_chunk, sh_thread, sh_last, sh_use_p;
   const int b = blockIdx.x, tid = threadIdx.x;
   const RowSel s = sel[b];
   if (!s.active) return;
@@ -318,6 +331,8 @@ __global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, floa
     sh_base = run;
     sh_chunk = cs;
     sh_use_p = use_p;
+    sh_thread = kScanThreads;
+    sh_last = -1;
   }
   __syncthreads();
   const int cs = sh_chunk;
@@ -329,24 +344,20 @@ __global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, floa
   double w = 0.0;
 #pragma unroll
   for (int j = 0; j < kScanPer; ++j) w += wv[j];
-  st[tid] = w;
-  __syncthreads();
-  if (tid == 0) {
-    double acc = sh_base;
-    int th = -1, last_nz = -1;
-    for (int i = 0; i < kScanThreads; ++i) {
-      if (st[i] > 0.0) last_nz = i;
-      if (th < 0 && acc + st[i] > sh_t) th = i;
-      if (th < 0) acc += st[i];
-    }
-    sh_found = th >= 0;
-    if (th < 0) th = last_nz < 0 ? 0 : last_nz;
-    sh_thread = th;
-    sh_base = acc;
+  const double incl = block_incl_scan(w, st);
+  // the running sum before this thread's run: the previous thread's inclusive sum
+  double excl = __shfl_up(incl, 1, kWave);
+  if ((tid & 63) == 0) {   // the waves before this one, summed as the scan sums them
+    excl = 0.0;
+    for (int q = 0; q < (tid >> 6); ++q) excl += st[q];
   }
+  if (sh_base + incl > sh_t) atomicMin(&sh_thread, tid);   // first run whose sum passes u * Z
+  if (w > 0.0) atomicMax(&sh_last, tid);                  // last run with mass (rounding fallback)
   __syncthreads();
-  if (tid == sh_thread) {
-    double acc = sh_base;
+  const bool found = sh_thread < kScanThreads;
+  const int th = found ? sh_thread : (sh_last >= 0 ? sh_last : 0);
+  if (tid == th) {
+    double acc = sh_base + excl;
     int x_last = -1, x_hit = -1;
 #pragma unroll
     for (int j = 0; j < kScanPer; ++j) {
@@ -354,7 +365,7 @@ __global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, floa
       if (x < V) {
         if (wv[j] > 0.0) x_last = x;
         acc += wv[j];
-        if (sh_found && x_hit < 0 && acc > sh_t) x_hit = x;
+        if (found && x_hit < 0 && acc > sh_t) x_hit = x;
       }
     }
     *s.dst = x_hit >= 0 ? x_hit : (x_last >= 0 ? x_last : (x0 < V ? x0 : V - 1));
@@ -448,21 +459,6 @@ void launch_tile_stats(const float *logits, long row_stride, int n_rows, int V, 
   TraceScope ts("draft_tile_stats", s);
   hipLaunchKernelGGL(tile_stats_kernel, dim3(n_rows, (geo.tiles + 3) / 4), dim3(256), 0, s, logits, row_stride, V,
                      inv_t, geo, tiles);
-}
-
-// Inclusive prefix sum of one double per thread over the block (256 threads).
-__device__ __forceinline__ double block_incl_scan(double v, double *wsum /* >= 4 */) {
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const double n = __shfl_up(v, o, kWave);
-    if (lane >= o) v += n;
-  }
-  if (lane == 63) wsum[wid] = v;
-  __syncthreads();
-  double off = 0.0;
-  for (int w = 0; w < wid; ++w) off += wsum[w];
-  return off + v;
 }
 
 // One block per row.  The row's max and arg-max come from its tile statistics

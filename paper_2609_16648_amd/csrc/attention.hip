@@ -140,9 +140,13 @@ __device__ __forceinline__ void attn_tile(int tb, int L, int g, float scale_log2
   tmax = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
   tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
   tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
-  if (__any(tmax > m + kLazyLog2)) {   // m = -inf and a finite score also lands here
-    const float mn = fmaxf(m, tmax);
-    const float alpha = mn == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m - mn);
+  // Each row decides for itself (m = -inf and a finite score also count as growth);
+  // rows that did not grow keep alpha = 1 exactly, so a row's result never depends
+  // on the other rows of the tile.  The branch only skips tiles where no row grew.
+  const bool up = tmax > m + kLazyLog2;
+  if (__any(up)) {
+    const float mn = up ? fmaxf(m, tmax) : m;
+    const float alpha = (!up || mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m - mn);
     l *= alpha;
 #pragma unroll
     for (int mm = 0; mm < 8; ++mm) O[mm] *= alpha;

@@ -129,3 +129,20 @@ def test_qwen_layer_bf16_forward_mid_batch(qwen_layer):
     print("[forward qwen3 layer bf16 B=24] logits rel err vs contract %.3e, hidden %.3e"
           % (rel_err(logits, ref_c), rel_err(hidden, ref_hc)), flush=True)
     assert rel_err(logits, ref_c) < 1e-2 and rel_err(hidden, ref_hc) < 1e-2
+
+
+def test_qwen_layer_bf16_block_is_causal(qwen_layer):
+    # Changing the last draft d_k leaves every earlier block row's logits and hidden
+    # bit-identical (a block position sees only the positions before it, Sec. 3.1's
+    # one-forward verification; outputs are deterministic), and does change row k
+    need_gpu()
+    wl, shape, W, lens, caches, tokens = qwen_layer
+    k = wl.k
+    model = gm.DeviceModel(shape, W)
+    alt = tokens.copy()
+    alt[:, k] = (alt[:, k] + 1 + np.arange(len(alt)) * 7919) % shape.vocab
+    l0, h0 = _gpu_forward(model, device_cache(shape, caches, lens, k + 1), tokens)
+    l1, h1 = _gpu_forward(model, device_cache(shape, caches, lens, k + 1), alt)
+    np.testing.assert_array_equal(l0[:, :k], l1[:, :k])
+    np.testing.assert_array_equal(h0[:, :k], h1[:, :k])
+    assert (np.abs(l0[:, k] - l1[:, k]).max(-1) > 0).all()

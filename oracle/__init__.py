@@ -22,6 +22,10 @@ What it computes, and where the paper states it:
   accepted, greedy acceptance is the longest argmax-matching prefix, and the
   committed tokens are distributed as the target), by Eq. alpha and by brute
   force on tiny vocabularies.
+* ``record`` -- the cycle record's verification distributions: the target's
+  top-64 log-probabilities per draft position, full-vocabulary normalised,
+  in bf16 (App. "Implementing Draft-Path Reconstruction in verl").  Pinned by
+  brute force (a full sort and an independent log-sum-exp) on small rows.
 * ``kv``     -- commit/rollback of the KV index (Sec. 2.2; App. "Train--Inference
   Inconsistency under Teacher Forcing", Eq. tf-restart-kv).  Closed form.
 * ``mtp``    -- the recurrent MTP draft head (Sec. 2.2; App. "Models and Draft
@@ -38,6 +42,7 @@ rounding contract), so that integer decisions can be compared bit for bit.
 from .numerics import Rounding, round_bf16, softmax, rmsnorm, silu, rope, inverse_cdf, inverse_cdf_rows  # noqa: F401
 from .model import attention, layer_forward, verify_forward, full_forward, prefill, ar_decode  # noqa: F401
 from .accept import spec_accept, AcceptResult  # noqa: F401
+from .record import record_topk  # noqa: F401
 from .kv import kv_commit  # noqa: F401
 from .mtp import mtp_apply, mtp_draft  # noqa: F401
 from .mixing import mixing_drafts  # noqa: F401

@@ -156,6 +156,20 @@ typedef struct {
   double sum;
 } gm_row_stats;
 
+/* The cycle record's verification distributions (App. "Implementing Draft-Path
+ * Reconstruction in verl", recording in rollout): for every sequence b and draft
+ * position i < k, the `topk` largest entries of p_i = softmax(target_logits[b][i] / T),
+ * as log p_i (normalised over the whole vocabulary, not over the kept entries)
+ * rounded to bf16, and their ids; in decreasing probability, equal probabilities
+ * in increasing id.  (The record's other items -- the drafts, the accepted
+ * length, the start position and the hidden at the cycle's start -- are inputs
+ * or outputs of the step already.) */
+typedef struct {
+  int topk;           /* 1..64, at most V */
+  uint16_t *logp;     /* [B][k][topk] bf16 */
+  int32_t *ids;       /* [B][k][topk] */
+} gm_record;
+
 /* Bytes of workspace the given call needs (0 on invalid arguments).
  * `max_ctx` is the bound that the call's gm_kv_cache carries. */
 size_t gm_workspace_size(int op, const gm_model_config *cfg, int B, int k, int max_ctx);
@@ -200,13 +214,17 @@ gm_status gm_verify_attention(const gm_model_config *cfg, const gm_kv_cache *cac
  *   writes them.  Given, they stand in for a pass over the draft rows; the
  *   caller guarantees that they describe these draft_logits.
  * Outputs: n_accept [B] in [0, k]; out_tokens [B][k+1] = d_0..d_{n-1}, final, -1 pad.
+ * record (host struct, may be NULL): also writes the cycle record's top-k
+ *   log-probabilities of the target rows 0..k-1 (see gm_record), taken in the same
+ *   pass over the target logits.  GM_ERR_INVALID_ARG if topk is outside 1..min(64, V)
+ *   or a record buffer is NULL.
  * The logits rows are read in place; no probability matrix is written. */
 gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature,
                          const float *target_logits, const float *draft_logits,
                          const gm_row_stats *draft_stats,
                          const int32_t *draft_tokens, const float *u_accept, const float *u_final,
-                         int32_t *n_accept, int32_t *out_tokens, void *ws, size_t ws_bytes,
-                         void *stream);
+                         int32_t *n_accept, int32_t *out_tokens, const gm_record *record, void *ws,
+                         size_t ws_bytes, void *stream);
 
 /* Commit / rollback (Sec. 2.2; App. "Train--Inference Inconsistency under
  * Teacher Forcing", Eq. tf-restart-kv): block positions 0..n_b stay, the rest

@@ -35,7 +35,7 @@ constexpr int kMaxK = 15;
 
 // ---------------------------------------------------------------- workspace plans
 struct AcceptPlan {
-  size_t tstat, dstat, sel, wsum, psum, total;
+  size_t tstat, dstat, sel, wsum, psum, submax, total;
 };
 AcceptPlan plan_accept(int B, int k, int V) {
   Carve c;
@@ -46,6 +46,7 @@ AcceptPlan plan_accept(int B, int k, int V) {
   p.sel = c.take(sizeof(RowSel) * (size_t)B);
   p.wsum = c.take(sizeof(double) * (size_t)B * nsc);
   p.psum = c.take(sizeof(double) * (size_t)B * nsc);
+  p.submax = c.take(sizeof(float) * (size_t)B * (k + 1) * nch * 64);   // run maxima of the record's selection
   p.total = c.off;
   return p;
 }
@@ -144,8 +145,8 @@ static_assert(sizeof(gm_row_stats) == sizeof(RowStat) && offsetof(gm_row_stats, 
 extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature, const float *target_logits,
                                     const float *draft_logits, const gm_row_stats *draft_stats,
                                     const int32_t *draft_tokens, const float *u_accept,
-                                    const float *u_final, int32_t *n_accept, int32_t *out_tokens, void *ws,
-                                    size_t ws_bytes, void *stream) {
+                                    const float *u_final, int32_t *n_accept, int32_t *out_tokens,
+                                    const gm_record *record, void *ws, size_t ws_bytes, void *stream) {
   if (B < 0 || k < 0 || k > kMaxK || V < 1) return fail(GM_ERR_INVALID_ARG, "bad B=%d k=%d V=%d", B, k, V);
   if (V > kMaxVocab) return fail(GM_ERR_UNSUPPORTED, "vocab %d exceeds %d", V, kMaxVocab);
   if (mode != GM_GREEDY && mode != GM_SAMPLE) return fail(GM_ERR_INVALID_ARG, "unknown accept mode %d", mode);
@@ -157,6 +158,11 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
     if (!u_final) return fail(GM_ERR_INVALID_ARG, "sample mode needs u_final");
     if (k > 0 && (!draft_logits || !u_accept)) return fail(GM_ERR_INVALID_ARG, "sample mode needs draft_logits and u_accept");
   }
+  if (record && k > 0) {
+    if (record->topk < 1 || record->topk > kRecMaxTopk || record->topk > V)
+      return fail(GM_ERR_INVALID_ARG, "record topk %d outside 1..min(%d, V)", record->topk, kRecMaxTopk);
+    if (!record->logp || !record->ids) return fail(GM_ERR_INVALID_ARG, "null record buffers");
+  }
   const AcceptPlan p = plan_accept(B, k, V);
   gm_status st = check_ws(ws, ws_bytes, p.total);
   if (st != GM_OK) return st;
@@ -165,7 +171,9 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
   RowStat *tstat = (RowStat *)(w + p.tstat), *dstat = (RowStat *)(w + p.dstat);
   RowSel *sel = (RowSel *)(w + p.sel);
   const float inv_t = 1.0f / temperature;
-  launch_row_stats("accept_row_stats", target_logits, V, B * (k + 1), V, inv_t, tstat, s);
+  const bool rec = record && k > 0;
+  float *submax = rec ? (float *)(w + p.submax) : nullptr;
+  launch_row_stats("accept_row_stats", target_logits, V, B * (k + 1), V, inv_t, tstat, s, submax);
   // q's statistics: the draft head's own (one per row) when the caller has them, else a pass over the rows
   int nch_d = stat_chunks(V);
   if (mode == GM_SAMPLE && k > 0) {
@@ -178,6 +186,8 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
   }
   launch_accept_decide(B, k, V, mode, inv_t, target_logits, draft_logits, tstat, dstat, nch_d, draft_tokens, u_accept,
                        u_final, n_accept, out_tokens, sel, s);
+  if (rec)
+    launch_record_topk(B, k, V, inv_t, record->topk, target_logits, tstat, submax, record->logp, record->ids, s);
   if (mode == GM_SAMPLE) launch_residual_draw("accept_residual_chunk", "accept_residual_scan", B, V, inv_t, sel, (double *)(w + p.wsum), (double *)(w + p.psum), s);
   return check_launch("gm_spec_accept");
 }

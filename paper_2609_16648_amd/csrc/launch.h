@@ -77,8 +77,15 @@ void launch_tile_draw(int B, int V, int mode, float inv_t, const float *logits, 
                       const RowStat *tiles, const float *u, int u_stride, int32_t *dst, int dst_stride,
                       RowStat *row_out, int row_stride_out, hipStream_t s);
 
+// submax (may be null): also the raw-logit maxima of every run of kRecSub ids, [row][stat_chunks(V) * 64]
 void launch_row_stats(const char *name, const float *logits, long row_stride, int n_rows, int V, float inv_t,
-                      RowStat *out, hipStream_t s);
+                      RowStat *out, hipStream_t s, float *submax = nullptr);
+// cycle record: the top `topk` entries of softmax(z / T) for block rows 0..k-1 of each
+// sequence, from the accept's row statistics (tstat) and run maxima (submax)
+constexpr int kRecSub = 256;       // ids per run maximum (one wave's load in the row-statistics pass)
+constexpr int kRecMaxTopk = 64;
+void launch_record_topk(int B, int k, int V, float inv_t, int topk, const float *logits, const RowStat *tstat,
+                        const float *submax, uint16_t *logp, int32_t *ids, hipStream_t s);
 // dstat holds nch_d RowStats per draft row (chunk statistics, or one combined per row)
 void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const float *tlog,
                           const float *dlog, const RowStat *tstat, const RowStat *dstat, int nch_d,

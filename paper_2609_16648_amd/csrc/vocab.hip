@@ -24,9 +24,12 @@
 namespace gm {
 
 // ------------------------------------------------------------------ 1. row statistics
+// submax (may be null): [row][n_chunks * 64] maxima of the raw logits over runs of
+// kRecSub = 256 ids (one wave's float4 load), for the cycle record's selection.
 __global__ __launch_bounds__(kStatThreads) void row_stats_kernel(const float *__restrict__ logits,
                                                                  long row_stride, int V, float inv_t,
-                                                                 int n_chunks, RowStat *__restrict__ out) {
+                                                                 int n_chunks, RowStat *__restrict__ out,
+                                                                 float *__restrict__ submax) {
   __shared__ float sm_max[kStatThreads / kWave];
   __shared__ int sm_arg[kStatThreads / kWave];
   __shared__ double sm_sum[kStatThreads / kWave];
@@ -36,16 +39,57 @@ __global__ __launch_bounds__(kStatThreads) void row_stats_kernel(const float *__
   const int hi = min(V, lo + kStatChunk);
   const bool vec = ((V & 3) == 0) && ((row_stride & 3) == 0);
 
-  float v[kStatVec][4];
+  float v[kStatVec][4], rmax[kStatVec];
 #pragma unroll
   for (int j = 0; j < kStatVec; ++j) {
     const int e = lo + 4 * (tid + kStatThreads * j);
+    float f[4];
     if (vec && e + 3 < hi) {
-      const float4 f = *reinterpret_cast<const float4 *>(row + e);
-      v[j][0] = f.x * inv_t; v[j][1] = f.y * inv_t; v[j][2] = f.z * inv_t; v[j][3] = f.w * inv_t;
+      const float4 g = *reinterpret_cast<const float4 *>(row + e);
+      f[0] = g.x; f[1] = g.y; f[2] = g.z; f[3] = g.w;
     } else {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) v[j][q] = (e + q < hi) ? row[e + q] * inv_t : -INFINITY;
+      for (int q = 0; q < 4; ++q) f[q] = (e + q < hi) ? row[e + q] : -INFINITY;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[j][q] = f[q] * inv_t;
+    rmax[j] = fmaxf(fmaxf(f[0], f[1]), fmaxf(f[2], f[3]));
+  }
+  if (submax) {
+    // maxima of the 16 runs of 256 ids this wave loaded (run j: load j of the wave), by a
+    // reduce-scatter over the lanes: after the rounds with masks 32..4 lane L holds run
+    // (L >> 2) & 15 reduced over its lane group, then masks 2 and 1 finish the reduction
+    const int lane = tid & 63;
+    float m8[8], m4[4], m2[2], m1;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const bool hi_half = lane & 32;
+      const float keep = hi_half ? rmax[8 + q] : rmax[q], send = hi_half ? rmax[q] : rmax[8 + q];
+      m8[q] = fmaxf(keep, __shfl_xor(send, 32, kWave));
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const bool hi_half = lane & 16;
+      const float keep = hi_half ? m8[4 + q] : m8[q], send = hi_half ? m8[q] : m8[4 + q];
+      m4[q] = fmaxf(keep, __shfl_xor(send, 16, kWave));
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const bool hi_half = lane & 8;
+      const float keep = hi_half ? m4[2 + q] : m4[q], send = hi_half ? m4[q] : m4[2 + q];
+      m2[q] = fmaxf(keep, __shfl_xor(send, 8, kWave));
+    }
+    {
+      const bool hi_half = lane & 4;
+      const float keep = hi_half ? m2[1] : m2[0], send = hi_half ? m2[0] : m2[1];
+      m1 = fmaxf(keep, __shfl_xor(send, 4, kWave));
+    }
+    m1 = fmaxf(m1, __shfl_xor(m1, 2, kWave));
+    m1 = fmaxf(m1, __shfl_xor(m1, 1, kWave));
+    if ((lane & 3) == 0) {
+      const int j = (lane >> 2) & 15, w = tid >> 6;
+      // run j of wave w covers ids lo + 1024 j + 256 w .. + 255
+      submax[(long)blockIdx.x * n_chunks * 64 + (long)c * 64 + 4 * j + w] = m1;
     }
   }
   // max and lowest arg-max: ids are visited in ascending order within a thread
@@ -91,12 +135,12 @@ __global__ __launch_bounds__(kStatThreads) void row_stats_kernel(const float *__
 }
 
 void launch_row_stats(const char *name, const float *logits, long row_stride, int n_rows, int V, float inv_t,
-                      RowStat *out, hipStream_t s) {
+                      RowStat *out, hipStream_t s, float *submax) {
   if (n_rows <= 0) return;
   TraceScope ts(name, s);
   dim3 grid(n_rows, stat_chunks(V));
   hipLaunchKernelGGL(row_stats_kernel, grid, dim3(kStatThreads), 0, s, logits, row_stride, V, inv_t,
-                     stat_chunks(V), out);
+                     stat_chunks(V), out, submax);
 }
 
 // max, normaliser and lowest arg-max of a whole row from its chunk statistics
@@ -201,6 +245,185 @@ void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const floa
   TraceScope ts("accept_decide", s);
   hipLaunchKernelGGL(accept_decide_kernel, dim3(B), dim3(64), 0, s, B, k, V, mode, inv_t, tlog, dlog, tstat, dstat,
                      stat_chunks(V), nch_d, drafts, u_accept, u_final, n_accept, out_tokens, sel);
+}
+
+// ------------------------------------------------------------------ cycle record
+// The record of a cycle keeps, per draft position, the target's top-k entries of
+// p_i = softmax(z_i / T) as log-probabilities with the full-vocabulary
+// normaliser, in bf16 (App. "Implementing Draft-Path Reconstruction in verl").
+// One block per recorded row.  The topk-th largest run maximum T (runs of
+// kRecSub ids, from the row-statistics pass) bounds the topk-th largest logit
+// from below (the maxima of the topk largest runs are topk distinct ids >= T),
+// so every kept entry is an id with z >= T inside a run whose maximum is >= T.
+// Those candidates, typically a few per run, are keyed (logit, then lower id
+// first), sorted in LDS, and the first topk kept.  When more than kRecCand
+// qualify (heavy ties), a bisection on the logit's order key finds the topk-th
+// value v exactly; the ids above v and then the lowest ids equal to v are taken.
+constexpr int kRecCand = 4096;
+constexpr int kRecMaxRuns = kMaxVocab / kRecSub;
+
+__device__ __forceinline__ uint32_t order_key(float x) {   // larger float, larger key (-0 as +0)
+  uint32_t u = __float_as_uint(x);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ unsigned long long cand_key(float x, int id) {   // larger logit first, then lower id
+  return ((unsigned long long)order_key(x) << 32) | (uint32_t)(0x7fffffff - id);
+}
+
+// descending bitonic sort of n (a power of two) keys in LDS by the whole block
+template <typename K>
+__device__ void block_sort_desc(K *a, int n) {
+  for (int size = 2; size <= n; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      __syncthreads();
+      for (int t = threadIdx.x; t < n / 2; t += blockDim.x) {
+        const int lo = 2 * t - (t & (stride - 1)), hi = lo + stride;
+        const K x = a[lo], y = a[hi];
+        if ((lo & size) == 0 ? x < y : x > y) { a[lo] = y; a[hi] = x; }
+      }
+    }
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(256) void record_topk_kernel(int k, int V, float inv_t, int topk,
+                                                          const float *__restrict__ logits,
+                                                          const RowStat *__restrict__ tstat, int nch,
+                                                          const float *__restrict__ submax,
+                                                          uint16_t *__restrict__ out_logp,
+                                                          int32_t *__restrict__ out_ids) {
+  __shared__ float runs[kRecMaxRuns], srt[kRecMaxRuns];
+  __shared__ unsigned long long cand[kRecCand];
+  __shared__ int sh_cnt;
+  __shared__ double sh_M, sh_lse;
+  const int bi = blockIdx.x, b = bi / k, i = bi % k;
+  const long row = (long)b * (k + 1) + i;   // the block row that verifies draft i
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int nrun = nch * 64;
+  const float *z = logits + row * V;
+  int n2 = 64;
+  while (n2 < nrun) n2 <<= 1;
+  for (int t = tid; t < n2; t += blockDim.x) {
+    const float m = t < nrun ? submax[row * nrun + t] : -INFINITY;
+    runs[t] = m;
+    srt[t] = m;
+  }
+  if (tid == 0) {
+    double M, S;
+    int am;
+    combine_stats(tstat + row * nch, nch, M, S, am);
+    sh_M = M;
+    sh_lse = log(S);
+    sh_cnt = 0;
+  }
+  block_sort_desc(srt, n2);
+  const float T = srt[topk - 1];
+  for (int r = w; r < nrun; r += 4) {
+    if (!(runs[r] >= T)) continue;   // the same for the whole wave
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int x = r * kRecSub + 4 * lane + q;
+      if (x < V) {
+        const float zx = z[x];
+        if (zx >= T) {
+          const int pos = atomicAdd(&sh_cnt, 1);
+          if (pos < kRecCand) cand[pos] = cand_key(zx, x);
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const int cnt = sh_cnt;   // at least topk
+  if (cnt <= kRecCand) {
+    int c2 = 64;
+    while (c2 < cnt) c2 <<= 1;
+    for (int t = cnt + tid; t < c2; t += blockDim.x) cand[t] = 0ull;
+    block_sort_desc(cand, c2);
+  } else {
+    // the largest order key v with at least topk ids at or above it
+    __shared__ int sh_c;
+    uint32_t lo_k = order_key(T), hi_k = 0xffffffffu;
+    while (lo_k < hi_k) {
+      const uint32_t mid = lo_k + (uint32_t)(((unsigned long long)hi_k - lo_k + 1) / 2);
+      if (tid == 0) sh_c = 0;
+      __syncthreads();
+      int local = 0;
+      for (int r = w; r < nrun; r += 4) {
+        if (!(runs[r] >= T)) continue;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int x = r * kRecSub + 4 * lane + q;
+          if (x < V && order_key(z[x]) >= mid) ++local;
+        }
+      }
+      atomicAdd(&sh_c, local);
+      __syncthreads();
+      if (sh_c >= topk) lo_k = mid;
+      else hi_k = mid - 1;
+      __syncthreads();
+    }
+    const uint32_t vk = lo_k;
+    if (tid == 0) sh_cnt = 0;
+    __syncthreads();
+    for (int r = w; r < nrun; r += 4) {   // the ids above v: fewer than topk
+      if (!(runs[r] >= T)) continue;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int x = r * kRecSub + 4 * lane + q;
+        if (x < V && order_key(z[x]) > vk) cand[atomicAdd(&sh_cnt, 1)] = cand_key(z[x], x);
+      }
+    }
+    __syncthreads();
+    const int gt = sh_cnt;
+    if (w == 0) {   // then the lowest ids equal to v, walking the runs in id order
+      int taken = 0;
+      for (int r = 0; r < nrun && taken < topk - gt; ++r) {
+        if (!(runs[r] >= T)) continue;
+        const int x0 = r * kRecSub + 4 * lane;
+        bool hit[4];
+        int m = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          hit[q] = x0 + q < V && order_key(z[x0 + q]) == vk;
+          m += hit[q];
+        }
+        int pre = m;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int n = __shfl_up(pre, o, kWave);
+          if (lane >= o) pre += n;
+        }
+        const int tot = __shfl(pre, 63, kWave);
+        int rank = taken + pre - m;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (hit[q]) {
+            if (rank < topk - gt) cand[gt + rank] = cand_key(z[x0 + q], x0 + q);
+            ++rank;
+          }
+        }
+        taken += tot;
+      }
+    }
+    __syncthreads();
+    for (int t = topk + tid; t < 64; t += blockDim.x) cand[t] = 0ull;
+    block_sort_desc(cand, 64);
+  }
+  for (int t = tid; t < topk; t += blockDim.x) {
+    const int id = 0x7fffffff - (int)(uint32_t)cand[t];
+    const double lp = (double)(z[id] * inv_t) - sh_M - sh_lse;   // the statistics' float32 z / T
+    out_logp[(long)bi * topk + t] = f32_to_bf16((float)lp);
+    out_ids[(long)bi * topk + t] = id;
+  }
+}
+
+void launch_record_topk(int B, int k, int V, float inv_t, int topk, const float *logits, const RowStat *tstat,
+                        const float *submax, uint16_t *logp, int32_t *ids, hipStream_t s) {
+  if (B <= 0 || k <= 0) return;
+  TraceScope ts("record_topk", s);
+  hipLaunchKernelGGL(record_topk_kernel, dim3(B * k), dim3(256), 0, s, k, V, inv_t, topk, logits, tstat,
+                     stat_chunks(V), submax, logp, ids);
 }
 
 // ------------------------------------------------------------------ 3. inverse-CDF draw

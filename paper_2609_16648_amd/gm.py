@@ -86,7 +86,7 @@ def lib() -> ctypes.CDLL:
                                       c_void_p, c_size_t, c_void_p, c_void_p]
     L.gm_spec_accept.restype = c_int
     L.gm_spec_accept.argtypes = [c_int, c_int, c_int, c_int, c_float, c_void_p, c_void_p, c_void_p, c_void_p,
-                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
+                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
     L.gm_kv_commit.restype = c_int
     L.gm_kv_commit.argtypes = [P(KVCacheDesc), c_int, c_int, c_void_p, c_void_p, c_void_p]
     L.gm_mtp_draft.restype = c_int
@@ -324,6 +324,12 @@ def verify_attention(cfg: ModelConfig, cache: PagedCache, layer: int, q: torch.T
 
 
 ROW_STATS_BYTES = 16   # gm_row_stats: float max, int32 argmax, double sum
+RECORD_MAX_TOPK = 64
+
+
+class Record(ctypes.Structure):
+    """gm_record: the cycle record's top-k log-probabilities (bf16) and ids."""
+    _fields_ = [("topk", ctypes.c_int), ("logp", ctypes.c_void_p), ("ids", ctypes.c_void_p)]
 
 
 def new_row_stats(B: int, k: int, device="cuda") -> torch.Tensor:
@@ -342,7 +348,8 @@ def decode_row_stats(t: torch.Tensor):
 def spec_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], draft_tokens: torch.Tensor,
                 u_accept: Optional[torch.Tensor], u_final: Optional[torch.Tensor], n_accept: torch.Tensor,
                 out_tokens: torch.Tensor, mode: int, ws: Workspace, temperature: float = 1.0, stream=None,
-                draft_stats: Optional[torch.Tensor] = None):
+                draft_stats: Optional[torch.Tensor] = None, record=None):
+    """record: optional (logp [B, k, topk] bfloat16, ids [B, k, topk] int32) for the cycle record."""
     B, k1, V = target_logits.shape
     k = k1 - 1
     _need(target_logits, torch.float32, (B, k1, V), "target_logits")
@@ -353,13 +360,21 @@ def spec_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor
     _need(out_tokens, torch.int32, (B, k1), "out_tokens")
     if draft_stats is not None:
         _need(draft_stats, torch.uint8, (B, k, ROW_STATS_BYTES), "draft_stats")
+    rec = None
+    if record is not None:
+        logp, ids = record
+        topk = logp.shape[-1] if logp.dim() == 3 else 0
+        _need(logp, torch.bfloat16, (B, k, topk), "record logp")
+        _need(ids, torch.int32, (B, k, topk), "record ids")
+        rec = Record(topk, _ptr(logp), _ptr(ids))
     cfg = ModelConfig()
     cfg.vocab = V
     n = workspace_size(GM_OP_SPEC_ACCEPT, cfg, B, k, 0)
     buf = ws.get(n)
     _check(lib().gm_spec_accept(B, k, V, mode, float(temperature), _ptr(target_logits), _ptr(draft_logits),
-                                _ptr(draft_stats), _ptr(draft_tokens), _ptr(u_accept), _ptr(u_final), _ptr(n_accept), _ptr(out_tokens),
-                                _ptr(buf), buf.numel(), _stream(stream)))
+                                _ptr(draft_stats), _ptr(draft_tokens), _ptr(u_accept), _ptr(u_final), _ptr(n_accept),
+                                _ptr(out_tokens), ctypes.byref(rec) if rec is not None else None, _ptr(buf),
+                                buf.numel(), _stream(stream)))
 
 
 def kv_commit(cache: PagedCache, k: int, n_accept: torch.Tensor, committed_slots: Optional[torch.Tensor] = None,

@@ -56,7 +56,7 @@ def test_spec_accept_rejects_bad_arguments():
 
     def call(a):
         return L.gm_spec_accept(a["B"], a["k"], a["V"], a["mode"], a["T"], a["tl"], a["dl"], None, a["dt"], a["ua"],
-                                a["uf"], a["n"], a["out"], a["ws"], a["nbytes"], None)
+                                a["uf"], a["n"], a["out"], a.get("rec"), a["ws"], a["nbytes"], None)
 
     assert call(args(k=16)) == gm.GM_ERR_INVALID_ARG
     assert call(args(mode=7)) == gm.GM_ERR_INVALID_ARG
@@ -68,6 +68,12 @@ def test_spec_accept_rejects_bad_arguments():
     assert call(args(nbytes=16)) == gm.GM_ERR_WORKSPACE
     assert call(args(ws=ctypes.c_void_p((1 << 20) + 8))) == gm.GM_ERR_WORKSPACE      # misaligned
     assert call(args(B=0)) == gm.GM_OK                                               # nothing to do
+    rec = gm.Record(65, FAKE, FAKE)                                                  # record width above 64
+    assert call(args(rec=ctypes.byref(rec))) == gm.GM_ERR_INVALID_ARG and "topk" in gm.last_error()
+    rec = gm.Record(64, FAKE, None)
+    assert call(args(rec=ctypes.byref(rec))) == gm.GM_ERR_INVALID_ARG
+    rec = gm.Record(64, FAKE, FAKE)
+    assert call(args(V=40, rec=ctypes.byref(rec))) == gm.GM_ERR_INVALID_ARG         # wider than the vocabulary
 
 
 class _FakeCache:

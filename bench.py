@@ -98,12 +98,17 @@ def accounting(wl, lens):
 class Step:
     """Device state of one workload and the enqueue of one step."""
 
-    def __init__(self, wl, mode, device="cuda"):
+    def __init__(self, wl, mode, device="cuda", record=0):
         import torch
         from paper_2609_16648_amd import gm
         self.torch, self.gm, self.wl = torch, gm, wl
         s, B, k = wl.shape, wl.batch, wl.k
         self.mode = gm.GM_SAMPLE if mode == "sample" else gm.GM_GREEDY
+        # the cycle record's top-k log-probabilities per draft position, taken in the accept's pass
+        self.record = None
+        if record:
+            self.record = (torch.zeros((wl.batch, wl.k, record), dtype=torch.bfloat16, device=device),
+                           torch.zeros((wl.batch, wl.k, record), dtype=torch.int32, device=device))
         t0 = time.time()
         self.lens = synth.context_lengths(wl)
         cap = self.lens + 2 * k + 2
@@ -188,12 +193,13 @@ class Step:
         self.cache.seq_lens.copy_(self.lens0)
         if wl.name == "long_ctx":
             gm.verify_attention(self.cfg, self.cache, 0, self.q, self.attn_out, self.ws_v)
-            gm.spec_accept(self.zt, self.zq, self.drafts, self.ua, self.uf, self.n, self.out, self.mode, self.ws_a)
+            gm.spec_accept(self.zt, self.zq, self.drafts, self.ua, self.uf, self.n, self.out, self.mode, self.ws_a,
+                           record=self.record)
             gm.kv_commit(self.cache, k, self.n, self.slots)
             return
         gm.verify_forward(self.model, self.cache, self.tokens, self.logits, self.hidden, self.ws_v)
         gm.spec_accept(self.logits, self.zq, self.drafts, self.ua, self.uf, self.n, self.out, self.mode, self.ws_a,
-                       draft_stats=self.zq_stats if wl.with_mtp else None)
+                       draft_stats=self.zq_stats if wl.with_mtp else None, record=self.record)
         gm.kv_commit(self.cache, k, self.n, self.slots)
         if wl.with_mtp:
             self.mcache.seq_lens.copy_(self.lens0)
@@ -309,6 +315,8 @@ def main():
     ap.add_argument("--mode", default="sample", choices=["sample", "greedy"])
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--record", type=int, default=0, metavar="K",
+                    help="also take the cycle record's top-K log-probabilities in the accept (0: off)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also time a plain device copy of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -322,7 +330,7 @@ def main():
     gm.lib()
     torch.cuda.set_device(0)
     wl = synth.WORKLOADS[args.workload]
-    step = Step(wl, args.mode)
+    step = Step(wl, args.mode, record=args.record)
 
     for _ in range(args.warmup):
         step()
@@ -417,7 +425,8 @@ def main():
             "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
             "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
             "config": {"workload": args.workload, "description": DESCRIPTIONS[args.workload],
-                       "batch": wl.batch, "k": wl.k, "accept_mode": args.mode, "parallelism": "none (1 GPU)"},
+                       "batch": wl.batch, "k": wl.k, "accept_mode": args.mode, "parallelism": "none (1 GPU)",
+                       "record_topk": args.record},
             "roofline": roof, "summary": summary, "kernels": kernels}
     if not args.no_cpu_baseline:
         weights = None

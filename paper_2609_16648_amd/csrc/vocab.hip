@@ -287,28 +287,25 @@ __device__ void block_sort_desc(K *a, int n) {
   __syncthreads();
 }
 
-__global__ __launch_bounds__(256) void record_topk_kernel(int k, int V, float inv_t, int topk,
+__global__ __launch_bounds__(1024) void record_topk_kernel(int k, int V, float inv_t, int topk,
                                                           const float *__restrict__ logits,
                                                           const RowStat *__restrict__ tstat, int nch,
                                                           const float *__restrict__ submax,
                                                           uint16_t *__restrict__ out_logp,
                                                           int32_t *__restrict__ out_ids) {
-  __shared__ float runs[kRecMaxRuns], srt[kRecMaxRuns];
-  __shared__ unsigned long long cand[kRecCand];
-  __shared__ int sh_cnt;
+  __shared__ __attribute__((aligned(16))) float runs[kRecMaxRuns];
+  __shared__ __attribute__((aligned(16))) unsigned long long cand[kRecCand];
+  __shared__ unsigned long long top[kRecMaxTopk];
+  __shared__ int qual[kRecMaxRuns];   // the runs whose maximum is >= T
+  __shared__ int sh_cnt, sh_nq;
+  __shared__ float sh_T;
   __shared__ double sh_M, sh_lse;
   const int bi = blockIdx.x, b = bi / k, i = bi % k;
   const long row = (long)b * (k + 1) + i;   // the block row that verifies draft i
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, nw = blockDim.x >> 6;
   const int nrun = nch * 64;
   const float *z = logits + row * V;
-  int n2 = 64;
-  while (n2 < nrun) n2 <<= 1;
-  for (int t = tid; t < n2; t += blockDim.x) {
-    const float m = t < nrun ? submax[row * nrun + t] : -INFINITY;
-    runs[t] = m;
-    srt[t] = m;
-  }
+  for (int t = tid; t < nrun; t += blockDim.x) runs[t] = submax[row * nrun + t];
   if (tid == 0) {
     double M, S;
     int am;
@@ -316,26 +313,80 @@ __global__ __launch_bounds__(256) void record_topk_kernel(int k, int V, float in
     sh_M = M;
     sh_lse = log(S);
     sh_cnt = 0;
+    sh_nq = 0;
   }
-  block_sort_desc(srt, n2);
-  const float T = srt[topk - 1];
-  for (int r = w; r < nrun; r += 4) {
-    if (!(runs[r] >= T)) continue;   // the same for the whole wave
+  __syncthreads();
+  // T: the topk-th largest run maximum, i.e. a maximum with fewer than topk maxima above
+  // it and at least topk at or above it (every such maximum has the same value)
+  for (int t = tid; t < nrun; t += blockDim.x) {   // nrun is a multiple of 64
+    const float m = runs[t];
+    int gt = 0, ge = 0;
+    const float4 *r4 = reinterpret_cast<const float4 *>(runs);
+    for (int j = 0; j < nrun / 4; j += 4) {
+      float4 r[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int x = r * kRecSub + 4 * lane + q;
-      if (x < V) {
-        const float zx = z[x];
-        if (zx >= T) {
+      for (int u = 0; u < 4; ++u) r[u] = r4[j + u];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        gt += (r[u].x > m) + (r[u].y > m) + (r[u].z > m) + (r[u].w > m);
+        ge += (r[u].x >= m) + (r[u].y >= m) + (r[u].z >= m) + (r[u].w >= m);
+      }
+    }
+    if (gt < topk && ge >= topk) sh_T = m;
+  }
+  __syncthreads();
+  const float T = sh_T;
+  for (int r = tid; r < nrun; r += blockDim.x)
+    if (runs[r] >= T) qual[atomicAdd(&sh_nq, 1)] = r;
+  __syncthreads();
+  // every 4-id group of the qualifying runs, spread over the whole block, 8 groups per
+  // thread in flight at once
+  const int ngroups = sh_nq * (kRecSub / 4);
+  for (int g0 = tid; g0 < ngroups; g0 += 8 * blockDim.x) {
+    float v[8][4];
+    int xb[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int g = g0 + u * blockDim.x;
+      xb[u] = g < ngroups ? qual[g / (kRecSub / 4)] * kRecSub + 4 * (g % (kRecSub / 4)) : V;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[u][q] = xb[u] + q < V ? z[xb[u] + q] : -INFINITY;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (xb[u] + q < V && v[u][q] >= T) {
           const int pos = atomicAdd(&sh_cnt, 1);
-          if (pos < kRecCand) cand[pos] = cand_key(zx, x);
+          if (pos < kRecCand) cand[pos] = cand_key(v[u][q], xb[u] + q);
         }
       }
     }
   }
   __syncthreads();
   const int cnt = sh_cnt;   // at least topk
-  if (cnt <= kRecCand) {
+  if (cnt <= 512) {
+    // few candidates: each one's rank is the number of larger keys (keys are distinct;
+    // the padding keys are 0, below every candidate)
+    const int c8 = (cnt + 7) & ~7;
+    for (int t = cnt + tid; t < c8; t += blockDim.x) cand[t] = 0ull;
+    __syncthreads();
+    for (int t = tid; t < cnt; t += blockDim.x) {
+      const unsigned long long key = cand[t];
+      int rank = 0;
+      for (int j = 0; j < c8; j += 8) {
+        unsigned long long c[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) c[u] = cand[j + u];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) rank += c[u] > key;
+      }
+      if (rank < topk) top[rank] = key;
+    }
+    __syncthreads();
+    for (int t = tid; t < topk; t += blockDim.x) cand[t] = top[t];
+    __syncthreads();
+  } else if (cnt <= kRecCand) {
     int c2 = 64;
     while (c2 < cnt) c2 <<= 1;
     for (int t = cnt + tid; t < c2; t += blockDim.x) cand[t] = 0ull;
@@ -349,7 +400,7 @@ __global__ __launch_bounds__(256) void record_topk_kernel(int k, int V, float in
       if (tid == 0) sh_c = 0;
       __syncthreads();
       int local = 0;
-      for (int r = w; r < nrun; r += 4) {
+      for (int r = w; r < nrun; r += nw) {
         if (!(runs[r] >= T)) continue;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -366,7 +417,7 @@ __global__ __launch_bounds__(256) void record_topk_kernel(int k, int V, float in
     const uint32_t vk = lo_k;
     if (tid == 0) sh_cnt = 0;
     __syncthreads();
-    for (int r = w; r < nrun; r += 4) {   // the ids above v: fewer than topk
+    for (int r = w; r < nrun; r += nw) {   // the ids above v: fewer than topk
       if (!(runs[r] >= T)) continue;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -422,7 +473,7 @@ void launch_record_topk(int B, int k, int V, float inv_t, int topk, const float 
                         const float *submax, uint16_t *logp, int32_t *ids, hipStream_t s) {
   if (B <= 0 || k <= 0) return;
   TraceScope ts("record_topk", s);
-  hipLaunchKernelGGL(record_topk_kernel, dim3(B * k), dim3(256), 0, s, k, V, inv_t, topk, logits, tstat,
+  hipLaunchKernelGGL(record_topk_kernel, dim3(B * k), dim3(1024), 0, s, k, V, inv_t, topk, logits, tstat,
                      stat_chunks(V), submax, logp, ids);
 }
 

@@ -26,6 +26,13 @@ What it computes, and where the paper states it:
   top-64 log-probabilities per draft position, full-vocabulary normalised,
   in bf16 (App. "Implementing Draft-Path Reconstruction in verl").  Pinned by
   brute force (a full sort and an independent log-sum-exp) on small rows.
+* ``dca``    -- the depth-coupled acceptance loss with verify-gated masking over
+  the record's top-64 support plus one residual bin, and its gradient with
+  respect to the head logits (Sec. "The Depth-Coupled Acceptance Loss",
+  "Learning up to the First Rejection"; App. "DCA").  Pinned by float64
+  autograd of an independent torch form, by Eq. alpha's identity alpha = 1 - TV
+  when the record covers the vocabulary, by Eq. dca-identity, by the range of
+  Eq. dca-tail and by the closed forms of VGM.
 * ``kv``     -- commit/rollback of the KV index (Sec. 2.2; App. "Train--Inference
   Inconsistency under Teacher Forcing", Eq. tf-restart-kv).  Closed form.
 * ``mtp``    -- the recurrent MTP draft head (Sec. 2.2; App. "Models and Draft
@@ -43,6 +50,7 @@ from .numerics import Rounding, round_bf16, softmax, rmsnorm, silu, rope, invers
 from .model import attention, layer_forward, verify_forward, full_forward, prefill, ar_decode  # noqa: F401
 from .accept import spec_accept, AcceptResult  # noqa: F401
 from .record import record_topk  # noqa: F401
+from .dca import dca_loss  # noqa: F401
 from .kv import kv_commit  # noqa: F401
 from .mtp import mtp_apply, mtp_draft  # noqa: F401
 from .mixing import mixing_drafts  # noqa: F401

@@ -59,7 +59,8 @@ typedef enum {
   GM_OP_VERIFY_FORWARD = 0,
   GM_OP_VERIFY_ATTENTION = 1,
   GM_OP_SPEC_ACCEPT = 2,
-  GM_OP_MTP_DRAFT = 3
+  GM_OP_MTP_DRAFT = 3,
+  GM_OP_DCA_LOSS = 4     /* B = cycles N, k = draft length K, cfg->vocab = V */
 } gm_op;
 
 /* Decoder shape: pre-norm RMSNorm / RoPE (rotate-half, angle pos * base^(-2i/d))
@@ -259,6 +260,26 @@ gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weights *mtp,
                        const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft,
                        int32_t *drafts, float *draft_logits, gm_row_stats *draft_stats, void *ws,
                        size_t ws_bytes, int32_t *dev_err, void *stream);
+
+/* Depth-coupled acceptance loss with verify-gated masking, and its gradient in
+ * the head logits (Sec. "The Depth-Coupled Acceptance Loss" and "Learning up to
+ * the First Rejection", Eqs. alpha, chain, dca, vgm; App. "DCA"), over the cycle
+ * record's sparse support (App. "Implementing Draft-Path Reconstruction in
+ * verl").  For cycle n and draft position k: q = softmax(head_logits[n][k]) over
+ * the whole vocabulary, gathered at the record's ids S; p = exp(rec_logp); one
+ * residual bin holds the mass outside S, p_R = max(0, 1 - sum_S p), q_R = 1 - sum_S q.
+ *   alpha[n][k] = sum_S min(p, q) + min(p_R, q_R)
+ *   loss[n]     = -log sum_{l=1}^{L} prod_{i<=l} alpha[n][i],
+ *                 L = min(n_accept[n] + 1, K) if vgm, else K
+ * grad (may be NULL) [N][K][V]: d loss[n] / d head_logits[n][k][x] (positions past
+ * L get 0; the subgradient of min is 0 where its arguments are equal).
+ * head_logits [N][K][V] float32; rec_logp [N][K][topk] bf16; rec_ids [N][K][topk]
+ * (distinct ids; ids outside 0..V-1 are left out of S); n_accept [N] in 0..K.
+ * loss [N] and alpha [N][K] are float32 (computed in float64); grad is float32.
+ * Limits: 1 <= K <= 15, 1 <= topk <= min(64, V), V <= 524288. */
+gm_status gm_dca_loss(int N, int K, int V, int topk, const float *head_logits, const uint16_t *rec_logp,
+                      const int32_t *rec_ids, const int32_t *n_accept, int vgm, float *loss, float *alpha,
+                      float *grad, void *ws, size_t ws_bytes, void *stream);
 
 /* Thread-local message describing the last non-OK status of this thread. */
 const char *gm_last_error(void);

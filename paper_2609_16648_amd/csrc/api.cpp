@@ -131,6 +131,9 @@ extern "C" size_t gm_workspace_size(int op, const gm_model_config *cfg, int B, i
     case GM_OP_MTP_DRAFT:
       if (check_config(cfg, B, k) != GM_OK) return 0;
       return plan_mtp(*cfg, B, k, max_ctx).total;
+    case GM_OP_DCA_LOSS:
+      if (B < 0 || k < 1 || k > kMaxK || cfg->vocab < 1 || cfg->vocab > kMaxVocab) return 0;
+      return dca_workspace(B, k, cfg->vocab);
     default:
       return 0;
   }
@@ -190,6 +193,24 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
     launch_record_topk(B, k, V, inv_t, record->topk, target_logits, tstat, submax, record->logp, record->ids, s);
   if (mode == GM_SAMPLE) launch_residual_draw("accept_residual_chunk", "accept_residual_scan", B, V, inv_t, sel, (double *)(w + p.wsum), (double *)(w + p.psum), s);
   return check_launch("gm_spec_accept");
+}
+
+// ---------------------------------------------------------------- gm_dca_loss
+extern "C" gm_status gm_dca_loss(int N, int K, int V, int topk, const float *head_logits, const uint16_t *rec_logp,
+                                 const int32_t *rec_ids, const int32_t *n_accept, int vgm, float *loss, float *alpha,
+                                 float *grad, void *ws, size_t ws_bytes, void *stream) {
+  if (N < 0 || K < 1 || K > kMaxK || V < 1) return fail(GM_ERR_INVALID_ARG, "bad N=%d K=%d V=%d", N, K, V);
+  if (V > kMaxVocab) return fail(GM_ERR_UNSUPPORTED, "vocab %d exceeds %d", V, kMaxVocab);
+  if (topk < 1 || topk > kRecMaxTopk || topk > V)
+    return fail(GM_ERR_INVALID_ARG, "topk %d outside 1..min(%d, V)", topk, kRecMaxTopk);
+  if (N == 0) return GM_OK;
+  if (!head_logits || !rec_logp || !rec_ids || !loss || !alpha || (vgm && !n_accept))
+    return fail(GM_ERR_INVALID_ARG, "null DCA input / output");
+  gm_status st = check_ws(ws, ws_bytes, dca_workspace(N, K, V));
+  if (st != GM_OK) return st;
+  run_dca_loss(N, K, V, topk, head_logits, rec_logp, rec_ids, n_accept, vgm, loss, alpha, grad, (char *)ws,
+               (hipStream_t)stream);
+  return check_launch("gm_dca_loss");
 }
 
 // ---------------------------------------------------------------- gm_kv_commit

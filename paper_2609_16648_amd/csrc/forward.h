@@ -100,6 +100,12 @@ struct RopeArgs {
   int32_t *dev_err;
 };
 void launch_rope_append(const RopeArgs &a, hipStream_t s);
+
+// DCA loss with verify-gated masking over the cycle record (dca.hip)
+size_t dca_workspace(int N, int K, int V);
+void run_dca_loss(int N, int K, int V, int topk, const float *head_logits, const uint16_t *rec_logp,
+                  const int32_t *rec_ids, const int32_t *n_accept, int vgm, float *loss, float *alpha, float *grad,
+                  char *ws, hipStream_t s);
 void launch_mtp_input(int dtype, int M, int H, int V, float eps, const float *h, const int32_t *tok,
                       int tok_stride, const void *E, const void *norm_h, const void *norm_e, void *out,
                       int32_t *dev_err, hipStream_t s);

@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(_HERE, "libgm.so")
 GM_OK, GM_ERR_INVALID_ARG, GM_ERR_UNSUPPORTED, GM_ERR_CAPACITY, GM_ERR_WORKSPACE, GM_ERR_DEVICE = 0, -1, -2, -3, -4, -5
 GM_F32, GM_BF16 = 0, 1
 GM_GREEDY, GM_SAMPLE = 0, 1
-GM_OP_VERIFY_FORWARD, GM_OP_VERIFY_ATTENTION, GM_OP_SPEC_ACCEPT, GM_OP_MTP_DRAFT = 0, 1, 2, 3
+GM_OP_VERIFY_FORWARD, GM_OP_VERIFY_ATTENTION, GM_OP_SPEC_ACCEPT, GM_OP_MTP_DRAFT, GM_OP_DCA_LOSS = 0, 1, 2, 3, 4
 GM_DEVERR_TOKEN, GM_DEVERR_PAGE = 1, 2
 
 c_int, c_float, c_void_p, c_size_t, c_double = ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_double
@@ -64,7 +64,7 @@ class KVCacheDesc(ctypes.Structure):
 _lib = None
 
 EXPORTS = ["gm_workspace_size", "gm_verify_forward", "gm_verify_attention", "gm_spec_accept", "gm_kv_commit",
-           "gm_mtp_draft", "gm_last_error", "gm_trace_start", "gm_trace_stop", "gm_trace_count", "gm_trace_get"]
+           "gm_mtp_draft", "gm_dca_loss", "gm_last_error", "gm_trace_start", "gm_trace_stop", "gm_trace_count", "gm_trace_get"]
 
 
 def lib() -> ctypes.CDLL:
@@ -93,6 +93,9 @@ def lib() -> ctypes.CDLL:
     L.gm_mtp_draft.argtypes = [P(ModelConfig), P(MtpWeights), P(ModelWeights), P(KVCacheDesc), c_int, c_int,
                                c_int, c_float, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                c_void_p, c_void_p, c_size_t, c_void_p, c_void_p]
+    L.gm_dca_loss.restype = c_int
+    L.gm_dca_loss.argtypes = [c_int, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_void_p,
+                              c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
     L.gm_last_error.restype = ctypes.c_char_p
     L.gm_last_error.argtypes = []
     L.gm_trace_start.restype = c_int
@@ -403,6 +406,29 @@ def mtp_draft(model: DeviceModel, mtp: DeviceMtp, mtp_cache: PagedCache, k: int,
                               _ptr(out_tokens), _ptr(u_draft), _ptr(drafts), _ptr(draft_logits), _ptr(draft_stats),
                               _ptr(buf),
                               buf.numel(), _ptr(dev_err), _stream(stream)))
+
+
+def dca_loss(head_logits: torch.Tensor, rec_logp: torch.Tensor, rec_ids: torch.Tensor,
+             n_accept: Optional[torch.Tensor], loss: torch.Tensor, alpha: torch.Tensor,
+             grad: Optional[torch.Tensor], ws: Workspace, vgm: bool = True, stream=None):
+    """DCA loss (with verify-gated masking when vgm) over the cycle record; see gm.h."""
+    N, K, V = head_logits.shape
+    topk = rec_ids.shape[-1]
+    _need(head_logits, torch.float32, (N, K, V), "head_logits")
+    _need(rec_logp, torch.bfloat16, (N, K, topk), "rec_logp")
+    _need(rec_ids, torch.int32, (N, K, topk), "rec_ids")
+    if n_accept is not None:
+        _need(n_accept, torch.int32, (N,), "n_accept")
+    _need(loss, torch.float32, (N,), "loss")
+    _need(alpha, torch.float32, (N, K), "alpha")
+    if grad is not None:
+        _need(grad, torch.float32, (N, K, V), "grad")
+    cfg = ModelConfig()
+    cfg.vocab = V
+    buf = ws.get(workspace_size(GM_OP_DCA_LOSS, cfg, N, K, 0))
+    _check(lib().gm_dca_loss(N, K, V, topk, _ptr(head_logits), _ptr(rec_logp), _ptr(rec_ids), _ptr(n_accept),
+                             int(bool(vgm)), _ptr(loss), _ptr(alpha), _ptr(grad), _ptr(buf), buf.numel(),
+                             _stream(stream)))
 
 
 # ------------------------------------------------------------------------ kernel timing

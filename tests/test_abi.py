@@ -183,3 +183,22 @@ def test_weight_tiling_matches_header_formula():
     t = flat[:512].reshape(64, 8)
     for lane in range(64):
         np.testing.assert_array_equal(t[lane], w[lane % 16, 8 * (lane // 16): 8 * (lane // 16) + 8])
+
+
+def test_dca_loss_rejects_bad_arguments():
+    L = gm.lib()
+    ws = ctypes.c_void_p(1 << 20)
+
+    def call(N=4, K=3, V=1000, topk=64, n=FAKE, vgm=1, nbytes=1 << 30):
+        return L.gm_dca_loss(N, K, V, topk, FAKE, FAKE, FAKE, n, vgm, FAKE, FAKE, None, ws, nbytes, None)
+
+    assert call(K=0) == gm.GM_ERR_INVALID_ARG
+    assert call(K=16) == gm.GM_ERR_INVALID_ARG
+    assert call(topk=65) == gm.GM_ERR_INVALID_ARG and "topk" in gm.last_error()
+    assert call(V=40) == gm.GM_ERR_INVALID_ARG                 # record wider than the vocabulary
+    assert call(n=None) == gm.GM_ERR_INVALID_ARG               # verify-gated masking needs n_accept
+    assert call(nbytes=64) == gm.GM_ERR_WORKSPACE
+    assert call(N=0) == gm.GM_OK
+    cfg = gm.ModelConfig()
+    cfg.vocab = 151936
+    assert gm.workspace_size(gm.GM_OP_DCA_LOSS, cfg, 1024, 3, 0) > gm.workspace_size(gm.GM_OP_DCA_LOSS, cfg, 8, 3, 0)

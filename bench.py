@@ -207,6 +207,46 @@ class Step:
                          self.next_drafts, self.dlog, self.ws_m, draft_stats=self.next_stats)
 
 
+# ----------------------------------------------------------------------------- DCA loss timing
+def time_dca(wl, N, iters=5):
+    """The DCA loss with verify-gated masking and its gradient (the head-training side
+    of the cycle record) over N synthetic records: head logits N(0,1) [N, k, V], a
+    top-64 record of other N(0,1) logits, accepted lengths uniform in 0..k.  The pass
+    reads the logits twice (statistics, gradient) and writes the gradient once."""
+    import torch
+    from paper_2609_16648_amd import gm
+    K, V = wl.k, wl.shape.vocab
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(synth.SEED_DRAFT)
+    z = torch.empty((N, K, V), dtype=torch.float32, device="cuda").normal_(generator=gen)
+    zt = torch.empty((N, K, V), dtype=torch.float32, device="cuda").normal_(generator=gen)
+    top = torch.topk(zt, 64, dim=-1)
+    lse = torch.logsumexp(zt, -1, keepdim=True)
+    rec_lp = (top.values - lse).to(torch.bfloat16)
+    rec_id = top.indices.to(torch.int32).contiguous()
+    del zt, top, lse
+    n = torch.randint(0, K + 1, (N,), generator=gen, device="cuda", dtype=torch.int32)
+    loss = torch.empty(N, dtype=torch.float32, device="cuda")
+    alpha = torch.empty((N, K), dtype=torch.float32, device="cuda")
+    grad = torch.empty_like(z)
+    ws = gm.Workspace()
+    gm.dca_loss(z, rec_lp, rec_id, n, loss, alpha, grad, ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(iters):
+        gm.dca_loss(z, rec_lp, rec_id, n, loss, alpha, grad, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / iters
+    nbytes = 3.0 * N * K * V * 4
+    out = {"cycles": N, "k": K, "vocab": V, "ms": round(ms, 4), "GB_s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+           "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_GBS, 3), "mean_loss": round(float(loss.mean()), 5)}
+    del z, grad
+    torch.cuda.empty_cache()
+    return out
+
+
 # ----------------------------------------------------------------------------- CPU baseline
 def cpu_baseline(wl, mode, budget_s, weights=None):
     """The oracle, as it stands, on a bounded sample of the same workload: the
@@ -315,6 +355,8 @@ def main():
     ap.add_argument("--mode", default="sample", choices=["sample", "greedy"])
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--dca", type=int, default=0, metavar="N",
+                    help="also time the DCA loss forward and gradient over N cycle records of the workload's shape")
     ap.add_argument("--record", type=int, default=0, metavar="K",
                     help="also take the cycle record's top-K log-probabilities in the accept (0: off)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -412,6 +454,9 @@ def main():
         "tau": round(1.0 + float(n.mean()), 4),
         "committed_tokens_per_step": committed,
     }
+
+    if args.dca:
+        summary["dca"] = time_dca(wl, args.dca)
 
     if args.copy_probe_mib:
         src = torch.empty(args.copy_probe_mib << 20, dtype=torch.uint8, device="cuda")

@@ -96,11 +96,12 @@ def qwen_mtp():
     return shape, synth.model_weights(shape), synth.mtp_weights(shape)
 
 
-def test_qwen_layer_bf16_mtp_greedy(qwen_mtp):
-    # bf16 logits sit ~1e-3 from the oracle's: drafts are compared in greedy mode (top-2 margin flags)
+@pytest.mark.parametrize("k", [3, 7])
+def test_qwen_layer_bf16_mtp_greedy(qwen_mtp, k):
+    # bf16 logits sit ~1e-3 from the oracle's: drafts are compared in greedy mode (top-2 margin flags);
+    # k = 7 runs the extend with 32-row GQA tiles (the deeper chains of the paper's depth study)
     need_gpu()
     shape, W, Wm = qwen_mtp
-    k = 3
     lens, caches, hidden, n, out, u = _inputs(shape, 8, k, 1, 3000, 2)
     _run(shape, W, Wm, lens, caches, hidden, n, out, u, k, gm.GM_GREEDY, CONTRACT, 1e-2)
 

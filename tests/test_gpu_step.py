@@ -51,12 +51,14 @@ def test_k0_gpu_reproduces_autoregressive_decoding():
     np.testing.assert_array_equal(cache.seq_lens.cpu().numpy(), T0 + steps)
 
 
-def test_greedy_loop_with_mtp_matches_oracle():
+@pytest.mark.parametrize("k", [3, 7])
+def test_greedy_loop_with_mtp_matches_oracle(k):
+    # k = 7: the deeper chains of the paper's depth study
     need_gpu()
     shape = synth.TINY
     W = synth.model_weights(shape)
     Wm = synth.mtp_weights(shape)
-    B, T0, k, cycles = 4, 48, 3, 5
+    B, T0, cycles = 4, 48, 5
     prompt = synth.token_ids(B * (T0 + 1), shape.vocab, 1, "loop").reshape(B, T0 + 1)
     caches = oracle.prefill(shape, W, prompt[:, :T0], EXACT)
     caches = [([a.astype(np.float32) for a in ks], [a.astype(np.float32) for a in vs]) for ks, vs in caches]

@@ -314,18 +314,31 @@ __global__ __launch_bounds__(64 * kAttnWavesPerGroup) void attn_mfma_kernel(Attn
     };
 
     // Tiles [t0, t0 + 16 n) lie below position m0 + 1, inside the window of every valid
-    // query row, and inside the context: no mask.  Rows that are not valid queries (past
-    // the block, or padding) compute finite values nobody reads.
+    // query row, and inside the context: no mask.  The rest (the causal diagonal and the
+    // partial tile at the end of the context) take the mask; the mask zeroes the V entries
+    // past the context in place.  Rows that are not valid queries (past the block, or
+    // padding) compute finite values nobody reads.  All nt tiles stream through the ring,
+    // the masked ones too, so the segment's end is as pipelined as its body.
     const int nm_end = min(tend, m0 + 1);
     const int n = __builtin_amdgcn_readfirstlane(nm_end > t0 ? (nm_end - t0) / 16 : 0);
-    if (n > 0) {
+    const int nt = __builtin_amdgcn_readfirstlane(tend > t0 ? (tend - t0 + 15) / 16 : 0);
+    auto consume = [&](int i, TileBuf &t) {
+      if (i < n) {
+#pragma unroll
+        for (int u = 0; u < RT; ++u) attn_tile<false>(t0 + 16 * i, L, g, a.scale_log2, t, qf[u], vis[u], m[u], l[u], O[u]);
+      } else {
+#pragma unroll
+        for (int u = 0; u < RT; ++u) attn_tile<true>(t0 + 16 * i, L, g, a.scale_log2, t, qf[u], vis[u], m[u], l[u], O[u]);
+      }
+    };
+    if (nt > 0) {
       // whole turns of the ring run unguarded (one straight path, so every wait counts
       // exactly the loads still in flight); the last < kAttnRing tiles are already in
       // the ring when the loop ends
       TileBuf ring[kAttnRing];
-      const int n_pipe = n - n % kAttnRing;
+      const int n_pipe = nt - nt % kAttnRing;
 #pragma unroll
-      for (int d = 0; d < kAttnRing - 1; ++d) load_tile(tile_off(t0 + 16 * min(d, n - 1)), ring[d]);
+      for (int d = 0; d < kAttnRing - 1; ++d) load_tile(tile_off(t0 + 16 * min(d, nt - 1)), ring[d]);
       for (int i = 0; i < n_pipe; i += kAttnRing) {
 #pragma unroll
         for (int d = 0; d < kAttnRing; ++d) {
@@ -333,28 +346,14 @@ __global__ __launch_bounds__(64 * kAttnWavesPerGroup) void attn_mfma_kernel(Attn
           // the scheduling barriers keep each refill after the step that frees its buffer,
           // so the ring keeps fixed registers and no copy waits on a load in flight
           __builtin_amdgcn_sched_barrier(0);
-          load_tile(tile_off(t0 + 16 * min(i + d + kAttnRing - 1, n - 1)), ring[(d + kAttnRing - 1) % kAttnRing]);
+          load_tile(tile_off(t0 + 16 * min(i + d + kAttnRing - 1, nt - 1)), ring[(d + kAttnRing - 1) % kAttnRing]);
           __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-          for (int u = 0; u < RT; ++u)
-            attn_tile<false>(t0 + 16 * (i + d), L, g, a.scale_log2, ring[d], qf[u], vis[u], m[u], l[u], O[u]);
+          consume(i + d, ring[d]);
         }
       }
 #pragma unroll
       for (int d = 0; d < kAttnRing - 1; ++d)
-        if (n_pipe + d < n) {
-#pragma unroll
-          for (int u = 0; u < RT; ++u)
-            attn_tile<false>(t0 + 16 * (n_pipe + d), L, g, a.scale_log2, ring[d], qf[u], vis[u], m[u], l[u], O[u]);
-        }
-    }
-    // the causal diagonal and the partial tile at the end of the context (the mask zeroes
-    // the V entries past the context in place: applying it again is a no-op)
-    for (int tb = t0 + 16 * n; tb < tend; tb += 16) {
-      TileBuf t;
-      load_tile(tile_off(tb), t);
-#pragma unroll
-      for (int u = 0; u < RT; ++u) attn_tile<true>(tb, L, g, a.scale_log2, t, qf[u], vis[u], m[u], l[u], O[u]);
+        if (n_pipe + d < nt) consume(n_pipe + d, ring[d]);
     }
 
 #pragma unroll

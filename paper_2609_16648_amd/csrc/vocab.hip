@@ -45,7 +45,7 @@ __global__ __launch_bounds__(kStatThreads) void row_stats_kernel(const float *__
     const int e = lo + 4 * (tid + kStatThreads * j);
     float f[4];
     if (vec && e + 3 < hi) {
-      const float4 g = *reinterpret_cast<const float4 *>(row + e);
+      const float4 g = __builtin_bit_cast(float4, load_nt(row + e));   // each logit is read once here
       f[0] = g.x; f[1] = g.y; f[2] = g.z; f[3] = g.w;
     } else {
 #pragma unroll
@@ -92,20 +92,21 @@ __global__ __launch_bounds__(kStatThreads) void row_stats_kernel(const float *__
       submax[(long)blockIdx.x * n_chunks * 64 + (long)c * 64 + 4 * j + w] = m1;
     }
   }
-  // max and lowest arg-max: ids are visited in ascending order within a thread
+  // max, then the lowest id attaining it, as two branch-free wave reductions
   float m = -INFINITY;
-  int am = 0x7fffffff;
 #pragma unroll
   for (int j = 0; j < kStatVec; ++j)
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (v[j][q] > m) { m = v[j][q]; am = lo + 4 * (tid + kStatThreads * j) + q; }
+    for (int q = 0; q < 4; ++q) m = fmaxf(m, v[j][q]);
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float om = __shfl_xor(m, o, kWave);
-    const int oa = __shfl_xor(am, o, kWave);
-    if (om > m || (om == m && oa < am)) { m = om; am = oa; }
-  }
+  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+  int am = 0x7fffffff;
+#pragma unroll
+  for (int j = kStatVec - 1; j >= 0; --j)
+#pragma unroll
+    for (int q = 3; q >= 0; --q) am = v[j][q] == m ? lo + 4 * (tid + kStatThreads * j) + q : am;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) am = min(am, __shfl_xor(am, o, kWave));
   const int lane = tid & 63, wid = tid >> 6;
   if (lane == 0) { sm_max[wid] = m; sm_arg[wid] = am; }
   __syncthreads();

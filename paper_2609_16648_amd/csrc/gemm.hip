@@ -634,15 +634,23 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
   p.Nw = epi == EPI_SWIGLU ? 2 * N : N;
   p.n_tiles = p.Nw / cols;
   const int target = 256;                           // workgroups that keep every CU streaming
-  // tile statistics (kStatCols = 128 columns per workgroup) take the 64 x 128 tiles
-  p.shape = (epi != EPI_STATS && M > 64 && p.n_tiles >= target) ? (M <= 128 ? 1 : 2) : 0;
+  // tile statistics (kStatCols = 128 columns per workgroup) take the 64 x 128 tiles.  Past
+  // 256 rows the M tiles already fill the chip, and taller tiles cut the L2 re-reads of
+  // each weight strip (M / BM of them): 256-row tiles, except 128-row ones for outputs of
+  // 128..255 column tiles, whose 256-row launch leaves 2.4 workgroups per CU (measured at
+  // 1024 rows: QKV, O, down and the MTP projection fastest at 256 rows, gate/up at 128).
+  if (epi == EPI_STATS) p.shape = 0;
+  else if (M > 256) p.shape = (p.n_tiles >= 128 && p.n_tiles < target) ? 1 : 2;
+  else p.shape = (M > 64 && p.n_tiles >= target) ? (M <= 128 ? 1 : 2) : 0;
   const int BM = p.shape == 2 ? 256 : p.shape == 1 ? 128 : 64;
   const int ITER = 8;                               // k32 steps per unrolled iteration (see kernel)
   p.m_tiles = (M + BM - 1) / BM;
   p.k_iters = K / (ITER * 32);
   int splits = target / (p.n_tiles * p.m_tiles);
-  // 2 * S * M * Nw * 4 <= Nw * K * 2 / 2 (one M tile), <= Nw * K * 2 (several)
-  const int cap = p.m_tiles > 1 ? K / (4 * M) : K / (8 * M);
+  // 2 * S * M * Nw * 4 <= Nw * K * 2 / 2 (one M tile), <= Nw * K * 2 (several), and up to
+  // 4 Nw * K * 2 past 256 rows, where the weights are re-read from L2 by every M tile anyway
+  // (1024 rows, O projection: 33 us with 3 splits, 47 us unsplit)
+  const int cap = M > 256 ? K / M : p.m_tiles > 1 ? K / (4 * M) : K / (8 * M);
   if (splits > cap) splits = cap;
   if (splits > p.k_iters) splits = p.k_iters;
   if (splits < 1 || epi == EPI_STATS) splits = 1;   // tile statistics need whole dot products

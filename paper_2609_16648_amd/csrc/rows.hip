@@ -137,18 +137,20 @@ __global__ __launch_bounds__(1024) void mtp_input_kernel(int H, int V, float eps
   }
 }
 
-// One wave per (row, head): block (row, y) holds heads 4 y .. 4 y + 3, and lane
-// c < d/2 handles the pair (c, c + d/2).  Each wave reads its head's columns
-// straight from the projection (or sums its K-split partials, in split order),
-// so a row's heads run on as many waves as it has heads.
+// One wave per (row, kRopeHeads consecutive heads): block (row, y) holds 4 such
+// groups, and lane c < d/2 handles the pair (c, c + d/2) of every head of its group.
+// The wave reads its heads' columns straight from the projection (or sums their
+// K-split partials, in split order), all heads' loads in flight together, and
+// takes the rotation of its lane's pair once for the whole group.
+constexpr int kRopeHeads = 4;
 template <typename T>
 __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
   const int row = blockIdx.x, b = row / a.R, i = row % a.R;
   const int lane = threadIdx.x & 63;
   const int D = a.head_dim, half = D / 2;
   const int nh = a.n_heads + 2 * a.n_kv;
-  const int hh = blockIdx.y * 4 + (threadIdx.x >> 6);
-  if (hh >= nh) return;
+  const int h0 = (blockIdx.y * 4 + (threadIdx.x >> 6)) * kRopeHeads;
+  if (h0 >= nh) return;
   int blen = a.R;
   if (a.blk_len) {
     blen = a.blk_len[b] + a.blk_len_add;
@@ -156,12 +158,16 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
   }
   const int slot = a.base_lens[b] + a.base_off + i;
   const double pos = (double)(slot + a.pos_off);
-  const int kind = hh < a.n_heads ? 0 : (hh < a.n_heads + a.n_kv ? 1 : 2);
   const bool act = lane < half;
-  // the pair's two columns (all loads of the splits issued before the sums)
-  float x1 = 0.f, x2 = 0.f;
-  if (act) {
-    const long W = (long)nh * D, off = (long)row * W + (long)hh * D + lane;
+  // the pairs' two columns of every head of the group
+  float x1[kRopeHeads], x2[kRopeHeads];
+  const long W = (long)nh * D;
+#pragma unroll
+  for (int h = 0; h < kRopeHeads; ++h) {
+    x1[h] = 0.f;
+    x2[h] = 0.f;
+    if (!act || h0 + h >= nh) continue;
+    const long off = (long)row * W + (long)(h0 + h) * D + lane;
     if (a.splits > 1) {
       const long stride = (long)a.M * W;
       for (int s0 = 0; s0 < a.splits; s0 += 8) {
@@ -175,59 +181,73 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
           if (s0 + u < a.splits) {
-            x1 += v1[u];
-            x2 += v2[u];
+            x1[h] += v1[u];
+            x2[h] += v2[u];
           }
         }
       }
     } else {
-      x1 = a.qkv[off];
-      x2 = a.qkv[off + half];
+      x1[h] = a.qkv[off];
+      x2[h] = a.qkv[off + half];
     }
   }
-  // the rotation of pair `lane` at this position
+  // the rotation of pair `lane` at this position, shared by the group's heads
   double sn = 0.0, cs = 1.0;
-  if (kind < 2 && act) sincos(pos * pow((double)a.rope_base, -2.0 * lane / D), &sn, &cs);
+  if (act && h0 < a.n_heads + a.n_kv) sincos(pos * pow((double)a.rope_base, -2.0 * lane / D), &sn, &cs);
   const T *qn = (const T *)a.q_norm, *kn = (const T *)a.k_norm;
-  if (kind < 2 && qn) {
-    const T *nw = kind == 0 ? qn : kn;
-    const float ss = wave_sum(x1 * x1 + x2 * x2);
-    const float inv = 1.0f / sqrtf(ss / (float)D + a.eps);
-    if (act) {
-      x1 = x1 * inv * Elem<T>::load(nw, lane);
-      x2 = x2 * inv * Elem<T>::load(nw, lane + half);
+  // the block row's page, for the K/V heads of the group
+  long kv_base = -1;
+  int s_in = 0;
+  if (i < blen && h0 + kRopeHeads > a.n_heads) {
+    const int pi = slot / a.page_size;
+    const int page = pi < a.max_pages ? a.block_table[(long)b * a.max_pages + pi] : -1;
+    if (page < 0 || page >= a.num_pages) {
+      if (lane == 0) raise_dev_err(a.dev_err, GM_DEVERR_PAGE);
+    } else {
+      const int off = slot % a.page_size;
+      kv_base = (((long)page * a.n_kv) * a.page_size + (off & ~15)) * D;
+      s_in = off & 15;
     }
   }
-  if (!act) return;
-  float y1 = x1, y2 = x2;
-  if (kind < 2) {
-    y1 = (float)((double)x1 * cs - (double)x2 * sn);
-    y2 = (float)((double)x2 * cs + (double)x1 * sn);
-  }
-  if (kind == 0) {
-    T *q = (T *)a.q_out + ((long)row * a.n_heads + hh) * D;
-    Elem<T>::store(q, lane, y1);
-    Elem<T>::store(q, lane + half, y2);
-    return;
-  }
-  if (i >= blen) return;   // rows past the block's valid length append nothing
-  const int pi = slot / a.page_size;
-  const int page = pi < a.max_pages ? a.block_table[(long)b * a.max_pages + pi] : -1;
-  if (page < 0 || page >= a.num_pages) {
-    if (lane == 0) raise_dev_err(a.dev_err, GM_DEVERR_PAGE);
-    return;
-  }
-  const int off = slot % a.page_size, s_in = off & 15;
-  const int head = kind == 1 ? hh - a.n_heads : hh - a.n_heads - a.n_kv;
-  const long base = ((((long)page * a.n_kv) * a.page_size + (off & ~15)) * D) + (long)head * a.page_size * D;
-  if (kind == 1) {
-    T *kp = (T *)a.k_pages + base;
-    Elem<T>::store(kp, k_tile_off(s_in, lane), y1);
-    Elem<T>::store(kp, k_tile_off(s_in, lane + half), y2);
-  } else {
-    T *vp = (T *)a.v_pages + base;
-    Elem<T>::store(vp, v_tile_off(s_in, lane), y1);
-    Elem<T>::store(vp, v_tile_off(s_in, lane + half), y2);
+#pragma unroll
+  for (int h = 0; h < kRopeHeads; ++h) {
+    const int hh = h0 + h;
+    if (hh >= nh) break;
+    const int kind = hh < a.n_heads ? 0 : (hh < a.n_heads + a.n_kv ? 1 : 2);
+    float y1 = x1[h], y2 = x2[h];
+    if (kind < 2 && qn) {
+      const T *nw = kind == 0 ? qn : kn;
+      const float ss = wave_sum(y1 * y1 + y2 * y2);
+      const float inv = 1.0f / sqrtf(ss / (float)D + a.eps);
+      if (act) {
+        y1 = y1 * inv * Elem<T>::load(nw, lane);
+        y2 = y2 * inv * Elem<T>::load(nw, lane + half);
+      }
+    }
+    if (!act) continue;
+    if (kind < 2) {
+      const float r1 = (float)((double)y1 * cs - (double)y2 * sn);
+      const float r2 = (float)((double)y2 * cs + (double)y1 * sn);
+      y1 = r1;
+      y2 = r2;
+    }
+    if (kind == 0) {
+      T *q = (T *)a.q_out + ((long)row * a.n_heads + hh) * D;
+      Elem<T>::store(q, lane, y1);
+      Elem<T>::store(q, lane + half, y2);
+    } else if (kv_base >= 0) {   // rows past the block's valid length append nothing
+      const int head = kind == 1 ? hh - a.n_heads : hh - a.n_heads - a.n_kv;
+      const long base = kv_base + (long)head * a.page_size * D;
+      if (kind == 1) {
+        T *kp = (T *)a.k_pages + base;
+        Elem<T>::store(kp, k_tile_off(s_in, lane), y1);
+        Elem<T>::store(kp, k_tile_off(s_in, lane + half), y2);
+      } else {
+        T *vp = (T *)a.v_pages + base;
+        Elem<T>::store(vp, v_tile_off(s_in, lane), y1);
+        Elem<T>::store(vp, v_tile_off(s_in, lane + half), y2);
+      }
+    }
   }
 }
 
@@ -277,7 +297,7 @@ void launch_rmsnorm(int dtype, int M, int H, float eps, const float *x, const vo
 void launch_rope_append(const RopeArgs &a, hipStream_t s) {
   if (a.M <= 0) return;
   TraceScope ts("rope_append", s);
-  const dim3 grid(a.M, (a.n_heads + 2 * a.n_kv + 3) / 4);
+  const dim3 grid(a.M, (a.n_heads + 2 * a.n_kv + 4 * kRopeHeads - 1) / (4 * kRopeHeads));
   if (a.dtype == GM_BF16) hipLaunchKernelGGL(rope_append_kernel<bf16>, grid, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(rope_append_kernel<float>, grid, dim3(256), 0, s, a);
 }

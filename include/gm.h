@@ -274,7 +274,7 @@ gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weights *mtp,
  * grad (may be NULL) [N][K][V]: d loss[n] / d head_logits[n][k][x] (positions past
  * L get 0; the subgradient of min is 0 where its arguments are equal).
  * head_logits [N][K][V] float32; rec_logp [N][K][topk] bf16; rec_ids [N][K][topk]
- * (distinct ids; ids outside 0..V-1 are left out of S); n_accept [N] in 0..K.
+ * (distinct ids in 0..V-1; an id outside gets q = 0 and is never read); n_accept [N] in 0..K.
  * loss [N] and alpha [N][K] are float32 (computed in float64); grad is float32.
  * Limits: 1 <= K <= 15, 1 <= topk <= min(64, V), V <= 524288. */
 gm_status gm_dca_loss(int N, int K, int V, int topk, const float *head_logits, const uint16_t *rec_logp,

@@ -40,6 +40,8 @@ DESCRIPTIONS = {
                       "+ 1-layer MTP head of the same shape; B=64, contexts U[1024,4096], k=3, drafts = target "
                       "top-1 w.p. 0.7 else uniform; T=1",
     "qwen3_4b_full": "36-layer Qwen3-4B shape + 1-layer MTP head; B=256, contexts 512+U[0,8192], k=3; T=1",
+    "qwen3_4b_layer_k7": "the qwen3_4b_layer workload at k=7 (the deepest chain of the depth study): B=64, "
+                         "contexts U[1024,4096], drafts = target top-1 w.p. 0.7 else uniform; T=1",
     "mimo_7b": "36-layer MiMo-7B shape (H 4096, 32/8 heads x 128, FFN 11008, V 151680) + 1-layer MTP head; B=128, "
                "contexts U[2048,16384], k=1, drafts = target top-1 w.p. 0.5 else uniform; T=1",
     "long_ctx": "Qwen3-4B-shaped verify attention + accept only; B=32, contexts U[16384,32768], k=7, "

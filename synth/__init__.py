@@ -119,6 +119,9 @@ WORKLOADS: Dict[str, Workload] = {
     # MiMo-7B shape, 128 rollouts of 2K..16K tokens, k=1, 0.5 top-1 mixing
     "mimo_7b": Workload("mimo_7b", MIMO_7B, batch=128, k=1, ctx_lo=2048, ctx_hi=16384,
                         mix_prob=0.5, with_mtp=True),
+    # the qwen3_4b_layer workload at the depth study's deepest chain (k=7)
+    "qwen3_4b_layer_k7": Workload("qwen3_4b_layer_k7", QWEN3_4B_LAYER, batch=64, k=7,
+                                  ctx_lo=1024, ctx_hi=4096, mix_prob=0.7, with_mtp=True),
     # long-context attention + accept stress, 32 sequences of 16K..32K, k=7
     "long_ctx": Workload("long_ctx", QWEN3_4B_LAYER, batch=32, k=7, ctx_lo=16384,
                          ctx_hi=32768, mix_prob=None),

@@ -67,6 +67,32 @@ __device__ __forceinline__ int xcd_remap(int bid, int T) {
   return x * q + (x < rem ? x : rem) + slot;
 }
 
+// Reductions over the 16 lanes of one DPP row (the lanes j of a C-tile row): xor 1
+// and xor 2 inside quads, then the half-row and row mirrors.
+__device__ __forceinline__ int dpp_i(int v, int ctrl_sel) {
+  switch (ctrl_sel) {
+    case 0: return __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);    // quad_perm [1,0,3,2]
+    case 1: return __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);    // quad_perm [2,3,0,1]
+    case 2: return __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false);   // row_half_mirror
+    default: return __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, false);  // row_mirror
+  }
+}
+__device__ __forceinline__ float row16_max(float v) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v = fmaxf(v, __int_as_float(dpp_i(__float_as_int(v), c)));
+  return v;
+}
+__device__ __forceinline__ int row16_min(int v) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v = min(v, dpp_i(v, c));
+  return v;
+}
+__device__ __forceinline__ float row16_sum(float v) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v += __int_as_float(dpp_i(__float_as_int(v), c));
+  return v;
+}
+
 // MT: 16-row tiles per compute wave; NT: 16-column strips per compute wave;
 // WM: compute waves along M (1 or 2); SW: weights loaded non-temporally (one M
 // tile).  Waves 0-3 compute; wave 4 only stages
@@ -239,8 +265,10 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
 
   if (EPI == EPI_STATS) {
     // softmax statistics of this workgroup's kStatCols columns, per row: every wave
-    // reduces its own columns over the 16 lanes of a row, the waves of a row
-    // meet in LDS (A's buffers are free once the K loop is done)
+    // reduces its own columns over the 16 lanes of a row (branch-free DPP reductions:
+    // the max, then the lowest column attaining it, then the float32 sum of its
+    // terms), the waves of a row meet in LDS (A's buffers are free once the K loop
+    // is done) and combine in float64
     __syncthreads();
     float *sm = reinterpret_cast<float *>(&As[0][0]);          // [BM][WN][3]
     if (w < 4) {
@@ -248,25 +276,21 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
     for (int a = 0; a < MT; ++a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        float vmax = -INFINITY;
-        int varg = 0x7fffffff;
+        float v[NT], vmax = -INFINITY;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-          const float v = acc[a][t][r] * g.inv_t;
-          const int col = strip[t] * 16 + j;
-          if (v > vmax || (v == vmax && col < varg)) { vmax = v; varg = col; }
+          v[t] = acc[a][t][r] * g.inv_t;
+          vmax = fmaxf(vmax, v[t]);
         }
+        vmax = row16_max(vmax);
+        int varg = 0x7fffffff;
 #pragma unroll
-        for (int o = 1; o < 16; o <<= 1) {
-          const float om = __shfl_xor(vmax, o, kWave);
-          const int oa = __shfl_xor(varg, o, kWave);
-          if (om > vmax || (om == vmax && oa < varg)) { vmax = om; varg = oa; }
-        }
+        for (int t = NT - 1; t >= 0; --t) varg = v[t] == vmax ? strip[t] * 16 + j : varg;   // strips ascend with t
+        varg = row16_min(varg);
         float s = 0.f;
 #pragma unroll
-        for (int t = 0; t < NT; ++t) s += expf(acc[a][t][r] * g.inv_t - vmax);
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) s += __shfl_xor(s, o, kWave);
+        for (int t = 0; t < NT; ++t) s += expf(v[t] - vmax);
+        s = row16_sum(s);
         if (j == 0) {
           float *e = sm + ((wm * 16 * MT + 16 * a + 4 * g4 + r) * WN + wn) * 3;
           e[0] = vmax;
@@ -599,14 +623,10 @@ void launch_stream(const GemmS &g, hipStream_t s) {
 
 template <int EPI>
 void launch_stream_shape(int shape, const GemmS &g, hipStream_t s) {
-  if constexpr (EPI == EPI_STATS) {
-    launch_stream<4, 2, 1, EPI>(g, s);                  // 64 x 128 tiles: one tile-statistics block each
-  } else {
-    switch (shape) {
-      case 0: launch_stream<4, 2, 1, EPI>(g, s); break;    // 64 x 128 tiles
-      case 1: launch_stream<8, 2, 1, EPI>(g, s); break;    // 128 x 128 tiles
-      default: launch_stream<16, 2, 1, EPI>(g, s); break;  // 256 x 128 tiles
-    }
+  switch (shape) {   // every tile is 128 columns wide: one tile-statistics block each
+    case 0: launch_stream<4, 2, 1, EPI>(g, s); break;    // 64 x 128 tiles
+    case 1: launch_stream<8, 2, 1, EPI>(g, s); break;    // 128 x 128 tiles
+    default: launch_stream<16, 2, 1, EPI>(g, s); break;  // 256 x 128 tiles
   }
 }
 }  // namespace
@@ -634,13 +654,13 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
   p.Nw = epi == EPI_SWIGLU ? 2 * N : N;
   p.n_tiles = p.Nw / cols;
   const int target = 256;                           // workgroups that keep every CU streaming
-  // tile statistics (kStatCols = 128 columns per workgroup) take the 64 x 128 tiles.  Past
-  // 256 rows the M tiles already fill the chip, and taller tiles cut the L2 re-reads of
-  // each weight strip (M / BM of them): 256-row tiles, except 128-row ones for outputs of
-  // 128..255 column tiles, whose 256-row launch leaves 2.4 workgroups per CU (measured at
-  // 1024 rows: QKV, O, down and the MTP projection fastest at 256 rows, gate/up at 128).
-  if (epi == EPI_STATS) p.shape = 0;
-  else if (M > 256) p.shape = (p.n_tiles >= 128 && p.n_tiles < target) ? 1 : 2;
+  // Every shape is 128 columns wide, so tile statistics (kStatCols columns per workgroup)
+  // take any of them.  Past 256 rows the M tiles already fill the chip, and taller tiles
+  // cut the L2 re-reads of each weight strip (M / BM of them): 256-row tiles, except
+  // 128-row ones for outputs of 128..255 column tiles, whose 256-row launch leaves 2.4
+  // workgroups per CU (measured at 1024 rows: QKV, O, down and the MTP projection fastest
+  // at 256 rows, gate/up at 128).
+  if (M > 256) p.shape = (p.n_tiles >= 128 && p.n_tiles < target) ? 1 : 2;
   else p.shape = (M > 64 && p.n_tiles >= target) ? (M <= 128 ? 1 : 2) : 0;
   const int BM = p.shape == 2 ? 256 : p.shape == 1 ? 128 : 64;
   const int ITER = 8;                               // k32 steps per unrolled iteration (see kernel)

@@ -130,18 +130,20 @@ def test_qwen_layer_bf16_mtp_sample_logits(qwen_mtp):
     assert ((got >= 0) & (got < shape.vocab)).all()
 
 
-@pytest.mark.parametrize("temperature", [1.0, 0.7])
-def test_qwen_layer_bf16_mtp_sample_draw_from_own_logits(qwen_mtp, temperature):
+@pytest.mark.parametrize("B,temperature,max_ctx", [(64, 1.0, 3000), (64, 0.7, 3000), (96, 1.0, 600), (300, 0.7, 600)])
+def test_qwen_layer_bf16_mtp_sample_draw_from_own_logits(qwen_mtp, B, temperature, max_ctx):
     # Each sampled draft is the inverse-CDF draw from softmax(z / T) of the logits the
     # head itself wrote (Sec. 2.2: drafts are samples of q).  For every row, u * Z must
     # fall in the drawn id's CDF interval [C(x - 1), C(x)) of those logits, widened by
-    # 1e-6 Z for the float32 terms (the window of the float32 large-vocabulary draws).  The LM
-    # head's statistics tiles here are strip ranges of up to 160 ids, so a draw that
-    # reached only part of a tile lands intervals away and fails within a few rows.
+    # 1e-6 Z for the float32 terms (the window of the float32 large-vocabulary draws).  At
+    # 64 rows the LM head's statistics tiles are strip ranges of up to 160 ids; at 96 and
+    # 300 rows they are the 128-id tiles of the 128- and 256-row GEMM tiles (300: two M
+    # tiles, the second ragged).  A draw that reached only part of a tile lands intervals
+    # away and fails within a few rows; the row statistics are checked exactly.
     need_gpu()
     shape, W, Wm = qwen_mtp
     k = 3
-    lens, caches, hidden, n, out, u = _inputs(shape, 64, k, 1, 3000, 6)
+    lens, caches, hidden, n, out, u = _inputs(shape, B, k, 1, max_ctx, 6)
     B = len(lens)
     model, mtp = gm.DeviceModel(shape, W), gm.DeviceMtp(shape, Wm)
     cache = device_cache(shape, caches, lens, 2 * k + 2)
@@ -175,8 +177,8 @@ def test_qwen_layer_bf16_mtp_sample_draw_from_own_logits(qwen_mtp, temperature):
             exact += int(ref == x)
             r = int(np.searchsorted(first, ref // 16, side="right")) - 1
             in_tail += int(ref - 16 * first[r] >= 128)
-    print("[mtp bf16 draw T=%.1f] %d draws, %d identical to the oracle's, %d past the 128th id of their range"
-          % (temperature, B * k, exact, in_tail), flush=True)
+    print("[mtp bf16 draw B=%d T=%.1f] %d draws, %d identical to the oracle's, %d past the 128th id of their range"
+          % (B, temperature, B * k, exact, in_tail), flush=True)
 
 
 def test_f32_mtp_large_vocab_sample():

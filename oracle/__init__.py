@@ -21,7 +21,10 @@ What it computes, and where the paper states it:
   autoregressive decoding, a draft equal to the greedy choice is fully
   accepted, greedy acceptance is the longest argmax-matching prefix, and the
   committed tokens are distributed as the target), by Eq. alpha and by brute
-  force on tiny vocabularies.
+  force on tiny vocabularies.  The top-p variant of the paper's evaluation
+  setting (both distributions truncated to their nucleus) is pinned by the
+  same distribution check on the nucleus of the target, by its reduction to
+  greedy decoding as top_p goes to 0 and by hand-worked nuclei.
 * ``record`` -- the cycle record's verification distributions: the target's
   top-64 log-probabilities per draft position, full-vocabulary normalised,
   in bf16 (App. "Implementing Draft-Path Reconstruction in verl").  Pinned by
@@ -46,7 +49,7 @@ Precision: float64 throughout.  ``Rounding("contract")`` rounds to bfloat16
 exactly the tensors that the bf16 GPU path feeds to its matrix cores (the
 rounding contract), so that integer decisions can be compared bit for bit.
 """
-from .numerics import Rounding, round_bf16, softmax, rmsnorm, silu, rope, inverse_cdf, inverse_cdf_rows  # noqa: F401
+from .numerics import Rounding, round_bf16, softmax, rmsnorm, silu, rope, inverse_cdf, inverse_cdf_rows, nucleus  # noqa: F401
 from .model import attention, layer_forward, verify_forward, full_forward, prefill, ar_decode  # noqa: F401
 from .accept import spec_accept, AcceptResult  # noqa: F401
 from .record import record_topk  # noqa: F401

@@ -25,12 +25,18 @@ Readings where the paper is silent:
 * both p and q are softmax(z / T) with the same temperature T;
 * greedy mode (not used by the paper, whose rollouts sample at T = 1) accepts
   d_i iff d_i is the argmax of the float32 target logits (lowest id on ties)
-  and commits the argmax of row n + 1.
+  and commits the argmax of row n + 1;
+* top-p (the evaluation setting: T = 1, top-p 0.7, rejection sampling, App.
+  "Evaluation Configuration"): every p_i and q_i is replaced by its nucleus
+  (``numerics.nucleus``) before the rule, so the drafts are samples of the
+  truncated head distribution and the committed tokens are distributed as the
+  truncated target; greedy mode ignores top_p (the argmax is always kept).
 
 Flags mark decisions that a correct float32 evaluation could take the other
 way: an examined accept test with |u - min(1, p/q)| < accept_eps, a greedy
-row whose top-2 logit margin is < margin_eps, and a final draw whose target
-u * Z lies within final_eps of an edge of the chosen id's CDF interval.
+row whose top-2 logit margin is < margin_eps, a final draw whose target
+u * Z lies within final_eps of an edge of the chosen id's CDF interval, and a
+nucleus whose boundary lies within nucleus_eps of top_p.
 """
 from __future__ import annotations
 
@@ -39,7 +45,7 @@ from typing import Optional
 
 import numpy as np
 
-from .numerics import softmax, inverse_cdf_rows
+from .numerics import softmax, inverse_cdf_rows, nucleus
 
 
 @dataclasses.dataclass
@@ -61,7 +67,7 @@ def _top2_margin(z: np.ndarray) -> float:
 
 def spec_accept(target_logits, draft_logits, drafts, u_accept, u_final, mode: str = "sample",
                 temperature: float = 1.0, accept_eps: float = 1e-3, margin_eps: float = 1e-2,
-                final_eps: float = 0.0) -> AcceptResult:
+                final_eps: float = 0.0, top_p: float = 1.0, nucleus_eps: float = 0.0) -> AcceptResult:
     """target_logits [B, k+1, V]; draft_logits [B, k, V] (None in greedy mode);
     drafts [B, k]; u_accept [B, k]; u_final [B]."""
     zt = np.asarray(target_logits, dtype=np.float64)
@@ -94,6 +100,12 @@ def spec_accept(target_logits, draft_logits, drafts, u_accept, u_final, mode: st
         zq = np.asarray(draft_logits, dtype=np.float64)
         p = softmax(zt / temperature, axis=-1)                      # [B, k+1, V]
         q = softmax(zq / temperature, axis=-1)                      # [B, k, V]
+        if top_p < 1.0:
+            p, dist_p = nucleus(zt, p, top_p)
+            q, dist_q = nucleus(zq, q, top_p)
+            f_acc |= (dist_p < nucleus_eps).any(axis=-1)
+            if k:
+                f_acc |= (dist_q < nucleus_eps).any(axis=-1)
         alpha = np.minimum(p[:, :k], q).sum(axis=-1)                # Eq. alpha
         rows = np.arange(B)
         alive = np.ones(B, dtype=bool)       # no rejection yet: position i is examined

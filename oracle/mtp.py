@@ -34,7 +34,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from .numerics import Rounding, rmsnorm, softmax, inverse_cdf
+from .numerics import Rounding, rmsnorm, softmax, inverse_cdf, nucleus
 from .model import layer_forward, lm_head
 
 
@@ -58,15 +58,18 @@ def mtp_apply(shape, Wm, W, h: np.ndarray, toks: np.ndarray, pos: np.ndarray,
     return g[0], lm_head(shape, head, g[0], rnd), k[0], v[0]
 
 
-def _draw(z: np.ndarray, u: float, mode: str, temperature: float) -> int:
+def _draw(z: np.ndarray, u: float, mode: str, temperature: float, top_p: float = 1.0) -> int:
     z32 = z.astype(np.float32)
     if mode == "greedy":
         return int(np.argmax(z32))
-    return inverse_cdf(softmax(z32.astype(np.float64) / temperature), u)[0]
+    q = softmax(z32.astype(np.float64) / temperature)
+    if top_p < 1.0:                       # a sample of the head's nucleus (evaluation setting)
+        q = nucleus(z32, q, top_p)[0]
+    return inverse_cdf(q, u)[0]
 
 
 def mtp_draft(shape, Wm, W, cache_k, cache_v, mtp_lens, hidden, n_accept, out_tokens,
-              u_draft, k: int, mode: str, temperature: float, rnd: Rounding):
+              u_draft, k: int, mode: str, temperature: float, rnd: Rounding, top_p: float = 1.0):
     """Draft the next block of every sequence.
 
     cache_k[b] / cache_v[b] [>= mtp_lens[b], n_kv, d]: the head's cache;
@@ -94,7 +97,7 @@ def mtp_draft(shape, Wm, W, cache_k, cache_v, mtp_lens, hidden, n_accept, out_to
         ck, cv = [], []
         for i in range(k):
             dlog[b, i] = z
-            drafts[b, i] = _draw(z, u_draft[b, i], mode, temperature)
+            drafts[b, i] = _draw(z, u_draft[b, i], mode, temperature, top_p)
             if i + 1 < k:
                 slot = m + R + i
                 g1, l1, k1, v1 = mtp_apply(shape, Wm, W, g_prev[None], [drafts[b, i]],

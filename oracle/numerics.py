@@ -99,3 +99,31 @@ def inverse_cdf_rows(w: np.ndarray, u: np.ndarray):
     rows = np.arange(c.shape[0])
     lo = np.where(x > 0, c[rows, np.maximum(x - 1, 0)], 0.0)
     return x, np.minimum(t - lo, c[rows, x] - t), z
+
+
+def nucleus(z: np.ndarray, p: np.ndarray, top_p: float):
+    """Nucleus (top-p) truncation of distributions p [..., V] whose logits are
+    z [..., V] (the order of p is the order of z).
+
+    The kept set of a row is the shortest prefix of its ids ranked by logit
+    (float32, larger first, the lower id first among equal logits) whose total
+    probability reaches top_p: the top-p sampling of the paper's evaluation
+    setting (App. "Evaluation Configuration").  p is restricted to it and
+    renormalised; top_p >= 1 keeps every id.  Returns (p', dist): dist [...] is
+    the distance from top_p to the nearer of the two running sums around the
+    last kept id (before it and with it), used to flag sets that a correct
+    evaluation of the sums in another order could change."""
+    p = np.asarray(p, dtype=np.float64)
+    if top_p >= 1.0:
+        return p / p.sum(axis=-1, keepdims=True), np.full(p.shape[:-1], np.inf)
+    z32 = np.asarray(z, dtype=np.float32).astype(np.float64)
+    order = np.argsort(-z32, axis=-1, kind="stable")         # stable: lower ids first on ties
+    c = np.cumsum(np.take_along_axis(p, order, axis=-1), axis=-1)
+    reach = c >= top_p
+    n = np.where(reach.any(axis=-1), np.argmax(reach, axis=-1), p.shape[-1] - 1)   # last kept rank
+    rank = np.empty_like(order)
+    np.put_along_axis(rank, order, np.arange(p.shape[-1]) + np.zeros_like(order), axis=-1)
+    out = np.where(rank <= n[..., None], p, 0.0)
+    at = np.take_along_axis(c, n[..., None], axis=-1)[..., 0]
+    before = np.where(n > 0, np.take_along_axis(c, np.maximum(n - 1, 0)[..., None], axis=-1)[..., 0], 0.0)
+    return out / out.sum(axis=-1, keepdims=True), np.minimum(np.abs(at - top_p), np.abs(before - top_p))

@@ -54,7 +54,7 @@ def log(msg):
 
 
 # ----------------------------------------------------------------------------- accounting
-def accounting(wl, lens):
+def accounting(wl, lens, top_p=1.0):
     """Algorithmic flops and HBM bytes per step, per kernel name."""
     s, B, k = wl.shape, wl.batch, wl.k
     R, M = k + 1, wl.batch * (k + 1)
@@ -82,7 +82,11 @@ def accounting(wl, lens):
         put("gemm_lm_head", gemm(M, V, H, 4), 1)
     put("attn_verify", (attn_flops, kv_bytes + 2.0 * 2 * M * qd), L)
     # the target rows; the draft rows' statistics come from the draft head when it runs in the step
-    put("accept_row_stats", (0.0, 4.0 * B * ((k + 1) if wl.with_mtp else (2 * k + 1)) * V), 1)
+    # (not under top-p, whose draws produce none)
+    handoff = wl.with_mtp and top_p >= 1.0
+    put("accept_row_stats", (0.0, 4.0 * B * ((k + 1) if handoff else (2 * k + 1)) * V), 1)
+    if top_p < 1.0:   # three passes over every target and draft row (the selection's bins)
+        put("accept_nucleus", (0.0, 3 * 4.0 * B * (2 * k + 1) * V), 1)
     if wl.with_mtp:
         mkv = float((lens.astype(np.float64) * nkv * d * 2 * 2).sum())
         put("mtp_gemm_lm_head", gemm(B, V, H, 4), k)
@@ -93,6 +97,8 @@ def accounting(wl, lens):
         put("mtp_gemm_down", gemm(B, H, F, 4, add=True), k)
         put("attn_mtp", (4.0 * nq * float(lens.sum()) * d * k, mkv), k)
         put("draft_row_stats", (0.0, 4.0 * B * V), k)
+        if top_p < 1.0:
+            put("draft_nucleus", (0.0, 3 * 4.0 * B * V), k)
     return acc
 
 
@@ -100,10 +106,13 @@ def accounting(wl, lens):
 class Step:
     """Device state of one workload and the enqueue of one step."""
 
-    def __init__(self, wl, mode, device="cuda", record=0):
+    def __init__(self, wl, mode, device="cuda", record=0, top_p=1.0):
         import torch
         from paper_2609_16648_amd import gm
         self.torch, self.gm, self.wl = torch, gm, wl
+        # top-p below 1 (sample mode): the accept and the draft work on the nuclei; the
+        # draft then hands no row statistics to the accept
+        self.top_p = top_p
         s, B, k = wl.shape, wl.batch, wl.k
         self.mode = gm.GM_SAMPLE if mode == "sample" else gm.GM_GREEDY
         # the cycle record's top-k log-probabilities per draft position, taken in the accept's pass
@@ -196,17 +205,19 @@ class Step:
         if wl.name == "long_ctx":
             gm.verify_attention(self.cfg, self.cache, 0, self.q, self.attn_out, self.ws_v)
             gm.spec_accept(self.zt, self.zq, self.drafts, self.ua, self.uf, self.n, self.out, self.mode, self.ws_a,
-                           record=self.record)
+                           record=self.record, top_p=self.top_p)
             gm.kv_commit(self.cache, k, self.n, self.slots)
             return
         gm.verify_forward(self.model, self.cache, self.tokens, self.logits, self.hidden, self.ws_v)
+        handoff = wl.with_mtp and self.top_p >= 1.0
         gm.spec_accept(self.logits, self.zq, self.drafts, self.ua, self.uf, self.n, self.out, self.mode, self.ws_a,
-                       draft_stats=self.zq_stats if wl.with_mtp else None, record=self.record)
+                       draft_stats=self.zq_stats if handoff else None, record=self.record, top_p=self.top_p)
         gm.kv_commit(self.cache, k, self.n, self.slots)
         if wl.with_mtp:
             self.mcache.seq_lens.copy_(self.lens0)
             gm.mtp_draft(self.model, self.mtp, self.mcache, k, self.mode, self.hidden, self.n, self.out, self.ud,
-                         self.next_drafts, self.dlog, self.ws_m, draft_stats=self.next_stats)
+                         self.next_drafts, self.dlog, self.ws_m, draft_stats=self.next_stats if handoff else None,
+                         top_p=self.top_p)
 
 
 # ----------------------------------------------------------------------------- DCA loss timing
@@ -250,7 +261,7 @@ def time_dca(wl, N, iters=5):
 
 
 # ----------------------------------------------------------------------------- CPU baseline
-def cpu_baseline(wl, mode, budget_s, weights=None):
+def cpu_baseline(wl, mode, budget_s, weights=None, top_p=1.0):
     """The oracle, as it stands, on a bounded sample of the same workload: the
     same step (verify forward in the rounding-contract mode, accept, commit,
     MTP draft) for the first few sequences."""
@@ -278,7 +289,7 @@ def cpu_baseline(wl, mode, budget_s, weights=None):
             for b in range(nseq):
                 oracle.attention(q[b].astype(np.float64), ks[b].astype(np.float64), vs[b].astype(np.float64),
                                  lens[b] + np.arange(k + 1) + 1)
-            res = oracle.spec_accept(zt, zq_all[:nseq], dr, u_acc[:nseq], u_fin[:nseq])
+            res = oracle.spec_accept(zt, zq_all[:nseq], dr, u_acc[:nseq], u_fin[:nseq], top_p=top_p)
             oracle.kv_commit(lens, res.n_accept, k, np.arange(nseq * 4096).reshape(nseq, 4096), 16)
             return time.perf_counter() - t0, int((res.n_accept + 1).sum())
         caches = [synth.kv_prefix(s, lens, l, seqs=idx) for l in range(s.n_layers)]
@@ -291,12 +302,14 @@ def cpu_baseline(wl, mode, budget_s, weights=None):
         t0 = time.perf_counter()
         logits, hid, _ = oracle.verify_forward(s, W, caches, block, lens, rnd)
         if mode == "sample":
-            res = oracle.spec_accept(logits.astype(np.float32), zq_all[:nseq], dr, u_acc[:nseq], u_fin[:nseq])
+            res = oracle.spec_accept(logits.astype(np.float32), zq_all[:nseq], dr, u_acc[:nseq], u_fin[:nseq],
+                                     top_p=top_p)
         else:
             res = oracle.spec_accept(logits.astype(np.float32), None, dr, None, None, mode="greedy")
         oracle.kv_commit(lens, res.n_accept, k, np.arange(nseq * 4096).reshape(nseq, 4096), 16)
         if wl.with_mtp:
-            oracle.mtp_draft(s, Wm, W, mk, mv, lens, hid, res.n_accept, res.out_tokens, u_dr[:nseq], k, mode, 1.0, rnd)
+            oracle.mtp_draft(s, Wm, W, mk, mv, lens, hid, res.n_accept, res.out_tokens, u_dr[:nseq], k, mode, 1.0, rnd,
+                             top_p=top_p)
         return time.perf_counter() - t0, int((res.n_accept + 1).sum())
 
     # the oracle works in float64: hand it float64 weights once, outside the timed runs
@@ -361,6 +374,8 @@ def main():
                     help="also time the DCA loss forward and gradient over N cycle records of the workload's shape")
     ap.add_argument("--record", type=int, default=0, metavar="K",
                     help="also take the cycle record's top-K log-probabilities in the accept (0: off)")
+    ap.add_argument("--top-p", type=float, default=1.0,
+                    help="top-p of the accept and the draft (the paper's evaluation decodes at 0.7; 1: off)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also time a plain device copy of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -374,7 +389,7 @@ def main():
     gm.lib()
     torch.cuda.set_device(0)
     wl = synth.WORKLOADS[args.workload]
-    step = Step(wl, args.mode, record=args.record)
+    step = Step(wl, args.mode, record=args.record, top_p=args.top_p)
 
     for _ in range(args.warmup):
         step()
@@ -406,7 +421,7 @@ def main():
     committed = int((n + 1).sum())
     value = committed / (ms / 1e3)
 
-    acc = accounting(wl, step.lens)
+    acc = accounting(wl, step.lens, args.top_p)
     kernels = {}
     for name, (launches, tot) in sorted(per_kernel.items(), key=lambda kv: -kv[1][1]):
         ms_step = tot / probe_steps
@@ -473,13 +488,13 @@ def main():
             "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
             "config": {"workload": args.workload, "description": DESCRIPTIONS[args.workload],
                        "batch": wl.batch, "k": wl.k, "accept_mode": args.mode, "parallelism": "none (1 GPU)",
-                       "record_topk": args.record},
+                       "record_topk": args.record, "top_p": args.top_p},
             "roofline": roof, "summary": summary, "kernels": kernels}
     if not args.no_cpu_baseline:
         weights = None
         if hasattr(step, "W"):
             weights = (step.W, step.Wm) if wl.with_mtp else (step.W,)
-        line["cpu_baseline"] = cpu_baseline(wl, args.mode, args.cpu_budget, weights)
+        line["cpu_baseline"] = cpu_baseline(wl, args.mode, args.cpu_budget, weights, args.top_p)
     else:
         line["cpu_baseline"] = None
     for name, row in kernels.items():

@@ -210,6 +210,15 @@ gm_status gm_verify_attention(const gm_model_config *cfg, const gm_kv_cache *cac
  * GM_GREEDY: d_i is accepted iff it is the argmax of target_logits[b][i]
  *   (lowest id on ties); the final token is the argmax of row n.
  *   draft_logits, draft_stats, u_accept and u_final may be NULL.
+ * top_p in (0, 1] (GM_SAMPLE; the evaluation setting of App. "Evaluation
+ *   Configuration" decodes at T = 1, top-p 0.7): below 1, every p_i and q_i is
+ *   replaced by its nucleus before the rule -- the ids ranked by logit (larger
+ *   first, the lower id first among equal logits) up to the first at which the
+ *   running probability reaches top_p, renormalised -- so the drafts must be
+ *   samples of the head's nucleus (gm_mtp_draft with the same top_p).  The
+ *   running masses are exact sums of float64 exponentials rounded to 2^-44 of
+ *   the row maximum's term.  GM_GREEDY ignores top_p; 1 keeps every id.
+ *   GM_ERR_INVALID_ARG outside (0, 1].
  * draft_stats [B][k] (may be NULL; read in GM_SAMPLE mode only): the statistics
  *   of softmax(draft_logits[b][i] / T) at this temperature, as gm_mtp_draft
  *   writes them.  Given, they stand in for a pass over the draft rows; the
@@ -220,7 +229,7 @@ gm_status gm_verify_attention(const gm_model_config *cfg, const gm_kv_cache *cac
  *   pass over the target logits.  GM_ERR_INVALID_ARG if topk is outside 1..min(64, V)
  *   or a record buffer is NULL.
  * The logits rows are read in place; no probability matrix is written. */
-gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature,
+gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature, float top_p,
                          const float *target_logits, const float *draft_logits,
                          const gm_row_stats *draft_stats,
                          const int32_t *draft_tokens, const float *u_accept, const float *u_final,
@@ -252,11 +261,14 @@ gm_status gm_kv_commit(const gm_kv_cache *cache, int B, int k, const int32_t *n_
  * draft_logits [B][k][vocab] float32, and (if draft_stats is not NULL)
  * draft_stats [B][k], the softmax statistics of each draft_logits row at T
  * (the draw's own; gm_spec_accept takes them for the same rows and T).
+ * top_p in (0, 1] (GM_SAMPLE): below 1, each draft is the inverse-CDF draw with
+ * u_draft[b][j] from the nucleus of softmax(z / T) (as in gm_spec_accept);
+ * draft_stats must then be NULL (GM_ERR_UNSUPPORTED otherwise).
  * Errors: GM_ERR_CAPACITY if max_ctx + 2k + 1 > max_pages_per_seq * page_size
- * of the head's cache. */
+ * of the head's cache; GM_ERR_INVALID_ARG for top_p outside (0, 1]. */
 gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weights *mtp,
                        const gm_model_weights *shared, const gm_kv_cache *mtp_cache, int B, int k,
-                       int mode, float temperature, const float *verify_hidden,
+                       int mode, float temperature, float top_p, const float *verify_hidden,
                        const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft,
                        int32_t *drafts, float *draft_logits, gm_row_stats *draft_stats, void *ws,
                        size_t ws_bytes, int32_t *dev_err, void *stream);

@@ -35,7 +35,7 @@ constexpr int kMaxK = 15;
 
 // ---------------------------------------------------------------- workspace plans
 struct AcceptPlan {
-  size_t tstat, dstat, sel, wsum, psum, submax, total;
+  size_t tstat, dstat, sel, wsum, psum, submax, tnuc, dnuc, total;
 };
 AcceptPlan plan_accept(int B, int k, int V) {
   Carve c;
@@ -47,6 +47,8 @@ AcceptPlan plan_accept(int B, int k, int V) {
   p.wsum = c.take(sizeof(double) * (size_t)B * nsc);
   p.psum = c.take(sizeof(double) * (size_t)B * nsc);
   p.submax = c.take(sizeof(float) * (size_t)B * (k + 1) * nch * 64);   // run maxima of the record's selection
+  p.tnuc = c.take(sizeof(NucRow) * (size_t)B * (k + 1));                // top-p nuclei of the target rows
+  p.dnuc = c.take(sizeof(NucRow) * (size_t)B * (k > 0 ? k : 1));        // and of the draft rows
   p.total = c.off;
   return p;
 }
@@ -145,7 +147,8 @@ static_assert(sizeof(gm_row_stats) == sizeof(RowStat) && offsetof(gm_row_stats, 
                   offsetof(gm_row_stats, sum) == offsetof(RowStat, sum),
               "gm_row_stats is the device's RowStat");
 
-extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature, const float *target_logits,
+extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature, float top_p,
+                                    const float *target_logits,
                                     const float *draft_logits, const gm_row_stats *draft_stats,
                                     const int32_t *draft_tokens, const float *u_accept,
                                     const float *u_final, int32_t *n_accept, int32_t *out_tokens,
@@ -154,6 +157,7 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
   if (V > kMaxVocab) return fail(GM_ERR_UNSUPPORTED, "vocab %d exceeds %d", V, kMaxVocab);
   if (mode != GM_GREEDY && mode != GM_SAMPLE) return fail(GM_ERR_INVALID_ARG, "unknown accept mode %d", mode);
   if (!(temperature > 0.f)) return fail(GM_ERR_INVALID_ARG, "temperature must be > 0");
+  if (!(top_p > 0.f && top_p <= 1.f)) return fail(GM_ERR_INVALID_ARG, "top_p must be in (0, 1]");
   if (B == 0) return GM_OK;
   if (!target_logits || !n_accept || !out_tokens) return fail(GM_ERR_INVALID_ARG, "null target_logits / outputs");
   if (k > 0 && !draft_tokens) return fail(GM_ERR_INVALID_ARG, "null draft_tokens");
@@ -187,8 +191,20 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
       launch_row_stats("accept_row_stats", draft_logits, V, B * k, V, inv_t, dstat, s);
     }
   }
-  launch_accept_decide(B, k, V, mode, inv_t, target_logits, draft_logits, tstat, dstat, nch_d, draft_tokens, u_accept,
-                       u_final, n_accept, out_tokens, sel, s);
+  // top-p (sample mode): the nuclei of every target and draft row
+  const double inv_td = 1.0 / (double)temperature;
+  NucRow *tnuc = nullptr, *dnuc = nullptr;
+  if (mode == GM_SAMPLE && top_p < 1.f) {
+    tnuc = (NucRow *)(w + p.tnuc);
+    launch_nucleus("accept_nucleus", B * (k + 1), V, inv_td, (double)top_p, target_logits, V, tstat, stat_chunks(V),
+                   tnuc, s);
+    if (k > 0) {
+      dnuc = (NucRow *)(w + p.dnuc);
+      launch_nucleus("accept_nucleus", B * k, V, inv_td, (double)top_p, draft_logits, V, dstat, nch_d, dnuc, s);
+    }
+  }
+  launch_accept_decide(B, k, V, mode, inv_t, inv_td, target_logits, draft_logits, tstat, dstat, nch_d, tnuc, dnuc,
+                       draft_tokens, u_accept, u_final, n_accept, out_tokens, sel, s);
   if (rec)
     launch_record_topk(B, k, V, inv_t, record->topk, target_logits, tstat, submax, record->logp, record->ids, s);
   if (mode == GM_SAMPLE) launch_residual_draw("accept_residual_chunk", "accept_residual_scan", B, V, inv_t, sel, (double *)(w + p.wsum), (double *)(w + p.psum), s);
@@ -274,7 +290,7 @@ extern "C" gm_status gm_verify_forward(const gm_model_config *cfg, const gm_mode
 // ---------------------------------------------------------------- gm_mtp_draft
 extern "C" gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weights *mtp, const gm_model_weights *shared,
                                   const gm_kv_cache *mtp_cache, int B, int k, int mode, float temperature,
-                                  const float *verify_hidden, const int32_t *n_accept, const int32_t *out_tokens,
+                                  float top_p, const float *verify_hidden, const int32_t *n_accept, const int32_t *out_tokens,
                                   const float *u_draft, int32_t *drafts, float *draft_logits,
                                   gm_row_stats *draft_stats, void *ws, size_t ws_bytes, int32_t *dev_err,
                                   void *stream) {
@@ -283,6 +299,9 @@ extern "C" gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weigh
   if (k < 1) return fail(GM_ERR_INVALID_ARG, "gm_mtp_draft needs k >= 1");
   if (mode != GM_GREEDY && mode != GM_SAMPLE) return fail(GM_ERR_INVALID_ARG, "unknown draft mode %d", mode);
   if (!(temperature > 0.f)) return fail(GM_ERR_INVALID_ARG, "temperature must be > 0");
+  if (!(top_p > 0.f && top_p <= 1.f)) return fail(GM_ERR_INVALID_ARG, "top_p must be in (0, 1]");
+  if (mode == GM_SAMPLE && top_p < 1.f && draft_stats)
+    return fail(GM_ERR_UNSUPPORTED, "draft_stats are not produced with top_p < 1 (pass NULL)");
   if (!mtp || !mtp->norm_h || !mtp->norm_e || !mtp->w_proj || !mtp->final_norm) return fail(GM_ERR_INVALID_ARG, "null MTP weights");
   if ((st = check_layer(cfg, &mtp->layer, "gm_mtp_draft")) != GM_OK) return st;
   if (!shared || !shared->embed || !shared->lm_head) return fail(GM_ERR_INVALID_ARG, "null shared embedding / LM head");
@@ -295,7 +314,9 @@ extern "C" gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weigh
   const MtpPlan p = plan_mtp(*cfg, B, k, mtp_cache->max_ctx);
   st = check_ws(ws, ws_bytes, p.total);
   if (st != GM_OK) return st;
-  run_mtp_draft(*cfg, *mtp, *shared, *mtp_cache, B, k, mode, 1.0f / temperature, verify_hidden, n_accept, out_tokens,
-                u_draft, drafts, draft_logits, (RowStat *)draft_stats, p, (char *)ws, dev_err, (hipStream_t)stream);
+  run_mtp_draft(*cfg, *mtp, *shared, *mtp_cache, B, k, mode, 1.0f / temperature,
+                mode == GM_SAMPLE && top_p < 1.f ? (double)top_p : 1.0, 1.0 / (double)temperature, verify_hidden,
+                n_accept, out_tokens, u_draft, drafts, draft_logits, (RowStat *)draft_stats, p, (char *)ws, dev_err,
+                (hipStream_t)stream);
   return check_launch("gm_mtp_draft");
 }

@@ -141,6 +141,10 @@ MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx) {
   p.attn_ws = c.take(p.attn_ext.total > p.attn_chain.total ? p.attn_ext.total : p.attn_chain.total);
   const int V = cfg.vocab;
   p.stat = c.take(sizeof(RowStat) * (size_t)B * plan_lm_head(cfg.dtype, B, V, cfg.hidden).tiles);
+  p.nuc = c.take(sizeof(NucRow) * (size_t)B);        // top-p draws: nuclei, draws, chunk masses
+  p.sel = c.take(sizeof(RowSel) * (size_t)B);
+  p.wsum = c.take(sizeof(double) * (size_t)B * scan_chunks(V));
+  p.psum = c.take(sizeof(double) * (size_t)B * scan_chunks(V));
   const size_t pe = part_bytes(cfg, (int)Me, true), pb = part_bytes(cfg, B, true);
   p.part = c.take(pe > pb ? pe : pb);
   p.total = c.off;
@@ -152,7 +156,8 @@ MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx) {
 // the first n_b extend rows is needed; the rest of the layer runs on the last
 // row of each sequence (and on the single row of every chain step).
 void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const gm_model_weights &shared,
-                   const gm_kv_cache &c, int B, int k, int mode, float inv_t, const float *verify_hidden,
+                   const gm_kv_cache &c, int B, int k, int mode, float inv_t, double top_p, double inv_td,
+                   const float *verify_hidden,
                    const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft, int32_t *drafts,
                    float *draft_logits, RowStat *draft_stats, const MtpPlan &p, char *ws, int32_t *dev_err,
                    hipStream_t s) {
@@ -179,8 +184,18 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
     // then reads only the tile statistics and one tile of logits per sequence
     launch_gemm("mtp_gemm_lm_head", dt, EPI_STATS, B, V, H, nbuf, H, shared.lm_head, zl, (long)k * V, part, s, tiles,
                 inv_t);
-    launch_tile_draw(B, V, mode, inv_t, zl, (long)k * V, plan_lm_head(dt, B, V, H), tiles, u_draft ? u_draft + j : nullptr,
-                     k, drafts + j, k, draft_stats ? draft_stats + j : nullptr, k, s);
+    const TileGeom geo = plan_lm_head(dt, B, V, H);
+    if (top_p < 1.0) {   // top-p: a draw from each row's nucleus (a selection, then an inverse-CDF scan)
+      NucRow *nuc = (NucRow *)(ws + p.nuc);
+      RowSel *sel = (RowSel *)(ws + p.sel);
+      launch_nucleus("draft_nucleus", B, V, inv_td, top_p, zl, (long)k * V, tiles, geo.tiles, nuc, s);
+      launch_nucleus_select(B, zl, (long)k * V, nuc, u_draft + j, k, drafts + j, k, sel, s);
+      launch_residual_draw("draft_nucleus_chunk", "draft_nucleus_scan", B, V, inv_t, sel, (double *)(ws + p.wsum),
+                           (double *)(ws + p.psum), s);
+    } else {
+      launch_tile_draw(B, V, mode, inv_t, zl, (long)k * V, geo, tiles, u_draft ? u_draft + j : nullptr, k, drafts + j,
+                       k, draft_stats ? draft_stats + j : nullptr, k, s);
+    }
   };
 
   // ---- extend: rows (h_{m+i}, x_{m+i+1}), i = 0..n_b, at slots m_b + i

@@ -123,12 +123,14 @@ void run_verify_forward(const gm_model_config &cfg, const gm_model_weights &w, c
                         int32_t *dev_err, hipStream_t s);
 
 struct MtpPlan {
-  size_t u, x, xg, nbuf, act, qkv, q, attn, attn_g, attn_ws, stat, part, total;
+  size_t u, x, xg, nbuf, act, qkv, q, attn, attn_g, attn_ws, stat, nuc, sel, wsum, psum, part, total;
   AttnPlan attn_ext, attn_chain;
 };
 MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx);
+// top_p < 1 (sample mode): each draft is drawn from the nucleus of its row (inv_td = 1 / T in float64)
 void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const gm_model_weights &shared,
-                   const gm_kv_cache &c, int B, int k, int mode, float inv_t, const float *verify_hidden,
+                   const gm_kv_cache &c, int B, int k, int mode, float inv_t, double top_p, double inv_td,
+                   const float *verify_hidden,
                    const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft, int32_t *drafts,
                    float *draft_logits, RowStat *draft_stats, const MtpPlan &p, char *ws, int32_t *dev_err,
                    hipStream_t s);

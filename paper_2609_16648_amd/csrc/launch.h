@@ -32,6 +32,21 @@ struct RowSel {         // one inverse-CDF draw per sequence
   int32_t *dst;         // where the drawn id goes
   int active;           // 0: nothing to draw for this sequence
   int pad;
+  // top-p: id x of a row is kept iff key(z_x) > key, or key(z_x) == key and x <= id
+  // (key 0 with id INT32_MAX keeps every id); sp / sq are then the nucleus masses
+  uint32_t pkey, qkey;
+  int32_t pid, qid;
+};
+
+// Nucleus (top-p set) of one row of logits: the ids ranked by logit (larger first,
+// the lower id first among equal logits) up to the first at which the running
+// probability reaches top_p.  The kept ids are those whose order key (see
+// order_key in vocab.hip) exceeds `key`, and those equal to it up to id `idt`.
+struct NucRow {
+  double m;             // reference exponent z_ref / T (float64)
+  double s;             // the nucleus mass: sum of exp(z / T - m) over the kept ids
+  uint32_t key;         // order key of the smallest kept logit
+  int32_t idt;          // the largest kept id among the logits with that key
 };
 
 constexpr int kStatThreads = 256;
@@ -86,11 +101,21 @@ constexpr int kRecSub = 256;       // ids per run maximum (one wave's load in th
 constexpr int kRecMaxTopk = 64;
 void launch_record_topk(int B, int k, int V, float inv_t, int topk, const float *logits, const RowStat *tstat,
                         const float *submax, uint16_t *logp, int32_t *ids, hipStream_t s);
-// dstat holds nch_d RowStats per draft row (chunk statistics, or one combined per row)
-void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const float *tlog,
+// dstat holds nch_d RowStats per draft row (chunk statistics, or one combined per row);
+// tnuc / dnuc (top-p, else null): the nuclei of the target and draft rows
+void launch_accept_decide(int B, int k, int V, int mode, float inv_t, double inv_td, const float *tlog,
                           const float *dlog, const RowStat *tstat, const RowStat *dstat, int nch_d,
+                          const NucRow *tnuc, const NucRow *dnuc,
                           const int32_t *drafts, const float *u_accept, const float *u_final,
                           int32_t *n_accept, int32_t *out_tokens, RowSel *sel, hipStream_t s);
+// top-p: the nucleus of rows r = 0..n_rows-1 at logits + r * row_stride, each with nch
+// statistics (chunks or tiles) at st + r * nch; 0 < top_p < 1
+void launch_nucleus(const char *name, int n_rows, int V, double inv_td, double top_p, const float *logits,
+                    long row_stride, const RowStat *st, int nch, NucRow *out, hipStream_t s);
+// sel[b] := a draw from the nucleus nuc[b] of row b (logits + b * row_stride) with the
+// uniform u[b * u_stride], into dst[b * dst_stride]
+void launch_nucleus_select(int B, const float *logits, long row_stride, const NucRow *nuc, const float *u,
+                           int u_stride, int32_t *dst, int dst_stride, RowSel *sel, hipStream_t s);
 void launch_residual_draw(const char *chunk_name, const char *scan_name, int B, int V, float inv_t, const RowSel *sel, double *wsum,
                           double *psum, hipStream_t s);
 

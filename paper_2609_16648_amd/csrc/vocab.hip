@@ -23,6 +23,17 @@
 
 namespace gm {
 
+__device__ __forceinline__ uint32_t order_key(float x) {   // larger float, larger key (-0 as +0)
+  uint32_t u = __float_as_uint(x);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+// top-p: id x with logit z is in the nucleus (key, idt) (NucRow, RowSel)
+__device__ __forceinline__ bool in_nucleus(float z, int x, uint32_t key, int idt) {
+  const uint32_t k = order_key(z);
+  return k > key || (k == key && x <= idt);
+}
+
 // ------------------------------------------------------------------ 1. row statistics
 // submax (may be null): [row][n_chunks * 64] maxima of the raw logits over runs of
 // kRecSub = 256 ids (one wave's float4 load), for the cycle record's selection.
@@ -163,10 +174,13 @@ __device__ __forceinline__ void combine_stats(const RowStat *st, int nch, double
 // test for draft i (all in parallel), and the first failing lane is the first
 // rejection (the rule stops there, so later tests are not looked at).
 __global__ __launch_bounds__(64) void accept_decide_kernel(int B, int k, int V, int mode, float inv_t,
+                                                           double inv_td,
                                                            const float *__restrict__ tlog,
                                                            const float *__restrict__ dlog,
                                                            const RowStat *__restrict__ tstat,
                                                            const RowStat *__restrict__ dstat, int nch, int nch_d,
+                                                           const NucRow *__restrict__ tnuc,
+                                                           const NucRow *__restrict__ dnuc,
                                                            const int32_t *__restrict__ drafts,
                                                            const float *__restrict__ u_acc,
                                                            const float *__restrict__ u_fin,
@@ -178,13 +192,25 @@ __global__ __launch_bounds__(64) void accept_decide_kernel(int B, int k, int V, 
   const bool is_t = lane < k1, is_d = mode != GM_GREEDY && lane >= k1 && lane < k1 + k;
   double M = 0.0, S = 1.0;
   int am = 0;
+  uint32_t nkey = 0;
+  int nid = 0x7fffffff;
   if (is_t || is_d) {
     const RowStat *st = is_t ? tstat + (long)(b * k1 + lane) * nch : dstat + (long)(b * k + lane - k1) * nch_d;
     combine_stats(st, is_t ? nch : nch_d, M, S, am);
+    if (tnuc && mode != GM_GREEDY) {   // top-p: p and q are the rows' nuclei
+      const NucRow nr = is_t ? tnuc[b * k1 + lane] : dnuc[b * k + lane - k1];
+      M = nr.m;
+      S = nr.s;
+      nkey = nr.key;
+      nid = nr.idt;
+    }
   }
+  const bool top_p = tnuc != nullptr && mode != GM_GREEDY;
   // the draft row statistics moved to the lane of the same position
   const double Mq = __shfl(M, k1 + lane < 64 ? k1 + lane : lane, kWave);
   const double Sq = __shfl(S, k1 + lane < 64 ? k1 + lane : lane, kWave);
+  const uint32_t qkey = __shfl(nkey, k1 + lane < 64 ? k1 + lane : lane, kWave);
+  const int qid = __shfl(nid, k1 + lane < 64 ? k1 + lane : lane, kWave);
   bool ok = false;   // lane i < k: draft i passes its test
   int d = -1;
   if (lane < k) {
@@ -192,10 +218,15 @@ __global__ __launch_bounds__(64) void accept_decide_kernel(int B, int k, int V, 
     if (mode == GM_GREEDY) {
       ok = d == am;
     } else if (d >= 0 && d < V) {
-      const double zt = (double)(tlog[(long)(b * k1 + lane) * V + d] * inv_t);
-      const double zq = (double)(dlog[(long)(b * k + lane) * V + d] * inv_t);
-      const double p = exp(zt - M) / S;
-      const double q = exp(zq - Mq) / Sq;
+      const float rt = tlog[(long)(b * k1 + lane) * V + d], rq = dlog[(long)(b * k + lane) * V + d];
+      double p, q;
+      if (top_p) {     // p'(d), q'(d): zero outside the nucleus, exponents in float64
+        p = in_nucleus(rt, d, nkey, nid) ? exp((double)rt * inv_td - M) / S : 0.0;
+        q = in_nucleus(rq, d, qkey, qid) ? exp((double)rq * inv_td - Mq) / Sq : 0.0;
+      } else {
+        p = exp((double)(rt * inv_t) - M) / S;
+        q = exp((double)(rq * inv_t) - Mq) / Sq;
+      }
       const float ratio = q > 0.0 ? (float)(p / q) : INFINITY;
       ok = u_acc[b * k + lane] < ratio;
     }
@@ -205,6 +236,8 @@ __global__ __launch_bounds__(64) void accept_decide_kernel(int B, int k, int V, 
   // lane n holds the statistics of target row n (and of draft row n, n < k)
   const double mp = __shfl(M, n, kWave), sp = __shfl(S, n, kWave);
   const double mq = __shfl(Mq, n, kWave), sq = __shfl(Sq, n, kWave);
+  const uint32_t pkey_n = __shfl(nkey, n, kWave), qkey_n = __shfl(qkey, n, kWave);
+  const int pid_n = __shfl(nid, n, kWave), qid_n = __shfl(qid, n, kWave);
   const int am_n = __shfl(am, n, kWave);
   if (lane < k1) {
     int tok = -1;
@@ -225,11 +258,17 @@ __global__ __launch_bounds__(64) void accept_decide_kernel(int B, int k, int V, 
     rs.sp = sp;
     rs.u = 0.0;
     rs.dst = out_tokens + b * k1 + n;
+    rs.pkey = pkey_n;
+    rs.pid = pid_n;
+    rs.qkey = 0;
+    rs.qid = 0x7fffffff;
     if (mode != GM_GREEDY) {
       if (n < k) {
         rs.q_row = dlog + (long)(b * k + n) * V;
         rs.mq = mq;
         rs.sq = sq;
+        rs.qkey = qkey_n;
+        rs.qid = qid_n;
       }
       rs.u = (double)u_fin[b];
       rs.active = 1;
@@ -238,14 +277,15 @@ __global__ __launch_bounds__(64) void accept_decide_kernel(int B, int k, int V, 
   }
 }
 
-void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const float *tlog,
+void launch_accept_decide(int B, int k, int V, int mode, float inv_t, double inv_td, const float *tlog,
                           const float *dlog, const RowStat *tstat, const RowStat *dstat, int nch_d,
+                          const NucRow *tnuc, const NucRow *dnuc,
                           const int32_t *drafts, const float *u_accept, const float *u_final,
                           int32_t *n_accept, int32_t *out_tokens, RowSel *sel, hipStream_t s) {
   if (B <= 0) return;
   TraceScope ts("accept_decide", s);
-  hipLaunchKernelGGL(accept_decide_kernel, dim3(B), dim3(64), 0, s, B, k, V, mode, inv_t, tlog, dlog, tstat, dstat,
-                     stat_chunks(V), nch_d, drafts, u_accept, u_final, n_accept, out_tokens, sel);
+  hipLaunchKernelGGL(accept_decide_kernel, dim3(B), dim3(64), 0, s, B, k, V, mode, inv_t, inv_td, tlog, dlog, tstat,
+                     dstat, stat_chunks(V), nch_d, tnuc, dnuc, drafts, u_accept, u_final, n_accept, out_tokens, sel);
 }
 
 // ------------------------------------------------------------------ cycle record
@@ -263,11 +303,6 @@ void launch_accept_decide(int B, int k, int V, int mode, float inv_t, const floa
 constexpr int kRecCand = 4096;
 constexpr int kRecMaxRuns = kMaxVocab / kRecSub;
 
-__device__ __forceinline__ uint32_t order_key(float x) {   // larger float, larger key (-0 as +0)
-  uint32_t u = __float_as_uint(x);
-  if (u == 0x80000000u) u = 0u;
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
 __device__ __forceinline__ unsigned long long cand_key(float x, int id) {   // larger logit first, then lower id
   return ((unsigned long long)order_key(x) << 32) | (uint32_t)(0x7fffffff - id);
 }
@@ -478,43 +513,331 @@ void launch_record_topk(int B, int k, int V, float inv_t, int topk, const float 
                      stat_chunks(V), submax, logp, ids);
 }
 
+// ------------------------------------------------------------------ top-p nucleus
+// The evaluation setting of the paper decodes with top-p truncation (App.
+// "Evaluation Configuration"): the kept ids of a row are those ranked by logit
+// (larger first, lower id first among equal logits) up to the first at which the
+// running probability reaches top_p.  One 1024-thread block per row finds the
+// last kept id by a radix selection on the order key of the raw logits, carrying
+// probability mass: each id weighs exp(z / T - m) in float64 (m = z_ref / T of
+// the row's argmax), held as an unsigned fixed-point integer of 2^-44 units, so
+// the LDS histogram sums are exact and independent of the order of the atomic
+// adds.  Three passes over the row bin the key by its top 12 bits, the next 12
+// and the last 8; each pass ranks the bins from the top and keeps the one where
+// the running mass (plus that of every larger key) first reaches top_p times the
+// row's mass.  Ids equal to the boundary logit weigh the same, so the number of
+// them the nucleus needs follows from the masses; only when it keeps some but
+// not all of them does a fourth pass find the id of the last one.
+constexpr int kNucThreads = 1024;
+constexpr int kNucBins = 4096;
+
+// mass of one id in 2^-44 units (the same operations at every call: no contraction)
+__device__ __forceinline__ unsigned long long nuc_mass(float v, double inv_td, double m) {
+#pragma clang fp contract(off)
+  const double y = (double)v * inv_td - m;
+  if (!(y >= -32.0)) return 0ull;          // exp(-32) 2^44 < 0.5: rounds to 0 (and -inf, NaN)
+  return (unsigned long long)rint(exp(y) * 0x1p44);
+}
+
+__device__ __forceinline__ float key_value(uint32_t k) {   // inverse of order_key
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+// exclusive prefix sum of one value per thread over the block; wtot >= 16 entries
+__device__ __forceinline__ unsigned long long block_excl_scan_u64(unsigned long long v, unsigned long long *wtot) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  unsigned long long x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const unsigned long long n = __shfl_up(x, o, kWave);
+    if (lane >= o) x += n;
+  }
+  __syncthreads();
+  if (lane == 63) wtot[wid] = x;
+  __syncthreads();
+  unsigned long long off = 0;
+  for (int w = 0; w < wid && w < nw; ++w) off += wtot[w];
+  return off + x - v;
+}
+
+// The bin, ranking nbins bins from the highest key down, at which the running mass
+// (starting from `above`) first reaches thr; writes it and the mass before it.  The
+// running sums are exact integers, so exactly one bin qualifies when
+// above < thr <= above + the bins' total.
+__device__ void nuc_find_bin(const unsigned long long *hist, int nbins, unsigned long long above, double thr,
+                             unsigned long long *wtot, int *sh_bin, unsigned long long *sh_above) {
+  const int tid = threadIdx.x;
+  const int per = (nbins + kNucThreads - 1) / kNucThreads;
+  unsigned long long g = 0;
+  for (int j = 0; j < per; ++j) {
+    const int b = nbins - 1 - (tid * per + j);
+    if (b >= 0) g += hist[b];
+  }
+  unsigned long long cum = above + block_excl_scan_u64(g, wtot);
+  for (int j = 0; j < per; ++j) {
+    const int b = nbins - 1 - (tid * per + j);
+    if (b < 0) break;
+    const unsigned long long nb = cum + hist[b];
+    if ((double)cum < thr && (double)nb >= thr) {
+      *sh_bin = b;
+      *sh_above = cum;
+    }
+    cum = nb;
+  }
+  __syncthreads();
+}
+
+// f(v, x) for every id x of a row, with four 16-byte loads in flight per thread
+// (rows whose ids are 16-byte aligned), else one float per load, four in flight
+template <typename F>
+__device__ __forceinline__ void nuc_visit(const float *__restrict__ row, int V, bool vec, F &&f) {
+  const int tid = threadIdx.x;
+  if (vec) {
+    constexpr int kStep = kNucThreads * 16;
+    for (int x0 = tid * 4; x0 < V; x0 += kStep) {
+      float4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int x = x0 + u * kNucThreads * 4;
+        v[u] = x < V ? *reinterpret_cast<const float4 *>(row + x) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int x = x0 + u * kNucThreads * 4;
+        if (x < V) {
+          f(v[u].x, x);
+          f(v[u].y, x + 1);
+          f(v[u].z, x + 2);
+          f(v[u].w, x + 3);
+        }
+      }
+    }
+  } else {
+    for (int x0 = tid; x0 < V; x0 += 4 * kNucThreads) {
+      float v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int x = x0 + u * kNucThreads;
+        v[u] = x < V ? row[x] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (x0 + u * kNucThreads < V) f(v[u], x0 + u * kNucThreads);
+    }
+  }
+}
+
+__global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_td, double top_p,
+                                                              const float *__restrict__ logits, long row_stride,
+                                                              const RowStat *__restrict__ st, int nch,
+                                                              NucRow *__restrict__ out) {
+  __shared__ unsigned long long hist[kNucBins];
+  __shared__ unsigned long long wtot[kNucThreads / 64];
+  __shared__ float red_m[kNucThreads / 64];
+  __shared__ int red_a[kNucThreads / 64];
+  __shared__ int sh_bin, sh_idt;
+  __shared__ unsigned long long sh_above;
+  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const float *row = logits + (long)r * row_stride;
+
+  // the reference: the row's maximum (lowest id attaining it) from its statistics
+  float bm = -INFINITY;
+  int ba = 0x7fffffff;
+  for (int c = tid; c < nch; c += kNucThreads) {
+    const RowStat x = st[(long)r * nch + c];
+    if (x.max > bm || (x.max == bm && x.argmax < ba)) {
+      bm = x.max;
+      ba = x.argmax;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float om = __shfl_xor(bm, o, kWave);
+    const int oa = __shfl_xor(ba, o, kWave);
+    if (om > bm || (om == bm && oa < ba)) {
+      bm = om;
+      ba = oa;
+    }
+  }
+  if (lane == 0) {
+    red_m[wid] = bm;
+    red_a[wid] = ba;
+  }
+  for (int b = tid; b < kNucBins; b += kNucThreads) hist[b] = 0ull;
+  __syncthreads();
+  bm = red_m[0];
+  ba = red_a[0];
+  for (int w = 1; w < kNucThreads / 64; ++w)
+    if (red_m[w] > bm || (red_m[w] == bm && red_a[w] < ba)) {
+      bm = red_m[w];
+      ba = red_a[w];
+    }
+  if (ba < 0 || ba >= V) ba = 0;
+  const double m = (double)row[ba] * inv_td;
+
+  // pass 1: the top 12 bits of the key
+  const bool vec = (V & 3) == 0 && (row_stride & 3) == 0 && (reinterpret_cast<uintptr_t>(logits) & 15) == 0;
+  nuc_visit(row, V, vec, [&](float v, int) {
+    const unsigned long long e = nuc_mass(v, inv_td, m);
+    if (e) atomicAdd(&hist[order_key(v) >> 20], e);
+  });
+  __syncthreads();
+  unsigned long long tot = 0;
+  {
+    unsigned long long g = 0;
+    for (int b = tid; b < kNucBins; b += kNucThreads) g += hist[b];
+    tot = block_excl_scan_u64(g, wtot);   // the last thread holds the total of the others
+    tot += g;
+    __syncthreads();
+    if (tid == kNucThreads - 1) sh_above = tot;
+    __syncthreads();
+    tot = sh_above;
+  }
+  if (tot == 0) {           // no mass (every logit -inf or NaN): keep every id
+    if (tid == 0) out[r] = NucRow{m, 0.0, 0u, 0x7fffffff};
+    return;
+  }
+  const double thr = top_p * (double)tot;
+  nuc_find_bin(hist, kNucBins, 0ull, thr, wtot, &sh_bin, &sh_above);
+  const uint32_t b1 = (uint32_t)sh_bin;
+  unsigned long long above = sh_above;
+
+  // pass 2: the next 12 bits, among the ids of bin b1
+  for (int b = tid; b < kNucBins; b += kNucThreads) hist[b] = 0ull;
+  __syncthreads();
+  nuc_visit(row, V, vec, [&](float v, int) {
+    const uint32_t k = order_key(v);
+    if ((k >> 20) == b1) atomicAdd(&hist[(k >> 8) & 0xfffu], nuc_mass(v, inv_td, m));
+  });
+  __syncthreads();
+  nuc_find_bin(hist, kNucBins, above, thr, wtot, &sh_bin, &sh_above);
+  const uint32_t pre = (b1 << 12) | (uint32_t)sh_bin;
+  above = sh_above;
+
+  // pass 3: the last 8 bits
+  for (int b = tid; b < 256; b += kNucThreads) hist[b] = 0ull;
+  __syncthreads();
+  nuc_visit(row, V, vec, [&](float v, int) {
+    const uint32_t k = order_key(v);
+    if ((k >> 8) == pre) atomicAdd(&hist[k & 0xffu], nuc_mass(v, inv_td, m));
+  });
+  __syncthreads();
+  nuc_find_bin(hist, 256, above, thr, wtot, &sh_bin, &sh_above);
+  const uint32_t key = (pre << 8) | (uint32_t)sh_bin;
+  above = sh_above;
+  const unsigned long long hk = hist[sh_bin];          // cnt ids of equal mass et
+  const unsigned long long et = nuc_mass(key_value(key), inv_td, m);
+  const long long cnt = et ? (long long)(hk / et) : 1;
+  // the fewest of them that reach thr (at least one, at most all)
+  long long j = (long long)ceil((thr - (double)above) / (double)et);
+  if (j < 1) j = 1;
+  if (j > cnt) j = cnt;
+  while (j > 1 && (double)(above + (unsigned long long)(j - 1) * et) >= thr) --j;
+  while (j < cnt && (double)(above + (unsigned long long)j * et) < thr) ++j;
+  int idt = 0x7fffffff;
+  if (j < cnt) {
+    // pass 4: the j-th lowest id with this key (contiguous id ranges per thread)
+    if (tid == 0) sh_idt = 0x7fffffff;   // set before the scan's barriers
+    const int per = (V + kNucThreads - 1) / kNucThreads;
+    const int lo = tid * per, hi = min(V, lo + per);
+    unsigned long long c = 0;
+    for (int x = lo; x < hi; ++x) c += order_key(row[x]) == key;
+    const unsigned long long before = block_excl_scan_u64(c, wtot);
+    if (before < (unsigned long long)j && (unsigned long long)j <= before + c) {
+      unsigned long long n = before;
+      for (int x = lo; x < hi; ++x)
+        if (order_key(row[x]) == key && ++n == (unsigned long long)j) {
+          sh_idt = x;
+          break;
+        }
+    }
+    __syncthreads();
+    idt = sh_idt;
+  }
+  if (tid == 0) out[r] = NucRow{m, (double)(above + (unsigned long long)j * et) * 0x1p-44, key, idt};
+}
+
+void launch_nucleus(const char *name, int n_rows, int V, double inv_td, double top_p, const float *logits,
+                    long row_stride, const RowStat *st, int nch, NucRow *out, hipStream_t s) {
+  if (n_rows <= 0) return;
+  TraceScope ts(name, s);
+  hipLaunchKernelGGL(nucleus_kernel, dim3(n_rows), dim3(kNucThreads), 0, s, V, inv_td, top_p, logits, row_stride, st,
+                     nch, out);
+}
+
+__global__ void nucleus_select_kernel(int B, const float *__restrict__ logits, long row_stride,
+                                      const NucRow *__restrict__ nuc, const float *__restrict__ u, int u_stride,
+                                      int32_t *dst, int dst_stride, RowSel *__restrict__ sel) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const NucRow n = nuc[b];
+  RowSel rs;
+  rs.p_row = logits + (long)b * row_stride;
+  rs.q_row = nullptr;
+  rs.mp = n.m;
+  rs.sp = n.s;
+  rs.mq = 0.0;
+  rs.sq = 1.0;
+  rs.u = (double)u[(long)b * u_stride];
+  rs.dst = dst + (long)b * dst_stride;
+  rs.active = 1;
+  rs.pad = 0;
+  rs.pkey = n.key;
+  rs.pid = n.idt;
+  rs.qkey = 0;
+  rs.qid = 0x7fffffff;
+  sel[b] = rs;
+}
+
+void launch_nucleus_select(int B, const float *logits, long row_stride, const NucRow *nuc, const float *u,
+                           int u_stride, int32_t *dst, int dst_stride, RowSel *sel, hipStream_t s) {
+  if (B <= 0) return;
+  hipLaunchKernelGGL(nucleus_select_kernel, dim3((B + 63) / 64), dim3(64), 0, s, B, logits, row_stride, nuc, u,
+                     u_stride, dst, dst_stride, sel);
+}
+
 // ------------------------------------------------------------------ 3. inverse-CDF draw
 // Weight of id x: max(0, p(x) - q(x)) with q, p(x) without.  Each exponential is a
 // float32 expf of z / T - max (both float32); scaling by the float64 normaliser
 // and every sum are float64.
-// z / T - max for kScanPer consecutive ids of one row (float4 loads when the row allows)
-__device__ __forceinline__ void load_run(const float *row, int x0, int V, float inv_t, float mx,
-                                         float (&z)[kScanPer]) {
+// the raw logits of kScanPer consecutive ids of one row (float4 loads when the row
+// allows; -inf past the end)
+__device__ __forceinline__ void load_run(const float *row, int x0, int V, float (&r)[kScanPer]) {
   if ((V & 3) == 0 && x0 + kScanPer <= V) {
 #pragma unroll
     for (int j = 0; j < kScanPer; j += 4) {
       const float4 f = *reinterpret_cast<const float4 *>(row + x0 + j);
-      z[j] = f.x * inv_t - mx;
-      z[j + 1] = f.y * inv_t - mx;
-      z[j + 2] = f.z * inv_t - mx;
-      z[j + 3] = f.w * inv_t - mx;
+      r[j] = f.x;
+      r[j + 1] = f.y;
+      r[j + 2] = f.z;
+      r[j + 3] = f.w;
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < kScanPer; ++j) z[j] = x0 + j < V ? row[x0 + j] * inv_t - mx : -INFINITY;
+    for (int j = 0; j < kScanPer; ++j) r[j] = x0 + j < V ? row[x0 + j] : -INFINITY;
   }
 }
 
-// the kScanPer draw weights of one thread's run (max(0, p - q), or p alone) and their p
+// the kScanPer draw weights of one thread's run (max(0, p - q), or p alone) and their
+// p; under top-p, ids outside a row's nucleus weigh 0 in it
 __device__ __forceinline__ void run_weights(const RowSel &s, int x0, int V, float inv_t, bool use_p, double isp,
                                             double isq, double (&w)[kScanPer], double &psum) {
-  float zp[kScanPer], zq[kScanPer];
-  load_run(s.p_row, x0, V, inv_t, (float)s.mp, zp);
+  float rp[kScanPer], rq[kScanPer];
+  load_run(s.p_row, x0, V, rp);
   const bool with_q = !use_p && s.q_row != nullptr;
-  if (with_q) load_run(s.q_row, x0, V, inv_t, (float)s.mq, zq);
+  if (with_q) load_run(s.q_row, x0, V, rq);
+  const float mp = (float)s.mp, mq = (float)s.mq;
   psum = 0.0;
 #pragma unroll
   for (int j = 0; j < kScanPer; ++j) {
-    const double px = x0 + j < V ? (double)expf(zp[j]) * isp : 0.0;
+    const int x = x0 + j;
+    const bool kp = x < V && in_nucleus(rp[j], x, s.pkey, s.pid);
+    const double px = kp ? (double)expf(rp[j] * inv_t - mp) * isp : 0.0;
     psum += px;
     w[j] = px;
     if (with_q) {
-      const double qx = x0 + j < V ? (double)expf(zq[j]) * isq : 0.0;
+      const bool kq = x < V && in_nucleus(rq[j], x, s.qkey, s.qid);
+      const double qx = kq ? (double)expf(rq[j] * inv_t - mq) * isq : 0.0;
       w[j] = fmax(px - qx, 0.0);
     }
   }

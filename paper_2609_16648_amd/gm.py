@@ -85,13 +85,14 @@ def lib() -> ctypes.CDLL:
     L.gm_verify_attention.argtypes = [P(ModelConfig), P(KVCacheDesc), c_int, c_int, c_int, c_void_p, c_void_p,
                                       c_void_p, c_size_t, c_void_p, c_void_p]
     L.gm_spec_accept.restype = c_int
-    L.gm_spec_accept.argtypes = [c_int, c_int, c_int, c_int, c_float, c_void_p, c_void_p, c_void_p, c_void_p,
-                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
+    L.gm_spec_accept.argtypes = [c_int, c_int, c_int, c_int, c_float, c_float, c_void_p, c_void_p, c_void_p,
+                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
+                                 c_void_p]
     L.gm_kv_commit.restype = c_int
     L.gm_kv_commit.argtypes = [P(KVCacheDesc), c_int, c_int, c_void_p, c_void_p, c_void_p]
     L.gm_mtp_draft.restype = c_int
     L.gm_mtp_draft.argtypes = [P(ModelConfig), P(MtpWeights), P(ModelWeights), P(KVCacheDesc), c_int, c_int,
-                               c_int, c_float, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                               c_int, c_float, c_float, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                c_void_p, c_void_p, c_size_t, c_void_p, c_void_p]
     L.gm_dca_loss.restype = c_int
     L.gm_dca_loss.argtypes = [c_int, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_void_p,
@@ -351,8 +352,9 @@ def decode_row_stats(t: torch.Tensor):
 def spec_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], draft_tokens: torch.Tensor,
                 u_accept: Optional[torch.Tensor], u_final: Optional[torch.Tensor], n_accept: torch.Tensor,
                 out_tokens: torch.Tensor, mode: int, ws: Workspace, temperature: float = 1.0, stream=None,
-                draft_stats: Optional[torch.Tensor] = None, record=None):
-    """record: optional (logp [B, k, topk] bfloat16, ids [B, k, topk] int32) for the cycle record."""
+                draft_stats: Optional[torch.Tensor] = None, record=None, top_p: float = 1.0):
+    """record: optional (logp [B, k, topk] bfloat16, ids [B, k, topk] int32) for the cycle record;
+    top_p < 1: the accept rule on the nuclei of p and q (see gm.h)."""
     B, k1, V = target_logits.shape
     k = k1 - 1
     _need(target_logits, torch.float32, (B, k1, V), "target_logits")
@@ -374,7 +376,8 @@ def spec_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor
     cfg.vocab = V
     n = workspace_size(GM_OP_SPEC_ACCEPT, cfg, B, k, 0)
     buf = ws.get(n)
-    _check(lib().gm_spec_accept(B, k, V, mode, float(temperature), _ptr(target_logits), _ptr(draft_logits),
+    _check(lib().gm_spec_accept(B, k, V, mode, float(temperature), float(top_p), _ptr(target_logits),
+                                _ptr(draft_logits),
                                 _ptr(draft_stats), _ptr(draft_tokens), _ptr(u_accept), _ptr(u_final), _ptr(n_accept),
                                 _ptr(out_tokens), ctypes.byref(rec) if rec is not None else None, _ptr(buf),
                                 buf.numel(), _stream(stream)))
@@ -390,7 +393,8 @@ def mtp_draft(model: DeviceModel, mtp: DeviceMtp, mtp_cache: PagedCache, k: int,
               verify_hidden: torch.Tensor, n_accept: torch.Tensor, out_tokens: torch.Tensor,
               u_draft: Optional[torch.Tensor], drafts: torch.Tensor, draft_logits: torch.Tensor, ws: Workspace,
               temperature: float = 1.0, dev_err: Optional[torch.Tensor] = None, stream=None,
-              draft_stats: Optional[torch.Tensor] = None):
+              draft_stats: Optional[torch.Tensor] = None, top_p: float = 1.0):
+    """top_p < 1 (sample mode): each draft is drawn from its row's nucleus (see gm.h)."""
     B = mtp_cache.B
     s = model.shape
     _need(verify_hidden, torch.float32, (B, k + 1, s.hidden), "verify_hidden")
@@ -402,7 +406,8 @@ def mtp_draft(model: DeviceModel, mtp: DeviceMtp, mtp_cache: PagedCache, k: int,
     n = workspace_size(GM_OP_MTP_DRAFT, model.cfg, B, k, mtp_cache.max_ctx)
     buf = ws.get(n)
     _check(lib().gm_mtp_draft(ctypes.byref(model.cfg), ctypes.byref(mtp.struct), ctypes.byref(model.struct),
-                              ctypes.byref(cs), B, k, mode, float(temperature), _ptr(verify_hidden), _ptr(n_accept),
+                              ctypes.byref(cs), B, k, mode, float(temperature), float(top_p), _ptr(verify_hidden),
+                              _ptr(n_accept),
                               _ptr(out_tokens), _ptr(u_draft), _ptr(drafts), _ptr(draft_logits), _ptr(draft_stats),
                               _ptr(buf),
                               buf.numel(), _ptr(dev_err), _stream(stream)))

@@ -51,16 +51,18 @@ def test_workspace_sizes():
 def test_spec_accept_rejects_bad_arguments():
     L = gm.lib()
     ws = ctypes.c_void_p(1 << 20)
-    args = lambda **kw: dict(dict(B=4, k=3, V=100, mode=gm.GM_SAMPLE, T=1.0, tl=FAKE, dl=FAKE, dt=FAKE, ua=FAKE,
-                                  uf=FAKE, n=FAKE, out=FAKE, ws=ws, nbytes=1 << 30), **kw)
+    args = lambda **kw: dict(dict(B=4, k=3, V=100, mode=gm.GM_SAMPLE, T=1.0, top_p=1.0, tl=FAKE, dl=FAKE, dt=FAKE,
+                                  ua=FAKE, uf=FAKE, n=FAKE, out=FAKE, ws=ws, nbytes=1 << 30), **kw)
 
     def call(a):
-        return L.gm_spec_accept(a["B"], a["k"], a["V"], a["mode"], a["T"], a["tl"], a["dl"], None, a["dt"], a["ua"],
-                                a["uf"], a["n"], a["out"], a.get("rec"), a["ws"], a["nbytes"], None)
+        return L.gm_spec_accept(a["B"], a["k"], a["V"], a["mode"], a["T"], a["top_p"], a["tl"], a["dl"], None, a["dt"],
+                                a["ua"], a["uf"], a["n"], a["out"], a.get("rec"), a["ws"], a["nbytes"], None)
 
     assert call(args(k=16)) == gm.GM_ERR_INVALID_ARG
     assert call(args(mode=7)) == gm.GM_ERR_INVALID_ARG
     assert call(args(T=0.0)) == gm.GM_ERR_INVALID_ARG
+    for bad in (0.0, -0.5, 1.5, float("nan")):
+        assert call(args(top_p=bad)) == gm.GM_ERR_INVALID_ARG and "top_p" in gm.last_error()
     assert call(args(dl=None)) == gm.GM_ERR_INVALID_ARG
     assert "draft_logits" in gm.last_error()
     assert call(args(uf=None)) == gm.GM_ERR_INVALID_ARG
@@ -120,12 +122,20 @@ def test_mtp_and_attention_reject_bad_arguments():
     mtp = gm.MtpWeights(FAKE, FAKE, FAKE, FAKE, gm.LayerWeights(*([FAKE] * 8)))
     c = _FakeCache(1, 100)
     st = L.gm_mtp_draft(ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(c.desc), 4, 3,
-                        gm.GM_SAMPLE, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, None, FAKE, 1 << 30, None, None)
+                        gm.GM_SAMPLE, 1.0, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, None, FAKE, 1 << 30, None, None)
     assert st == gm.GM_ERR_INVALID_ARG and "u_draft" in gm.last_error()
     c2 = _FakeCache(1, 150)                                         # 150 + 2k + 1 > 160
     st = L.gm_mtp_draft(ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(c2.desc), 4, 5,
-                        gm.GM_GREEDY, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, None, FAKE, 1 << 30, None, None)
+                        gm.GM_GREEDY, 1.0, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, None, FAKE, 1 << 30, None, None)
     assert st == gm.GM_ERR_CAPACITY
+    for bad in (0.0, 2.0):
+        st = L.gm_mtp_draft(ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(c.desc), 4, 3,
+                            gm.GM_SAMPLE, 1.0, bad, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None, None)
+        assert st == gm.GM_ERR_INVALID_ARG and "top_p" in gm.last_error()
+    # top-p draws do not produce the row statistics of the accept handoff
+    st = L.gm_mtp_draft(ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(c.desc), 4, 3,
+                        gm.GM_SAMPLE, 1.0, 0.7, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None, None)
+    assert st == gm.GM_ERR_UNSUPPORTED and "draft_stats" in gm.last_error()
     st = L.gm_verify_attention(ctypes.byref(cfg), ctypes.byref(c.desc), 1, 4, 3, FAKE, FAKE, FAKE, 1 << 30, None, None)
     assert st == gm.GM_ERR_INVALID_ARG                              # layer out of range
     st = L.gm_kv_commit(ctypes.byref(c.desc), 4, 3, None, None, None)

@@ -206,3 +206,42 @@ def test_f32_mtp_large_vocab_sample():
     for b in range(B):
         np.testing.assert_array_equal(got[b, :first[b]], ref["drafts"][b, :first[b]])
     assert rel_err(dlog.cpu().numpy()[:, 0], ref["draft_logits"][:, 0]) < 1e-4
+
+
+@pytest.mark.parametrize("B,temperature,top_p", [(64, 1.0, 0.7), (96, 0.7, 0.9)])
+def test_qwen_layer_bf16_mtp_top_p_draw_from_own_logits(qwen_mtp, B, temperature, top_p):
+    # top-p drafting (the evaluation setting): each draft is the inverse-CDF draw from the
+    # nucleus of softmax(z / T) of the logits the head wrote.  u * Z' (Z' the nucleus
+    # mass) must fall in the drawn id's interval of the nucleus's CDF, widened by 1e-6 Z'
+    # for the float32 terms, and the draw equals the oracle's from the same logits unless
+    # the nucleus boundary lies within 1e-9 of top_p
+    need_gpu()
+    shape, W, Wm = qwen_mtp
+    k = 3
+    lens, caches, hidden, n, out, u = _inputs(shape, B, k, 1, 600, 9)
+    model, mtp = gm.DeviceModel(shape, W), gm.DeviceMtp(shape, Wm)
+    cache = device_cache(shape, caches, lens, 2 * k + 2)
+    drafts = torch.zeros((B, k), dtype=torch.int32, device="cuda")
+    dlog = torch.zeros((B, k, shape.vocab), dtype=torch.float32, device="cuda")
+    gm.mtp_draft(model, mtp, cache, k, gm.GM_SAMPLE, t32(hidden), i32(n), i32(out), t32(u), drafts, dlog,
+                 gm.Workspace(), temperature=temperature, top_p=top_p)
+    torch.cuda.synchronize()
+    z = dlog.cpu().numpy()
+    got = drafts.cpu().numpy()
+    exact, flagged = 0, 0
+    for b in range(B):
+        for j in range(k):
+            pn, dist = oracle.nucleus(z[b, j], oracle.softmax(z[b, j].astype(np.float64) / temperature), top_p)
+            if dist < 1e-9:
+                flagged += 1
+                continue
+            x = int(got[b, j])
+            assert pn[x] > 0, (b, j, x)
+            c = np.cumsum(pn)
+            t = float(u[b, j])
+            lo = c[x - 1] if x > 0 else 0.0
+            assert lo - 1e-6 <= t < c[x] + 1e-6, (b, j, x, t - lo, c[x] - t)
+            exact += int(oracle.inverse_cdf(pn, u[b, j])[0] == x)
+    print("[mtp bf16 top-p %.1f B=%d T=%.1f] %d draws, %d identical to the oracle's, %d flagged"
+          % (top_p, B, temperature, B * k, exact, flagged), flush=True)
+    assert exact >= B * k - flagged - 2

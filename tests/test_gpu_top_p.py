@@ -1,0 +1,108 @@
+"""GPU parity of the top-p variant of gm_spec_accept (the evaluation setting of
+App. "Evaluation Configuration": rejection sampling at T = 1, top-p 0.7) against
+the oracle on the same seeded logits.  The drafts are samples of the head's
+nucleus.  Accept counts and committed tokens must match bit for bit outside the
+flag windows (those of the plain rule, plus a nucleus whose boundary lies within
+1e-9 of top_p); the flagged count is printed."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from helpers import need_gpu, t32, i32, flag_report
+from paper_2609_16648_amd import gm
+
+pytestmark = pytest.mark.gpu
+FINAL_EPS = 1e-8
+NUC_EPS = 1e-9
+
+
+def _nucleus_drafts(zq, ud, top_p, temperature):
+    """d_i ~ nucleus(q_i) by the inverse CDF."""
+    B, k, V = zq.shape
+    q = oracle.softmax(zq.astype(np.float64) / temperature)
+    qn = oracle.nucleus(zq, q, top_p)[0]
+    d = np.zeros((B, k), np.int64)
+    for i in range(k):
+        d[:, i] = oracle.inverse_cdf_rows(qn[:, i], ud[:, i])[0]
+    return d
+
+
+def _run(zt, zq, drafts, ua, uf, mode, temperature, top_p):
+    B, k1, V = zt.shape
+    n = torch.zeros(B, dtype=torch.int32, device="cuda")
+    out = torch.zeros((B, k1), dtype=torch.int32, device="cuda")
+    gm.spec_accept(t32(zt), t32(zq) if zq is not None else None, i32(drafts), t32(ua) if ua is not None else None,
+                   t32(uf) if uf is not None else None, n, out, mode, gm.Workspace(), temperature=temperature,
+                   top_p=top_p)
+    torch.cuda.synchronize()
+    return n.cpu().numpy(), out.cpu().numpy()
+
+
+def _logits(shape, kind, *tags):
+    z = synth.normal_logits(shape, 3, *tags)
+    if kind == "ties":          # values on a 0.5 grid: long runs of equal logits at every boundary
+        z = np.round(z * 2.0) / 2.0
+    return z.astype(np.float32)
+
+
+@pytest.mark.parametrize("B,k,V,T,top_p,kind", [
+    (64, 3, 151936, 1.0, 0.7, "normal"),       # the evaluation setting at the layer workload's shape
+    (32, 7, 151936, 0.7, 0.9, "normal"),
+    (257, 2, 1000, 1.0, 0.5, "normal"),        # ragged vocabulary, more sequences than CUs
+    (40, 3, 5000, 1.0, 0.7, "ties"),           # the boundary inside a run of equal logits
+    (8, 1, 4096, 1.3, 0.2, "ties"),
+])
+def test_top_p_accept_matches_oracle(B, k, V, T, top_p, kind):
+    need_gpu()
+    zt = _logits((B, k + 1, V), kind, "tp-t", B, k, V)
+    zq = _logits((B, k, V), kind, "tp-q", B, k, V)
+    ua, uf, ud = synth.uniforms(B, k, 4, "tp", B, k, V)
+    drafts = _nucleus_drafts(zq, ud, top_p, T)
+    ref = oracle.spec_accept(zt, zq, drafts, ua, uf, temperature=T, final_eps=FINAL_EPS, top_p=top_p,
+                             nucleus_eps=NUC_EPS)
+    n, out = _run(zt, zq, drafts, ua, uf, gm.GM_SAMPLE, T, top_p)
+    name = "top-p %.2f T=%.1f B=%d k=%d V=%d %s" % (top_p, T, B, k, V, kind)
+    flag_report(name, ref.flagged, B)
+    ok = ~ref.flagged
+    np.testing.assert_array_equal(n[ok], ref.n_accept[ok])
+    np.testing.assert_array_equal(out[ok], ref.out_tokens[ok])
+    assert ref.flagged.mean() < 0.1
+    # every committed final token lies in the nucleus of its target row (all sequences)
+    p = oracle.softmax(zt.astype(np.float64) / T)
+    for b in range(B):
+        row = oracle.nucleus(zt[b, n[b]], p[b, n[b]], top_p)
+        if row[1] >= NUC_EPS:
+            assert row[0][out[b, n[b]]] > 0, (b, n[b], out[b, n[b]])
+    print("[%s] mean accepted %.2f" % (name, n.mean()), flush=True)
+
+
+def test_top_p_one_is_the_plain_rule():
+    need_gpu()
+    B, k, V = 32, 3, 151936
+    zt = _logits((B, k + 1, V), "normal", "tp1-t")
+    zq = _logits((B, k, V), "normal", "tp1-q")
+    ua, uf, ud = synth.uniforms(B, k, 4, "tp1")
+    drafts = _nucleus_drafts(zq, ud, 1.0, 1.0)
+    a = _run(zt, zq, drafts, ua, uf, gm.GM_SAMPLE, 1.0, 1.0)
+    b = _run(zt, zq, drafts, ua, uf, gm.GM_SAMPLE, 1.0, 0.999999)   # a nucleus of nearly all ids
+    np.testing.assert_array_equal(a[0], b[0])
+
+
+def test_tiny_top_p_is_greedy():
+    # every nucleus is the row's argmax: with drafts = the head's argmax, sampled
+    # acceptance at top_p -> 0 takes the greedy rule's decisions and tokens
+    need_gpu()
+    B, k, V = 48, 3, 151936
+    zt = _logits((B, k + 1, V), "normal", "tp0-t")
+    zq = _logits((B, k, V), "normal", "tp0-q")
+    agree = np.random.default_rng(4).random((B, k)) < 0.6
+    zq[agree] = zt[:, :k][agree]
+    drafts = zq.argmax(-1)
+    ua, uf, _ = synth.uniforms(B, k, 4, "tp0")
+    n, out = _run(zt, zq, drafts, ua, uf, gm.GM_SAMPLE, 1.0, 1e-6)
+    ng, outg = _run(zt, None, drafts, None, None, gm.GM_GREEDY, 1.0, 1.0)
+    np.testing.assert_array_equal(n, ng)
+    np.testing.assert_array_equal(out, outg)
+    assert 0 < n.mean() < k

@@ -527,16 +527,24 @@ void launch_record_topk(int B, int k, int V, float inv_t, int topk, const float 
 // the running mass (plus that of every larger key) first reaches top_p times the
 // row's mass.  Ids equal to the boundary logit weigh the same, so the number of
 // them the nucleus needs follows from the masses; only when it keeps some but
-// not all of them does a fourth pass find the id of the last one.
+// not all of them is the id of the last one looked for.  The second pass only
+// gathers the logits and ids of the boundary's 12-bit bin into LDS; the finer
+// bins and the ties are then taken from there (a bin too large for LDS takes
+// passes over the row instead).
 constexpr int kNucThreads = 1024;
 constexpr int kNucBins = 4096;
+constexpr int kNucQueue = 12288;     // logits and ids of the boundary's 12-bit bin kept in LDS (96 KiB)
+constexpr int kNucTieRank = 2048;    // ties at the boundary ranked in LDS (more: a pass over the row)
 
 // mass of one id in 2^-44 units (the same operations at every call: no contraction)
 __device__ __forceinline__ unsigned long long nuc_mass(float v, double inv_td, double m) {
 #pragma clang fp contract(off)
   const double y = (double)v * inv_td - m;
   if (!(y >= -32.0)) return 0ull;          // exp(-32) 2^44 < 0.5: rounds to 0 (and -inf, NaN)
-  return (unsigned long long)rint(exp(y) * 0x1p44);
+  // exp(y) 2^44 < 2^52: adding 2^52 leaves its nearest integer (ties to even) in the
+  // low mantissa bits
+  const double t = exp(y) * 0x1p44 + 0x1p52;
+  return (unsigned long long)(__double_as_longlong(t) - 0x4330000000000000ll);
 }
 
 __device__ __forceinline__ float key_value(uint32_t k) {   // inverse of order_key
@@ -632,6 +640,9 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
                                                               const RowStat *__restrict__ st, int nch,
                                                               NucRow *__restrict__ out) {
   __shared__ unsigned long long hist[kNucBins];
+  __shared__ float qv[kNucQueue];
+  __shared__ int qx[kNucQueue];
+  __shared__ unsigned sh_qn;
   __shared__ unsigned long long wtot[kNucThreads / 64];
   __shared__ float red_m[kNucThreads / 64];
   __shared__ int red_a[kNucThreads / 64];
@@ -702,13 +713,36 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
   const uint32_t b1 = (uint32_t)sh_bin;
   unsigned long long above = sh_above;
 
-  // pass 2: the next 12 bits, among the ids of bin b1
+  // pass 2: the logits of bin b1 (a few percent of the row) gathered into LDS, so that
+  // the masses of the finer bins are taken by full waves, and the last bits need no
+  // further pass over the row; more than kNucQueue of them (heavy ties, narrow rows of
+  // equal logits) take the two finer passes over the row instead
+  if (tid == 0) sh_qn = 0u;
   for (int b = tid; b < kNucBins; b += kNucThreads) hist[b] = 0ull;
   __syncthreads();
-  nuc_visit(row, V, vec, [&](float v, int) {
-    const uint32_t k = order_key(v);
-    if ((k >> 20) == b1) atomicAdd(&hist[(k >> 8) & 0xfffu], nuc_mass(v, inv_td, m));
+  nuc_visit(row, V, vec, [&](float v, int x) {
+    if ((order_key(v) >> 20) == b1) {
+      const unsigned slot = atomicAdd(&sh_qn, 1u);
+      if (slot < kNucQueue) {
+        qv[slot] = v;
+        qx[slot] = x;
+      }
+    }
   });
+  __syncthreads();
+  const unsigned qn = sh_qn;
+  const bool queued = qn <= (unsigned)kNucQueue;
+  if (queued) {
+    for (unsigned i = tid; i < qn; i += kNucThreads) {
+      const float v = qv[i];
+      atomicAdd(&hist[(order_key(v) >> 8) & 0xfffu], nuc_mass(v, inv_td, m));
+    }
+  } else {
+    nuc_visit(row, V, vec, [&](float v, int) {
+      const uint32_t k = order_key(v);
+      if ((k >> 20) == b1) atomicAdd(&hist[(k >> 8) & 0xfffu], nuc_mass(v, inv_td, m));
+    });
+  }
   __syncthreads();
   nuc_find_bin(hist, kNucBins, above, thr, wtot, &sh_bin, &sh_above);
   const uint32_t pre = (b1 << 12) | (uint32_t)sh_bin;
@@ -717,10 +751,18 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
   // pass 3: the last 8 bits
   for (int b = tid; b < 256; b += kNucThreads) hist[b] = 0ull;
   __syncthreads();
-  nuc_visit(row, V, vec, [&](float v, int) {
-    const uint32_t k = order_key(v);
-    if ((k >> 8) == pre) atomicAdd(&hist[k & 0xffu], nuc_mass(v, inv_td, m));
-  });
+  if (queued) {
+    for (unsigned i = tid; i < qn; i += kNucThreads) {
+      const float v = qv[i];
+      const uint32_t k = order_key(v);
+      if ((k >> 8) == pre) atomicAdd(&hist[k & 0xffu], nuc_mass(v, inv_td, m));
+    }
+  } else {
+    nuc_visit(row, V, vec, [&](float v, int) {
+      const uint32_t k = order_key(v);
+      if ((k >> 8) == pre) atomicAdd(&hist[k & 0xffu], nuc_mass(v, inv_td, m));
+    });
+  }
   __syncthreads();
   nuc_find_bin(hist, 256, above, thr, wtot, &sh_bin, &sh_above);
   const uint32_t key = (pre << 8) | (uint32_t)sh_bin;
@@ -735,7 +777,31 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
   while (j > 1 && (double)(above + (unsigned long long)(j - 1) * et) >= thr) --j;
   while (j < cnt && (double)(above + (unsigned long long)j * et) < thr) ++j;
   int idt = 0x7fffffff;
-  if (j < cnt) {
+  if (j < cnt && queued && cnt <= kNucTieRank) {
+    // the j-th lowest id with this key, from the gathered bin: the ids of the ties are
+    // listed in LDS (the histogram's memory), and the one with j - 1 lower ids is kept
+    int *ties = reinterpret_cast<int *>(hist);
+    if (tid == 0) {
+      sh_qn = 0u;
+      sh_idt = 0x7fffffff;
+    }
+    __syncthreads();
+    for (unsigned i = tid; i < qn; i += kNucThreads)
+      if (order_key(qv[i]) == key) {
+        const unsigned slot = atomicAdd(&sh_qn, 1u);
+        if (slot < (unsigned)kNucTieRank) ties[slot] = qx[i];
+      }
+    __syncthreads();
+    const int nt = (int)min(sh_qn, (unsigned)kNucTieRank);
+    for (int i = tid; i < nt; i += kNucThreads) {
+      const int x = ties[i];
+      int below = 0;
+      for (int i2 = 0; i2 < nt; ++i2) below += ties[i2] < x;
+      if (below == j - 1) sh_idt = x;
+    }
+    __syncthreads();
+    idt = sh_idt;
+  } else if (j < cnt) {
     // pass 4: the j-th lowest id with this key (contiguous id ranges per thread)
     if (tid == 0) sh_idt = 0x7fffffff;   // set before the scan's barriers
     const int per = (V + kNucThreads - 1) / kNucThreads;

@@ -44,6 +44,8 @@ def _logits(shape, kind, *tags):
     z = synth.normal_logits(shape, 3, *tags)
     if kind == "ties":          # values on a 0.5 grid: long runs of equal logits at every boundary
         z = np.round(z * 2.0) / 2.0
+    elif kind == "flat":        # nearly every logit equal: the boundary inside a run of ~10^5 ties
+        z = np.where(synth.stream(3, "flat", *tags).random(shape) < 1e-3, z * 3.0, 0.0)
     return z.astype(np.float32)
 
 
@@ -53,6 +55,7 @@ def _logits(shape, kind, *tags):
     (257, 2, 1000, 1.0, 0.5, "normal"),        # ragged vocabulary, more sequences than CUs
     (40, 3, 5000, 1.0, 0.7, "ties"),           # the boundary inside a run of equal logits
     (8, 1, 4096, 1.3, 0.2, "ties"),
+    (8, 2, 151936, 1.0, 0.5, "flat"),          # too many ties for LDS: the passes over the row
 ])
 def test_top_p_accept_matches_oracle(B, k, V, T, top_p, kind):
     need_gpu()

@@ -35,7 +35,7 @@ constexpr int kMaxK = 15;
 
 // ---------------------------------------------------------------- workspace plans
 struct AcceptPlan {
-  size_t tstat, dstat, sel, wsum, psum, submax, tnuc, dnuc, total;
+  size_t tstat, dstat, sel, wsum, psum, submax, tnuc, dnuc, nucpart, total;
 };
 AcceptPlan plan_accept(int B, int k, int V) {
   Carve c;
@@ -49,6 +49,7 @@ AcceptPlan plan_accept(int B, int k, int V) {
   p.submax = c.take(sizeof(float) * (size_t)B * (k + 1) * nch * 64);   // run maxima of the record's selection
   p.tnuc = c.take(sizeof(NucRow) * (size_t)B * (k + 1));                // top-p nuclei of the target rows
   p.dnuc = c.take(sizeof(NucRow) * (size_t)B * (k > 0 ? k : 1));        // and of the draft rows
+  p.nucpart = c.take(kNucPartBytes);                                    // their split first pass
   p.total = c.off;
   return p;
 }
@@ -196,11 +197,12 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
   NucRow *tnuc = nullptr, *dnuc = nullptr;
   if (mode == GM_SAMPLE && top_p < 1.f) {
     tnuc = (NucRow *)(w + p.tnuc);
+    unsigned long long *part = (unsigned long long *)(w + p.nucpart);
     launch_nucleus("accept_nucleus", B * (k + 1), V, inv_td, (double)top_p, target_logits, V, tstat, stat_chunks(V),
-                   tnuc, s);
+                   tnuc, part, s);
     if (k > 0) {
       dnuc = (NucRow *)(w + p.dnuc);
-      launch_nucleus("accept_nucleus", B * k, V, inv_td, (double)top_p, draft_logits, V, dstat, nch_d, dnuc, s);
+      launch_nucleus("accept_nucleus", B * k, V, inv_td, (double)top_p, draft_logits, V, dstat, nch_d, dnuc, part, s);
     }
   }
   launch_accept_decide(B, k, V, mode, inv_t, inv_td, target_logits, draft_logits, tstat, dstat, nch_d, tnuc, dnuc,

@@ -145,6 +145,7 @@ MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx) {
   p.sel = c.take(sizeof(RowSel) * (size_t)B);
   p.wsum = c.take(sizeof(double) * (size_t)B * scan_chunks(V));
   p.psum = c.take(sizeof(double) * (size_t)B * scan_chunks(V));
+  p.nucpart = c.take(kNucPartBytes);
   const size_t pe = part_bytes(cfg, (int)Me, true), pb = part_bytes(cfg, B, true);
   p.part = c.take(pe > pb ? pe : pb);
   p.total = c.off;
@@ -188,7 +189,8 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
     if (top_p < 1.0) {   // top-p: a draw from each row's nucleus (a selection, then an inverse-CDF scan)
       NucRow *nuc = (NucRow *)(ws + p.nuc);
       RowSel *sel = (RowSel *)(ws + p.sel);
-      launch_nucleus("draft_nucleus", B, V, inv_td, top_p, zl, (long)k * V, tiles, geo.tiles, nuc, s);
+      launch_nucleus("draft_nucleus", B, V, inv_td, top_p, zl, (long)k * V, tiles, geo.tiles, nuc,
+                     (unsigned long long *)(ws + p.nucpart), s);
       launch_nucleus_select(B, zl, (long)k * V, nuc, u_draft + j, k, drafts + j, k, sel, s);
       launch_residual_draw("draft_nucleus_chunk", "draft_nucleus_scan", B, V, inv_t, sel, (double *)(ws + p.wsum),
                            (double *)(ws + p.psum), s);

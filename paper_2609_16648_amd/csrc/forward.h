@@ -123,7 +123,7 @@ void run_verify_forward(const gm_model_config &cfg, const gm_model_weights &w, c
                         int32_t *dev_err, hipStream_t s);
 
 struct MtpPlan {
-  size_t u, x, xg, nbuf, act, qkv, q, attn, attn_g, attn_ws, stat, nuc, sel, wsum, psum, part, total;
+  size_t u, x, xg, nbuf, act, qkv, q, attn, attn_g, attn_ws, stat, nuc, sel, wsum, psum, nucpart, part, total;
   AttnPlan attn_ext, attn_chain;
 };
 MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx);

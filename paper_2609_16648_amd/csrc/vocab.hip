@@ -635,27 +635,16 @@ __device__ __forceinline__ void nuc_visit(const float *__restrict__ row, int V, 
   }
 }
 
-__global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_td, double top_p,
-                                                              const float *__restrict__ logits, long row_stride,
-                                                              const RowStat *__restrict__ st, int nch,
-                                                              NucRow *__restrict__ out) {
-  __shared__ unsigned long long hist[kNucBins];
-  __shared__ float qv[kNucQueue];
-  __shared__ int qx[kNucQueue];
-  __shared__ unsigned sh_qn;
-  __shared__ unsigned long long wtot[kNucThreads / 64];
-  __shared__ float red_m[kNucThreads / 64];
-  __shared__ int red_a[kNucThreads / 64];
-  __shared__ int sh_bin, sh_idt;
-  __shared__ unsigned long long sh_above;
-  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const float *row = logits + (long)r * row_stride;
-
-  // the reference: the row's maximum (lowest id attaining it) from its statistics
+// The reference exponent of a row: z / T (float64) of its maximum, the lowest id
+// attaining the largest statistic among its nch chunk or tile statistics.  Holds a
+// barrier: the caller's LDS writes before it are visible to the block after it.
+__device__ double nuc_reference(const float *__restrict__ row, const RowStat *__restrict__ st, int nch, int V,
+                                double inv_td, float *red_m, int *red_a) {
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   float bm = -INFINITY;
   int ba = 0x7fffffff;
   for (int c = tid; c < nch; c += kNucThreads) {
-    const RowStat x = st[(long)r * nch + c];
+    const RowStat x = st[c];
     if (x.max > bm || (x.max == bm && x.argmax < ba)) {
       bm = x.max;
       ba = x.argmax;
@@ -674,7 +663,6 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
     red_m[wid] = bm;
     red_a[wid] = ba;
   }
-  for (int b = tid; b < kNucBins; b += kNucThreads) hist[b] = 0ull;
   __syncthreads();
   bm = red_m[0];
   ba = red_a[0];
@@ -684,14 +672,70 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
       ba = red_a[w];
     }
   if (ba < 0 || ba >= V) ba = 0;
-  const double m = (double)row[ba] * inv_td;
+  return (double)row[ba] * inv_td;
+}
 
-  // pass 1: the top 12 bits of the key
+// Pass 1 of the selection split over S workgroups per row, for launches with too
+// few rows to fill the chip: workgroup (r, s) writes the histogram of its slice of
+// row r (ids [lo, hi), lo and hi multiples of 4) to part[(r S + s) kNucBins ...];
+// the selection sums the S of them (exact integers: the same result as one pass).
+__global__ __launch_bounds__(kNucThreads) void nucleus_hist_kernel(int V, double inv_td,
+                                                                   const float *__restrict__ logits, long row_stride,
+                                                                   const RowStat *__restrict__ st, int nch, int S,
+                                                                   unsigned long long *__restrict__ part) {
+  __shared__ unsigned long long hist[kNucBins];
+  __shared__ float red_m[kNucThreads / 64];
+  __shared__ int red_a[kNucThreads / 64];
+  const int r = blockIdx.x / S, sg = blockIdx.x % S, tid = threadIdx.x;
+  const float *row = logits + (long)r * row_stride;
+  for (int b = tid; b < kNucBins; b += kNucThreads) hist[b] = 0ull;
+  const double m = nuc_reference(row, st + (long)r * nch, nch, V, inv_td, red_m, red_a);
+  const int lo = (int)(((long)V * sg / S) & ~3l), hi = sg + 1 == S ? V : (int)(((long)V * (sg + 1) / S) & ~3l);
   const bool vec = (V & 3) == 0 && (row_stride & 3) == 0 && (reinterpret_cast<uintptr_t>(logits) & 15) == 0;
-  nuc_visit(row, V, vec, [&](float v, int) {
+  nuc_visit(row + lo, hi - lo, vec, [&](float v, int) {
     const unsigned long long e = nuc_mass(v, inv_td, m);
     if (e) atomicAdd(&hist[order_key(v) >> 20], e);
   });
+  __syncthreads();
+  unsigned long long *dst = part + ((long)r * S + sg) * kNucBins;
+  for (int b = tid; b < kNucBins; b += kNucThreads) dst[b] = hist[b];
+}
+
+__global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_td, double top_p,
+                                                              const float *__restrict__ logits, long row_stride,
+                                                              const RowStat *__restrict__ st, int nch,
+                                                              const unsigned long long *__restrict__ part, int S,
+                                                              NucRow *__restrict__ out) {
+  __shared__ unsigned long long hist[kNucBins];
+  __shared__ float qv[kNucQueue];
+  __shared__ int qx[kNucQueue];
+  __shared__ unsigned sh_qn;
+  __shared__ unsigned long long wtot[kNucThreads / 64];
+  __shared__ float red_m[kNucThreads / 64];
+  __shared__ int red_a[kNucThreads / 64];
+  __shared__ int sh_bin, sh_idt;
+  __shared__ unsigned long long sh_above;
+  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const float *row = logits + (long)r * row_stride;
+
+  for (int b = tid; b < kNucBins; b += kNucThreads) hist[b] = 0ull;
+  const double m = nuc_reference(row, st + (long)r * nch, nch, V, inv_td, red_m, red_a);
+
+  // pass 1: the top 12 bits of the key (or the sum of the S slices' histograms)
+  const bool vec = (V & 3) == 0 && (row_stride & 3) == 0 && (reinterpret_cast<uintptr_t>(logits) & 15) == 0;
+  if (part) {
+    const unsigned long long *src = part + (long)r * S * kNucBins;
+    for (int b = tid; b < kNucBins; b += kNucThreads) {
+      unsigned long long t = 0;
+      for (int sg = 0; sg < S; ++sg) t += src[(long)sg * kNucBins + b];
+      hist[b] = t;
+    }
+  } else {
+    nuc_visit(row, V, vec, [&](float v, int) {
+      const unsigned long long e = nuc_mass(v, inv_td, m);
+      if (e) atomicAdd(&hist[order_key(v) >> 20], e);
+    });
+  }
   __syncthreads();
   unsigned long long tot = 0;
   {
@@ -824,11 +868,19 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
 }
 
 void launch_nucleus(const char *name, int n_rows, int V, double inv_td, double top_p, const float *logits,
-                    long row_stride, const RowStat *st, int nch, NucRow *out, hipStream_t s) {
+                    long row_stride, const RowStat *st, int nch, NucRow *out, unsigned long long *part,
+                    hipStream_t s) {
   if (n_rows <= 0) return;
   TraceScope ts(name, s);
+  // fewer than 128 rows leave CUs idle: their first pass is split over up to 8 workgroups per row
+  int S = part ? kNucSplitRows / n_rows : 1;
+  if (S > kNucMaxSplit) S = kNucMaxSplit;
+  if (S < 2 || V < S * 4096) S = 1;
+  if (S > 1)
+    hipLaunchKernelGGL(nucleus_hist_kernel, dim3(n_rows * S), dim3(kNucThreads), 0, s, V, inv_td, logits, row_stride,
+                       st, nch, S, part);
   hipLaunchKernelGGL(nucleus_kernel, dim3(n_rows), dim3(kNucThreads), 0, s, V, inv_td, top_p, logits, row_stride, st,
-                     nch, out);
+                     nch, S > 1 ? part : nullptr, S, out);
 }
 
 __global__ void nucleus_select_kernel(int B, const float *__restrict__ logits, long row_stride,

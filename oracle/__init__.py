@@ -39,8 +39,11 @@ What it computes, and where the paper states it:
 * ``kv``     -- commit/rollback of the KV index (Sec. 2.2; App. "Train--Inference
   Inconsistency under Teacher Forcing", Eq. tf-restart-kv).  Closed form.
 * ``mtp``    -- the recurrent MTP draft head (Sec. 2.2; App. "Models and Draft
-  Heads"; Eqs. tf-restart and tf-restart-kv).  Pinned by the pass-through
-  special cases; beyond them the head's composition is described only in
+  Heads"; Eqs. tf-restart and tf-restart-kv), and the draft-path
+  reconstruction that re-runs recorded chains with the recorded drafts as
+  inputs (App. "Draft-Path Reconstruction").  Pinned by the pass-through
+  special cases and by the reconstruction reproducing the drafting's own
+  distributions; beyond them the head's composition is described only in
   prose, so its parity is "parity unpinned" past those cases.
 * ``mixing`` -- the draft construction of the top-1 mixing workloads (an input
   recipe, not part of the method).
@@ -55,5 +58,5 @@ from .accept import spec_accept, AcceptResult  # noqa: F401
 from .record import record_topk  # noqa: F401
 from .dca import dca_loss  # noqa: F401
 from .kv import kv_commit  # noqa: F401
-from .mtp import mtp_apply, mtp_draft  # noqa: F401
+from .mtp import mtp_apply, mtp_draft, mtp_reconstruct  # noqa: F401
 from .mixing import mixing_drafts  # noqa: F401

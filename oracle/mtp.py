@@ -27,8 +27,18 @@ step accepted n drafts and drew the final token f, the extend rows are
 output g_1 gives q_1 and the first new draft; chain step i feeds
 (g_{i-1}, d'_{i-1}) at slot m+n+i-1.  The committed length becomes m+n+1.
 
+Draft-path reconstruction (App. "Draft-Path Reconstruction"; "Parallelizing
+GrowMTP Training"): the training side re-runs the chain of every recorded cycle
+with the recorded drafts as inputs and nothing sampled.  A cycle that starts
+with s committed head entries (slot s holds its first row, the pair of the
+boundary hidden and the last committed token) is rebuilt from those s entries
+alone: depth 1 feeds the recorded start pair at slot s, depth j feeds
+(g_{j-1}, d_{j-1}) at slot s + j - 1, each rotated at its slot + 1, and every
+depth sees only the prefix and its own chain's earlier entries.
+
 Parity beyond the pass-through special cases in the tests is unpinned: the
-paper describes the head's composition in prose only.
+paper describes the head's composition in prose only.  The reconstruction is
+further pinned by reproducing the drafting's own distributions.
 """
 from __future__ import annotations
 
@@ -111,3 +121,35 @@ def mtp_draft(shape, Wm, W, cache_k, cache_v, mtp_lens, hidden, n_accept, out_to
         new_lens[b] = m + R
     return dict(drafts=drafts, draft_logits=dlog, new_lens=new_lens,
                 ext_k=ext_k, ext_v=ext_v, chain_k=ch_k, chain_v=ch_v)
+
+
+def mtp_reconstruct(shape, Wm, W, cache_k, cache_v, starts, start_hidden, start_tokens, drafts, K: int,
+                    rnd: Rounding):
+    """Reconstruct the head's distributions along recorded draft paths.
+
+    For cycle r: cache_k[r] / cache_v[r] [>= starts[r], n_kv, d] hold the head's
+    committed entries (the first starts[r] are visible); start_hidden [R, H] and
+    start_tokens [R] are the recorded start pair; drafts [R, >= K-1] the recorded
+    drafts, fed back in order (d_1 .. d_{K-1}).  Returns dict(logits [R, K, V] --
+    the head logits whose softmax is q_{r,k} -- and chain_k / chain_v [R][K, n_kv, d],
+    the entries the chain writes at slots starts[r] .. starts[r] + K - 1)."""
+    R = len(starts)
+    V = np.asarray(W["lm_head"]).shape[0]
+    logits = np.zeros((R, K, V))
+    ck, cv = [], []
+    for r in range(R):
+        s = int(starts[r])
+        kc, vc = _f64(cache_k[r][:s]), _f64(cache_v[r][:s])
+        h, t = _f64(start_hidden[r]), int(start_tokens[r])
+        ks, vs = [], []
+        for j in range(K):
+            g, lg, k1, v1 = mtp_apply(shape, Wm, W, h[None], [t], [s + j + 1], kc, vc, rnd)
+            logits[r, j] = lg[0]
+            kc, vc = np.concatenate([kc, k1]), np.concatenate([vc, v1])
+            ks.append(k1[0])
+            vs.append(v1[0])
+            if j + 1 < K:
+                h, t = g[0], int(drafts[r][j])
+        ck.append(np.array(ks))
+        cv.append(np.array(vs))
+    return dict(logits=logits, chain_k=ck, chain_v=cv)

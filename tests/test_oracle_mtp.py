@@ -117,3 +117,79 @@ def test_stale_cache_beyond_length_is_ignored():
         ck2[b][m:] = 1e3
     b_ = oracle.mtp_draft(SHAPE, Wm, W, ck2, cv, lens, hidden, n, out, u, 3, "sample", 1.0, EXACT)
     np.testing.assert_array_equal(a["draft_logits"], b_["draft_logits"])
+
+
+# ------------------------------------------------------------------ draft-path reconstruction
+def _reconstruct_inputs(r, lens, ck, cv, hidden, n, out):
+    """The record of the cycles mtp_draft just drafted: each starts with the committed
+    entries before the boundary row (the head's old entries and extend rows 0..n-1),
+    from the boundary hidden and the cycle's final token."""
+    B = len(lens)
+    starts = np.array([int(lens[b]) + int(n[b]) for b in range(B)])
+    pk = [np.concatenate([ck[b][:lens[b]], r["ext_k"][b][:n[b]]]) for b in range(B)]
+    pv = [np.concatenate([cv[b][:lens[b]], r["ext_v"][b][:n[b]]]) for b in range(B)]
+    return starts, pk, pv, hidden[np.arange(B), n], out[np.arange(B), n]
+
+
+def test_reconstruction_reproduces_the_drafting():
+    # Fed the recorded drafts from the recorded start, every depth sees the context the
+    # drafting saw (App. "Draft-Path Reconstruction": the drafts turn from outputs into
+    # inputs; the start state is the one drafting consumed), so the reconstructed head
+    # logits are the draft logits and the chain rewrites the same cache entries
+    shape = SHAPE
+    W = synth.model_weights(shape, 5)
+    Wm = synth.mtp_weights(shape, 5)
+    k = 4
+    for mode in ("sample", "greedy"):
+        lens, ck, cv, hidden, n, out, u = _inputs(5, B=5, k=k)
+        r = oracle.mtp_draft(shape, Wm, W, ck, cv, lens, hidden, n, out, u, k, mode, 1.0, EXACT)
+        starts, pk, pv, h0, t0 = _reconstruct_inputs(r, lens, ck, cv, hidden, n, out)
+        rec = oracle.mtp_reconstruct(shape, Wm, W, pk, pv, starts, h0, t0, r["drafts"], k, EXACT)
+        np.testing.assert_allclose(rec["logits"], r["draft_logits"], rtol=1e-12, atol=1e-12)
+        for b in range(len(lens)):
+            np.testing.assert_allclose(rec["chain_k"][b][0], r["ext_k"][b][n[b]], atol=1e-12)   # the boundary row
+            np.testing.assert_allclose(rec["chain_k"][b][1:], r["chain_k"][b], atol=1e-12)
+
+
+def test_reconstruction_feeds_the_recorded_drafts_in_order():
+    # embedding path (W_proj = [0 | I], zero layer): depth 1 reads the start token, depth
+    # j the recorded draft d_{j-1}, whatever the head itself would have drawn
+    W, Wm = _setup(6, "embed")
+    K, R = 4, 3
+    g = np.random.default_rng(6)
+    starts = g.integers(1, 7, R)
+    ck = [g.standard_normal((s + K, SHAPE.n_kv_heads, SHAPE.head_dim)) for s in starts]
+    drafts = g.integers(0, SHAPE.vocab, (R, K))
+    t0 = g.integers(0, SHAPE.vocab, R)
+    rec = oracle.mtp_reconstruct(SHAPE, Wm, W, ck, ck, starts, g.standard_normal((R, SHAPE.hidden)), t0, drafts, K,
+                                 EXACT)
+    E, L = W["embed"].astype(np.float64), W["lm_head"].astype(np.float64)
+    head = lambda t: _rms(_rms(E[t], Wm["norm_e"]), Wm["final_norm"]) @ L.T
+    for r_ in range(R):
+        fed = [t0[r_]] + list(drafts[r_, :K - 1])
+        for j in range(K):
+            np.testing.assert_allclose(rec["logits"][r_, j], head(fed[j]), rtol=1e-12, atol=1e-12)
+
+
+def test_reconstructed_cycles_are_independent():
+    # chains share only recorded inputs: a cycle's result does not depend on the others
+    # in the batch (App. "Parallelizing GrowMTP Training"), nor on entries past its start
+    shape = SHAPE
+    W = synth.model_weights(shape, 7)
+    Wm = synth.mtp_weights(shape, 7)
+    K, R = 3, 4
+    g = np.random.default_rng(7)
+    starts = g.integers(2, 9, R)
+    ck = [g.standard_normal((s + 5, shape.n_kv_heads, shape.head_dim)) for s in starts]
+    cv = [g.standard_normal((s + 5, shape.n_kv_heads, shape.head_dim)) for s in starts]
+    h0 = g.standard_normal((R, shape.hidden))
+    t0 = g.integers(0, shape.vocab, R)
+    drafts = g.integers(0, shape.vocab, (R, K))
+    full = oracle.mtp_reconstruct(shape, Wm, W, ck, cv, starts, h0, t0, drafts, K, EXACT)
+    ck2 = [c.copy() for c in ck]
+    for r_, s in enumerate(starts):
+        ck2[r_][s:] = 1e3
+    for r_ in (2, 0):
+        one = oracle.mtp_reconstruct(shape, Wm, W, ck2[r_:r_ + 1], cv[r_:r_ + 1], starts[r_:r_ + 1], h0[r_:r_ + 1],
+                                     t0[r_:r_ + 1], drafts[r_:r_ + 1], K, EXACT)
+        np.testing.assert_array_equal(one["logits"][0], full["logits"][r_])

@@ -60,7 +60,8 @@ typedef enum {
   GM_OP_VERIFY_ATTENTION = 1,
   GM_OP_SPEC_ACCEPT = 2,
   GM_OP_MTP_DRAFT = 3,
-  GM_OP_DCA_LOSS = 4     /* B = cycles N, k = draft length K, cfg->vocab = V */
+  GM_OP_DCA_LOSS = 4,    /* B = cycles N, k = draft length K, cfg->vocab = V */
+  GM_OP_MTP_RECONSTRUCT = 5   /* B = cycles R, k = depth K, max_ctx = the cache's max_ctx */
 } gm_op;
 
 /* Decoder shape: pre-norm RMSNorm / RoPE (rotate-half, angle pos * base^(-2i/d))
@@ -272,6 +273,29 @@ gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weights *mtp,
                        const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft,
                        int32_t *drafts, float *draft_logits, gm_row_stats *draft_stats, void *ws,
                        size_t ws_bytes, int32_t *dev_err, void *stream);
+
+/* Draft-path reconstruction (App. "Draft-Path Reconstruction"; App. "Parallelizing
+ * GrowMTP Training"): the head's chain of each of R recorded cycles re-run under the
+ * current head weights with the recorded drafts as inputs and nothing sampled, as K
+ * batched single-row steps (one per depth, all cycles together).  mtp_cache is a
+ * one-layer cache with one block table row per cycle; seq_lens[r] = s_r, the number of
+ * committed head entries the cycle sees (slot s holds the pair (h_s, x_{s+1}) rotated
+ * at position s+1, as gm_mtp_draft writes them).  Depth 1 feeds (start_hidden[r],
+ * start_tokens[r]) -- the boundary hidden and the last committed token the cycle
+ * started from -- at slot s_r; depth j >= 2 feeds (its layer output at depth j-1,
+ * drafts[r][j-2]) at slot s_r + j - 1.  Depth j attends to slots 0 .. s_r + j - 1 of the
+ * cycle's own table: causal over the committed prefix, its own chain's entries (the
+ * diagonal mask of the batched form).  The entries at slots s_r .. s_r + K - 1 are
+ * written, so those pages must be the cycle's own (cycles may share the pages of their
+ * prefix).  seq_lens is not changed.
+ * start_hidden [R][H] float32; start_tokens [R]; drafts [R][K] (d_1..d_{K-1} are read;
+ * may be NULL when K = 1); head_logits [R][K][vocab] float32: row j is the head's
+ * logits at depth j+1 (q_{r,j+1} = softmax of it), the input of gm_dca_loss.
+ * Errors: GM_ERR_CAPACITY if max_ctx + K > max_pages_per_seq * page_size. */
+gm_status gm_mtp_reconstruct(const gm_model_config *cfg, const gm_mtp_weights *mtp,
+                             const gm_model_weights *shared, const gm_kv_cache *mtp_cache, int R, int K,
+                             const float *start_hidden, const int32_t *start_tokens, const int32_t *drafts,
+                             float *head_logits, void *ws, size_t ws_bytes, int32_t *dev_err, void *stream);
 
 /* Depth-coupled acceptance loss with verify-gated masking, and its gradient in
  * the head logits (Sec. "The Depth-Coupled Acceptance Loss" and "Learning up to

@@ -134,6 +134,9 @@ extern "C" size_t gm_workspace_size(int op, const gm_model_config *cfg, int B, i
     case GM_OP_MTP_DRAFT:
       if (check_config(cfg, B, k) != GM_OK) return 0;
       return plan_mtp(*cfg, B, k, max_ctx).total;
+    case GM_OP_MTP_RECONSTRUCT:
+      if (k < 1 || check_config(cfg, B, k) != GM_OK) return 0;
+      return plan_mtp(*cfg, B, k, max_ctx).total;
     case GM_OP_DCA_LOSS:
       if (B < 0 || k < 1 || k > kMaxK || cfg->vocab < 1 || cfg->vocab > kMaxVocab) return 0;
       return dca_workspace(B, k, cfg->vocab);
@@ -321,4 +324,29 @@ extern "C" gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weigh
                 n_accept, out_tokens, u_draft, drafts, draft_logits, (RowStat *)draft_stats, p, (char *)ws, dev_err,
                 (hipStream_t)stream);
   return check_launch("gm_mtp_draft");
+}
+
+// ---------------------------------------------------------------- gm_mtp_reconstruct
+extern "C" gm_status gm_mtp_reconstruct(const gm_model_config *cfg, const gm_mtp_weights *mtp,
+                                        const gm_model_weights *shared, const gm_kv_cache *mtp_cache, int R, int K,
+                                        const float *start_hidden, const int32_t *start_tokens,
+                                        const int32_t *drafts, float *head_logits, void *ws, size_t ws_bytes,
+                                        int32_t *dev_err, void *stream) {
+  gm_status st = check_config(cfg, R, K);
+  if (st != GM_OK) return st;
+  if (K < 1) return fail(GM_ERR_INVALID_ARG, "gm_mtp_reconstruct needs K >= 1");
+  if (!mtp || !mtp->norm_h || !mtp->norm_e || !mtp->w_proj || !mtp->final_norm) return fail(GM_ERR_INVALID_ARG, "null MTP weights");
+  if ((st = check_layer(cfg, &mtp->layer, "gm_mtp_reconstruct")) != GM_OK) return st;
+  if (!shared || !shared->embed || !shared->lm_head) return fail(GM_ERR_INVALID_ARG, "null shared embedding / LM head");
+  st = check_cache(cfg, mtp_cache, 1, K, "gm_mtp_reconstruct");
+  if (st != GM_OK) return st;
+  if (R == 0) return GM_OK;
+  if (!start_hidden || !start_tokens || !head_logits || (K > 1 && !drafts))
+    return fail(GM_ERR_INVALID_ARG, "null reconstruction input / output");
+  const MtpPlan p = plan_mtp(*cfg, R, K, mtp_cache->max_ctx);
+  st = check_ws(ws, ws_bytes, p.total);
+  if (st != GM_OK) return st;
+  run_mtp_reconstruct(*cfg, *mtp, *shared, *mtp_cache, R, K, start_hidden, start_tokens, drafts, head_logits, p,
+                      (char *)ws, dev_err, (hipStream_t)stream);
+  return check_launch("gm_mtp_reconstruct");
 }

@@ -244,4 +244,48 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
   }
 }
 
+// Draft-path reconstruction: K batched single-row steps of the head, one row per
+// recorded cycle.  Depth j + 1 feeds the recorded start pair (j = 0) or
+// (g_j, d_j) at slot start + j, rotated at slot + 1, and attends to slots
+// 0 .. start + j of its own block table: the committed prefix and its own chain.
+// Nothing is drawn; the head logits of depth j + 1 go to head_logits[:, j, :].
+void run_mtp_reconstruct(const gm_model_config &cfg, const gm_mtp_weights &mtp, const gm_model_weights &shared,
+                         const gm_kv_cache &c, int R, int K, const float *start_hidden, const int32_t *start_tokens,
+                         const int32_t *drafts, float *head_logits, const MtpPlan &p, char *ws, int32_t *dev_err,
+                         hipStream_t s) {
+  const int H = cfg.hidden, F = cfg.ffn, V = cfg.vocab, dt = cfg.dtype;
+  const int qd = cfg.n_heads * cfg.head_dim, qw = qkv_width(cfg);
+  const gm_layer_weights &L = mtp.layer;
+  void *u = ws + p.u, *nbuf = ws + p.nbuf, *act = ws + p.act, *q = ws + p.q, *attn_g = ws + p.attn_g;
+  float *xg = (float *)(ws + p.xg), *qkv = (float *)(ws + p.qkv);
+  float *part = (float *)(ws + p.part);
+  int32_t *lens = c.seq_lens;
+  const float eps = cfg.rms_eps;
+  for (int j = 0; j < K; ++j) {
+    if (j == 0)
+      launch_mtp_input(dt, R, H, V, eps, start_hidden, start_tokens, 1, shared.embed, mtp.norm_h, mtp.norm_e, u,
+                       dev_err, s);
+    else
+      launch_mtp_input(dt, R, H, V, eps, xg, drafts + (j - 1), K, shared.embed, mtp.norm_h, mtp.norm_e, u, dev_err,
+                       s);
+    gemm_norm("recon_gemm_proj", dt, EPI_STORE_F32, R, H, 2 * H, u, 2 * H, mtp.w_proj, xg, part, L.attn_norm, eps,
+              nbuf, s);
+    const int sq = launch_gemm("recon_gemm_qkv", dt, EPI_STORE_F32, R, qw, H, nbuf, H, L.w_qkv, qkv, qw, part, s,
+                               nullptr, 1.f, true);
+    launch_rope_append(rope_args(cfg, c, 0, R, 1, qkv, part, sq, q, lens, j, nullptr, 1, L, dev_err), s);
+    AttnArgs a = attn_args(cfg, c, 0, R, 1, lens, j, nullptr);
+    a.trace = "attn_recon";
+    a.trace_combine = "attn_recon_combine";
+    a.q = q;
+    a.out = attn_g;
+    a.dev_err = dev_err;
+    run_attention(a, p.attn_chain, ws + p.attn_ws, s);
+    gemm_norm("recon_gemm_o", dt, EPI_ADD_F32, R, H, qd, attn_g, qd, L.w_o, xg, part, L.ffn_norm, eps, nbuf, s);
+    launch_gemm("recon_gemm_gate_up", dt, EPI_SWIGLU, R, F, H, nbuf, H, L.w_gate_up, act, F, part, s);
+    gemm_norm("recon_gemm_down", dt, EPI_ADD_F32, R, H, F, act, F, L.w_down, xg, part, mtp.final_norm, eps, nbuf, s);
+    launch_gemm("recon_gemm_lm_head", dt, EPI_STORE_F32, R, V, H, nbuf, H, shared.lm_head, head_logits + (long)j * V,
+                (long)K * V, part, s);
+  }
+}
+
 }  // namespace gm

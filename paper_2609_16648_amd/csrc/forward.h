@@ -127,6 +127,11 @@ struct MtpPlan {
   AttnPlan attn_ext, attn_chain;
 };
 MtpPlan plan_mtp(const gm_model_config &cfg, int B, int k, int max_ctx);
+// draft-path reconstruction of R recorded cycles over K depths (workspace: plan_mtp(cfg, R, K, max_ctx))
+void run_mtp_reconstruct(const gm_model_config &cfg, const gm_mtp_weights &mtp, const gm_model_weights &shared,
+                         const gm_kv_cache &c, int R, int K, const float *start_hidden, const int32_t *start_tokens,
+                         const int32_t *drafts, float *head_logits, const MtpPlan &p, char *ws, int32_t *dev_err,
+                         hipStream_t s);
 // top_p < 1 (sample mode): each draft is drawn from the nucleus of its row (inv_td = 1 / T in float64)
 void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const gm_model_weights &shared,
                    const gm_kv_cache &c, int B, int k, int mode, float inv_t, double top_p, double inv_td,

@@ -23,6 +23,7 @@ GM_OK, GM_ERR_INVALID_ARG, GM_ERR_UNSUPPORTED, GM_ERR_CAPACITY, GM_ERR_WORKSPACE
 GM_F32, GM_BF16 = 0, 1
 GM_GREEDY, GM_SAMPLE = 0, 1
 GM_OP_VERIFY_FORWARD, GM_OP_VERIFY_ATTENTION, GM_OP_SPEC_ACCEPT, GM_OP_MTP_DRAFT, GM_OP_DCA_LOSS = 0, 1, 2, 3, 4
+GM_OP_MTP_RECONSTRUCT = 5
 GM_DEVERR_TOKEN, GM_DEVERR_PAGE = 1, 2
 
 c_int, c_float, c_void_p, c_size_t, c_double = ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_double
@@ -64,7 +65,7 @@ class KVCacheDesc(ctypes.Structure):
 _lib = None
 
 EXPORTS = ["gm_workspace_size", "gm_verify_forward", "gm_verify_attention", "gm_spec_accept", "gm_kv_commit",
-           "gm_mtp_draft", "gm_dca_loss", "gm_last_error", "gm_trace_start", "gm_trace_stop", "gm_trace_count", "gm_trace_get"]
+           "gm_mtp_draft", "gm_mtp_reconstruct", "gm_dca_loss", "gm_last_error", "gm_trace_start", "gm_trace_stop", "gm_trace_count", "gm_trace_get"]
 
 
 def lib() -> ctypes.CDLL:
@@ -94,6 +95,9 @@ def lib() -> ctypes.CDLL:
     L.gm_mtp_draft.argtypes = [P(ModelConfig), P(MtpWeights), P(ModelWeights), P(KVCacheDesc), c_int, c_int,
                                c_int, c_float, c_float, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                c_void_p, c_void_p, c_size_t, c_void_p, c_void_p]
+    L.gm_mtp_reconstruct.restype = c_int
+    L.gm_mtp_reconstruct.argtypes = [P(ModelConfig), P(MtpWeights), P(ModelWeights), P(KVCacheDesc), c_int, c_int,
+                                     c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p, c_void_p]
     L.gm_dca_loss.restype = c_int
     L.gm_dca_loss.argtypes = [c_int, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_void_p,
                               c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
@@ -411,6 +415,25 @@ def mtp_draft(model: DeviceModel, mtp: DeviceMtp, mtp_cache: PagedCache, k: int,
                               _ptr(out_tokens), _ptr(u_draft), _ptr(drafts), _ptr(draft_logits), _ptr(draft_stats),
                               _ptr(buf),
                               buf.numel(), _ptr(dev_err), _stream(stream)))
+
+
+def mtp_reconstruct(model: DeviceModel, mtp: DeviceMtp, mtp_cache: PagedCache, K: int,
+                    start_hidden: torch.Tensor, start_tokens: torch.Tensor, drafts: Optional[torch.Tensor],
+                    head_logits: torch.Tensor, ws: Workspace, dev_err: Optional[torch.Tensor] = None, stream=None):
+    """Draft-path reconstruction of mtp_cache.B recorded cycles over K depths (see gm.h)."""
+    R = mtp_cache.B
+    s = model.shape
+    _need(start_hidden, torch.float32, (R, s.hidden), "start_hidden")
+    _need(start_tokens, torch.int32, (R,), "start_tokens")
+    if drafts is not None:
+        _need(drafts, torch.int32, (R, K), "drafts")
+    _need(head_logits, torch.float32, (R, K, s.vocab), "head_logits")
+    cs = mtp_cache.struct()
+    n = workspace_size(GM_OP_MTP_RECONSTRUCT, model.cfg, R, K, mtp_cache.max_ctx)
+    buf = ws.get(n)
+    _check(lib().gm_mtp_reconstruct(ctypes.byref(model.cfg), ctypes.byref(mtp.struct), ctypes.byref(model.struct),
+                                    ctypes.byref(cs), R, K, _ptr(start_hidden), _ptr(start_tokens), _ptr(drafts),
+                                    _ptr(head_logits), _ptr(buf), buf.numel(), _ptr(dev_err), _stream(stream)))
 
 
 def dca_loss(head_logits: torch.Tensor, rec_logp: torch.Tensor, rec_ids: torch.Tensor,

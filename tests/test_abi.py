@@ -36,7 +36,8 @@ def _cfg(shape=synth.QWEN3_4B_LAYER):
 
 def test_workspace_sizes():
     cfg = _cfg()
-    for op in (gm.GM_OP_VERIFY_FORWARD, gm.GM_OP_VERIFY_ATTENTION, gm.GM_OP_SPEC_ACCEPT, gm.GM_OP_MTP_DRAFT):
+    for op in (gm.GM_OP_VERIFY_FORWARD, gm.GM_OP_VERIFY_ATTENTION, gm.GM_OP_SPEC_ACCEPT, gm.GM_OP_MTP_DRAFT,
+               gm.GM_OP_MTP_RECONSTRUCT):
         assert gm.workspace_size(op, cfg, 64, 3, 4096) > 0
     assert gm.workspace_size(99, cfg, 64, 3, 4096) == 0
     assert gm.workspace_size(gm.GM_OP_VERIFY_FORWARD, cfg, 64, 16, 4096) == 0      # k beyond the limit
@@ -136,6 +137,15 @@ def test_mtp_and_attention_reject_bad_arguments():
     st = L.gm_mtp_draft(ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(c.desc), 4, 3,
                         gm.GM_SAMPLE, 1.0, 0.7, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None, None)
     assert st == gm.GM_ERR_UNSUPPORTED and "draft_stats" in gm.last_error()
+    # reconstruction: K >= 1, inputs, and room for the K chain entries past max_ctx
+    rc = lambda cache, K, hid=FAKE, toks=FAKE, dr=FAKE: L.gm_mtp_reconstruct(
+        ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(cache.desc), 4, K, hid, toks, dr, FAKE,
+        FAKE, 1 << 30, None, None)
+    assert rc(c, 0) == gm.GM_ERR_INVALID_ARG
+    assert rc(c, 3, hid=None) == gm.GM_ERR_INVALID_ARG and "reconstruction" in gm.last_error()
+    assert rc(c, 3, dr=None) == gm.GM_ERR_INVALID_ARG
+    assert rc(_FakeCache(1, 150), 11) == gm.GM_ERR_CAPACITY           # 150 + 11 > 160
+    assert gm.workspace_size(gm.GM_OP_MTP_RECONSTRUCT, cfg, 4, 0, 100) == 0
     st = L.gm_verify_attention(ctypes.byref(cfg), ctypes.byref(c.desc), 1, 4, 3, FAKE, FAKE, FAKE, 1 << 30, None, None)
     assert st == gm.GM_ERR_INVALID_ARG                              # layer out of range
     st = L.gm_kv_commit(ctypes.byref(c.desc), 4, 3, None, None, None)

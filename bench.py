@@ -260,6 +260,49 @@ def time_dca(wl, N, iters=5):
     return out
 
 
+def time_reconstruct(step, wl, R, iters=3):
+    """Draft-path reconstruction (gm_mtp_reconstruct) of R recorded cycles over the
+    workload's depth K, with the workload's head weights: cycle r starts after the
+    committed prefix of the workload's context lengths (repeated to R), N(0,1) head
+    cache, start hiddens N(0,1), uniform start tokens and drafts.  One call runs the K
+    batched depths; its algorithmic bytes are K x (head weights incl. the LM head
+    + every cycle's visible KV + the head logits)."""
+    import torch
+    from paper_2609_16648_amd import gm
+    s, K, V, H = wl.shape, wl.k, wl.shape.vocab, wl.shape.hidden
+    starts = np.resize(step.lens, R)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(synth.SEED_KV + 7)
+    cache = gm.PagedCache(s, 1, starts, starts + K + 1, page_size=wl.page_size, fill="empty")
+    for t in cache.k + cache.v:
+        t.normal_(generator=gen)
+    h0 = torch.empty((R, H), dtype=torch.float32, device="cuda").normal_(generator=gen)
+    t0 = torch.randint(0, V, (R,), generator=gen, device="cuda", dtype=torch.int32)
+    drafts = torch.randint(0, V, (R, K), generator=gen, device="cuda", dtype=torch.int32)
+    out = torch.empty((R, K, V), dtype=torch.float32, device="cuda")
+    ws = gm.Workspace()
+    gm.mtp_reconstruct(step.model, step.mtp, cache, K, h0, t0, drafts, out, ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(iters):
+        gm.mtp_reconstruct(step.model, step.mtp, cache, K, h0, t0, drafts, out, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / iters
+    d, nkv, nq, F = s.head_dim, s.n_kv_heads, s.n_heads, s.ffn
+    params = 2 * H * H + H * (nq + 2 * nkv) * d + nq * d * H + 2 * F * H + F * H + V * H
+    kv = float(sum((starts.astype(np.float64) + j + 1).sum() for j in range(K))) * nkv * d * 2 * 2
+    flops = K * 2.0 * R * params + 4.0 * nq * d * kv / (nkv * d * 2 * 2)
+    nbytes = K * (2.0 * params + R * V * 4.0) + kv
+    out_ = {"cycles": R, "k": K, "ms": round(ms, 3), "ms_per_depth": round(ms / K, 3),
+            "TFLOP_s": round(flops / (ms * 1e-3) / 1e12, 1), "mfma_frac": round(flops / (ms * 1e-3) / 1e12 / BF16_TFLOPS, 3),
+            "GB_s": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+    del cache, out
+    torch.cuda.empty_cache()
+    return out_
+
+
 # ----------------------------------------------------------------------------- CPU baseline
 def cpu_baseline(wl, mode, budget_s, weights=None, top_p=1.0):
     """The oracle, as it stands, on a bounded sample of the same workload: the
@@ -374,6 +417,8 @@ def main():
                     help="also time the DCA loss forward and gradient over N cycle records of the workload's shape")
     ap.add_argument("--record", type=int, default=0, metavar="K",
                     help="also take the cycle record's top-K log-probabilities in the accept (0: off)")
+    ap.add_argument("--reconstruct", type=int, default=0, metavar="R",
+                    help="also time the draft-path reconstruction of R recorded cycles (the paper's chunks: 1024)")
     ap.add_argument("--top-p", type=float, default=1.0,
                     help="top-p of the accept and the draft (the paper's evaluation decodes at 0.7; 1: off)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -474,6 +519,10 @@ def main():
 
     if args.dca:
         summary["dca"] = time_dca(wl, args.dca)
+    if args.reconstruct:
+        if not wl.with_mtp:
+            raise SystemExit("--reconstruct needs a workload with the MTP head")
+        summary["reconstruct"] = time_reconstruct(step, wl, args.reconstruct)
 
     if args.copy_probe_mib:
         src = torch.empty(args.copy_probe_mib << 20, dtype=torch.uint8, device="cuda")

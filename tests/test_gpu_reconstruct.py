@@ -96,3 +96,36 @@ def test_reconstruct_reproduces_gpu_drafting():
           % (e, same, int(clear.sum())), flush=True)
     assert e < 1e-2
     assert same == 1.0
+
+
+def test_reconstruct_full_size_sampled():
+    # the bench's launch configuration: 1024 cycles (the paper's chunk) at the Qwen3-4B
+    # shape, K = 3, starts from the layer workload's contexts U[1024, 4096]; the head
+    # cache is filled on the device, and four sampled cycles (first, last, two inside)
+    # are checked against the oracle from the entries read back
+    need_gpu()
+    shape = synth.QWEN3_4B_LAYER
+    W, Wm = synth.model_weights(shape), synth.mtp_weights(shape)
+    R, K = 1024, 3
+    g = np.random.default_rng(13)
+    starts = g.integers(1024, 4097, R)
+    model, mtp = gm.DeviceModel(shape, W), gm.DeviceMtp(shape, Wm)
+    cache = gm.PagedCache(shape, 1, starts, starts + K + 1, fill="empty")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(13)
+    for t in cache.k + cache.v:
+        t.normal_(generator=gen)
+    h0 = g.standard_normal((R, shape.hidden)).astype(np.float32)
+    t0 = g.integers(0, shape.vocab, R).astype(np.int32)
+    drafts = g.integers(0, shape.vocab, (R, K)).astype(np.int32)
+    out = torch.zeros((R, K, shape.vocab), dtype=torch.float32, device="cuda")
+    gm.mtp_reconstruct(model, mtp, cache, K, t32(h0), i32(t0), i32(drafts), out, gm.Workspace())
+    torch.cuda.synchronize()
+    worst = 0.0
+    for r in (0, 377, 800, R - 1):
+        ks, vs = cache.read(0, r, np.arange(starts[r]))
+        ref = oracle.mtp_reconstruct(shape, Wm, W, [ks], [vs], starts[r:r + 1], h0[r:r + 1], t0[r:r + 1],
+                                     drafts[r:r + 1], K, CONTRACT)
+        worst = max(worst, rel_err(out[r].cpu().numpy(), ref["logits"][0]))
+    print("[reconstruct R=1024 K=3] sampled cycles' head logits rel err %.3e" % worst, flush=True)
+    assert worst < 1e-2

@@ -214,7 +214,7 @@ def test_qwen_layer_bf16_mtp_top_p_draw_from_own_logits(qwen_mtp, B, temperature
     # nucleus of softmax(z / T) of the logits the head wrote.  u * Z' (Z' the nucleus
     # mass) must fall in the drawn id's interval of the nucleus's CDF, widened by 1e-6 Z'
     # for the float32 terms, and the draw equals the oracle's from the same logits unless
-    # the nucleus boundary lies within 1e-9 of top_p
+    # the nucleus boundary lies within 5e-9 of top_p
     need_gpu()
     shape, W, Wm = qwen_mtp
     k = 3
@@ -232,7 +232,7 @@ def test_qwen_layer_bf16_mtp_top_p_draw_from_own_logits(qwen_mtp, B, temperature
     for b in range(B):
         for j in range(k):
             pn, dist = oracle.nucleus(z[b, j], oracle.softmax(z[b, j].astype(np.float64) / temperature), top_p)
-            if dist < 1e-9:
+            if dist < 5e-9:
                 flagged += 1
                 continue
             x = int(got[b, j])

@@ -3,7 +3,7 @@ App. "Evaluation Configuration": rejection sampling at T = 1, top-p 0.7) against
 the oracle on the same seeded logits.  The drafts are samples of the head's
 nucleus.  Accept counts and committed tokens must match bit for bit outside the
 flag windows (those of the plain rule, plus a nucleus whose boundary lies within
-1e-9 of top_p); the flagged count is printed."""
+5e-9 of top_p); the flagged count is printed."""
 import numpy as np
 import pytest
 import torch
@@ -15,7 +15,7 @@ from paper_2609_16648_amd import gm
 
 pytestmark = pytest.mark.gpu
 FINAL_EPS = 1e-8
-NUC_EPS = 1e-9
+NUC_EPS = 5e-9         # >= V 2^-45, the largest distance of the kernel's fixed-point sums from float64
 
 
 def _nucleus_drafts(zq, ud, top_p, temperature):

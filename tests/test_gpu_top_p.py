@@ -56,6 +56,9 @@ def _logits(shape, kind, *tags):
     (40, 3, 5000, 1.0, 0.7, "ties"),           # the boundary inside a run of equal logits
     (8, 1, 4096, 1.3, 0.2, "ties"),
     (8, 2, 151936, 1.0, 0.5, "flat"),          # too many ties for LDS: the passes over the row
+    (3, 0, 5000, 1.0, 0.7, "normal"),          # no drafts: the bonus draw from the target's nucleus
+    (16, 2, 1001, 1.0, 0.6, "normal"),         # rows not a multiple of 4 ids: unaligned row reads
+    (1, 1, 151936, 1.0, 0.7, "normal"),        # one sequence: the first pass split over 8 workgroups
 ])
 def test_top_p_accept_matches_oracle(B, k, V, T, top_p, kind):
     need_gpu()

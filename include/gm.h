@@ -158,6 +158,19 @@ typedef struct {
   double sum;
 } gm_row_stats;
 
+/* Top-p: the nucleus of one logits row (see gm_spec_accept's top_p): the kept ids are
+ * those whose logit's order key exceeds `key`, and those with that key up to id
+ * `last_id`; `mass` is sum over them of exp(z / T - m).  (The order key of a float32
+ * x: its bits with the sign bit set if x >= 0, all bits inverted if x < 0; -0 as +0.)
+ * gm_mtp_draft can emit them for its draft rows under top-p; gm_spec_accept can take
+ * them in place of its own passes over those rows. */
+typedef struct {
+  double m;
+  double mass;
+  uint32_t key;
+  int32_t last_id;
+} gm_nucleus;
+
 /* The cycle record's verification distributions (App. "Implementing Draft-Path
  * Reconstruction in verl", recording in rollout): for every sequence b and draft
  * position i < k, the `topk` largest entries of p_i = softmax(target_logits[b][i] / T),
@@ -220,6 +233,10 @@ gm_status gm_verify_attention(const gm_model_config *cfg, const gm_kv_cache *cac
  *   running masses are exact sums of float64 exponentials rounded to 2^-44 of
  *   the row maximum's term.  GM_GREEDY ignores top_p; 1 keeps every id.
  *   GM_ERR_INVALID_ARG outside (0, 1].
+ * draft_nucleus [B][k] (may be NULL; read in GM_SAMPLE mode with top_p < 1 only): the
+ *   nuclei of the draft_logits rows at this T and top_p, as gm_mtp_draft writes them.
+ *   Given, they stand in for the passes over the draft rows (their statistics and
+ *   their nucleus); the caller guarantees that they describe these draft_logits.
  * draft_stats [B][k] (may be NULL; read in GM_SAMPLE mode only): the statistics
  *   of softmax(draft_logits[b][i] / T) at this temperature, as gm_mtp_draft
  *   writes them.  Given, they stand in for a pass over the draft rows; the
@@ -232,7 +249,7 @@ gm_status gm_verify_attention(const gm_model_config *cfg, const gm_kv_cache *cac
  * The logits rows are read in place; no probability matrix is written. */
 gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature, float top_p,
                          const float *target_logits, const float *draft_logits,
-                         const gm_row_stats *draft_stats,
+                         const gm_row_stats *draft_stats, const gm_nucleus *draft_nucleus,
                          const int32_t *draft_tokens, const float *u_accept, const float *u_final,
                          int32_t *n_accept, int32_t *out_tokens, const gm_record *record, void *ws,
                          size_t ws_bytes, void *stream);
@@ -264,14 +281,17 @@ gm_status gm_kv_commit(const gm_kv_cache *cache, int B, int k, const int32_t *n_
  * (the draw's own; gm_spec_accept takes them for the same rows and T).
  * top_p in (0, 1] (GM_SAMPLE): below 1, each draft is the inverse-CDF draw with
  * u_draft[b][j] from the nucleus of softmax(z / T) (as in gm_spec_accept);
- * draft_stats must then be NULL (GM_ERR_UNSUPPORTED otherwise).
+ * draft_stats must then be NULL (GM_ERR_UNSUPPORTED otherwise); draft_nucleus [B][k]
+ * (may be NULL) receives the nucleus of every draft_logits row (gm_spec_accept takes
+ * them for the same rows, T and top_p).  With top_p = 1 or GM_GREEDY it is not written.
  * Errors: GM_ERR_CAPACITY if max_ctx + 2k + 1 > max_pages_per_seq * page_size
  * of the head's cache; GM_ERR_INVALID_ARG for top_p outside (0, 1]. */
 gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weights *mtp,
                        const gm_model_weights *shared, const gm_kv_cache *mtp_cache, int B, int k,
                        int mode, float temperature, float top_p, const float *verify_hidden,
                        const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft,
-                       int32_t *drafts, float *draft_logits, gm_row_stats *draft_stats, void *ws,
+                       int32_t *drafts, float *draft_logits, gm_row_stats *draft_stats,
+                       gm_nucleus *draft_nucleus, void *ws,
                        size_t ws_bytes, int32_t *dev_err, void *stream);
 
 /* Draft-path reconstruction (App. "Draft-Path Reconstruction"; App. "Parallelizing

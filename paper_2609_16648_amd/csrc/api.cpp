@@ -150,10 +150,15 @@ static_assert(sizeof(gm_row_stats) == sizeof(RowStat) && offsetof(gm_row_stats, 
                   offsetof(gm_row_stats, argmax) == offsetof(RowStat, argmax) &&
                   offsetof(gm_row_stats, sum) == offsetof(RowStat, sum),
               "gm_row_stats is the device's RowStat");
+static_assert(sizeof(gm_nucleus) == sizeof(NucRow) && offsetof(gm_nucleus, m) == offsetof(NucRow, m) &&
+                  offsetof(gm_nucleus, mass) == offsetof(NucRow, s) && offsetof(gm_nucleus, key) == offsetof(NucRow, key) &&
+                  offsetof(gm_nucleus, last_id) == offsetof(NucRow, idt),
+              "gm_nucleus is the device's NucRow");
 
 extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature, float top_p,
                                     const float *target_logits,
                                     const float *draft_logits, const gm_row_stats *draft_stats,
+                                    const gm_nucleus *draft_nucleus,
                                     const int32_t *draft_tokens, const float *u_accept,
                                     const float *u_final, int32_t *n_accept, int32_t *out_tokens,
                                     const gm_record *record, void *ws, size_t ws_bytes, void *stream) {
@@ -187,8 +192,11 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
   launch_row_stats("accept_row_stats", target_logits, V, B * (k + 1), V, inv_t, tstat, s, submax);
   // q's statistics: the draft head's own (one per row) when the caller has them, else a pass over the rows
   int nch_d = stat_chunks(V);
+  const bool top_p_on = mode == GM_SAMPLE && top_p < 1.f;
   if (mode == GM_SAMPLE && k > 0) {
-    if (draft_stats) {
+    if (top_p_on && draft_nucleus) {
+      nch_d = 0;                      // the draft rows' nuclei carry their reference and mass
+    } else if (draft_stats) {
       dstat = (RowStat *)draft_stats;
       nch_d = 1;
     } else {
@@ -198,14 +206,17 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
   // top-p (sample mode): the nuclei of every target and draft row
   const double inv_td = 1.0 / (double)temperature;
   NucRow *tnuc = nullptr, *dnuc = nullptr;
-  if (mode == GM_SAMPLE && top_p < 1.f) {
+  if (top_p_on) {
     tnuc = (NucRow *)(w + p.tnuc);
     unsigned long long *part = (unsigned long long *)(w + p.nucpart);
     launch_nucleus("accept_nucleus", B * (k + 1), V, inv_td, (double)top_p, target_logits, V, tstat, stat_chunks(V),
-                   tnuc, part, s);
-    if (k > 0) {
+                   tnuc, 1, part, s);
+    if (k > 0 && draft_nucleus) {
+      dnuc = (NucRow *)draft_nucleus;
+    } else if (k > 0) {
       dnuc = (NucRow *)(w + p.dnuc);
-      launch_nucleus("accept_nucleus", B * k, V, inv_td, (double)top_p, draft_logits, V, dstat, nch_d, dnuc, part, s);
+      launch_nucleus("accept_nucleus", B * k, V, inv_td, (double)top_p, draft_logits, V, dstat, nch_d, dnuc, 1, part,
+                     s);
     }
   }
   launch_accept_decide(B, k, V, mode, inv_t, inv_td, target_logits, draft_logits, tstat, dstat, nch_d, tnuc, dnuc,
@@ -297,7 +308,8 @@ extern "C" gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weigh
                                   const gm_kv_cache *mtp_cache, int B, int k, int mode, float temperature,
                                   float top_p, const float *verify_hidden, const int32_t *n_accept, const int32_t *out_tokens,
                                   const float *u_draft, int32_t *drafts, float *draft_logits,
-                                  gm_row_stats *draft_stats, void *ws, size_t ws_bytes, int32_t *dev_err,
+                                  gm_row_stats *draft_stats, gm_nucleus *draft_nucleus, void *ws, size_t ws_bytes,
+                                  int32_t *dev_err,
                                   void *stream) {
   gm_status st = check_config(cfg, B, k);
   if (st != GM_OK) return st;
@@ -321,7 +333,8 @@ extern "C" gm_status gm_mtp_draft(const gm_model_config *cfg, const gm_mtp_weigh
   if (st != GM_OK) return st;
   run_mtp_draft(*cfg, *mtp, *shared, *mtp_cache, B, k, mode, 1.0f / temperature,
                 mode == GM_SAMPLE && top_p < 1.f ? (double)top_p : 1.0, 1.0 / (double)temperature, verify_hidden,
-                n_accept, out_tokens, u_draft, drafts, draft_logits, (RowStat *)draft_stats, p, (char *)ws, dev_err,
+                n_accept, out_tokens, u_draft, drafts, draft_logits, (RowStat *)draft_stats, (NucRow *)draft_nucleus, p,
+                (char *)ws, dev_err,
                 (hipStream_t)stream);
   return check_launch("gm_mtp_draft");
 }

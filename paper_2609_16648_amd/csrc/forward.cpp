@@ -160,7 +160,8 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
                    const gm_kv_cache &c, int B, int k, int mode, float inv_t, double top_p, double inv_td,
                    const float *verify_hidden,
                    const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft, int32_t *drafts,
-                   float *draft_logits, RowStat *draft_stats, const MtpPlan &p, char *ws, int32_t *dev_err,
+                   float *draft_logits, RowStat *draft_stats, NucRow *draft_nucleus, const MtpPlan &p, char *ws,
+                   int32_t *dev_err,
                    hipStream_t s) {
   const int R = k + 1, Me = B * R, H = cfg.hidden, F = cfg.ffn, V = cfg.vocab, dt = cfg.dtype;
   const int qd = cfg.n_heads * cfg.head_dim, qw = qkv_width(cfg);
@@ -187,11 +188,13 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
                 inv_t);
     const TileGeom geo = plan_lm_head(dt, B, V, H);
     if (top_p < 1.0) {   // top-p: a draw from each row's nucleus (a selection, then an inverse-CDF scan)
-      NucRow *nuc = (NucRow *)(ws + p.nuc);
+      // the nuclei go to the caller's draft_nucleus[:, j] when given (the accept's handoff)
+      NucRow *nuc = draft_nucleus ? draft_nucleus + j : (NucRow *)(ws + p.nuc);
+      const int ns = draft_nucleus ? k : 1;
       RowSel *sel = (RowSel *)(ws + p.sel);
-      launch_nucleus("draft_nucleus", B, V, inv_td, top_p, zl, (long)k * V, tiles, geo.tiles, nuc,
+      launch_nucleus("draft_nucleus", B, V, inv_td, top_p, zl, (long)k * V, tiles, geo.tiles, nuc, ns,
                      (unsigned long long *)(ws + p.nucpart), s);
-      launch_nucleus_select(B, zl, (long)k * V, nuc, u_draft + j, k, drafts + j, k, sel, s);
+      launch_nucleus_select(B, zl, (long)k * V, nuc, ns, u_draft + j, k, drafts + j, k, sel, s);
       launch_residual_draw("draft_nucleus_chunk", "draft_nucleus_scan", B, V, inv_t, sel, (double *)(ws + p.wsum),
                            (double *)(ws + p.psum), s);
     } else {

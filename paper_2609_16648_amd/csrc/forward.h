@@ -137,7 +137,8 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
                    const gm_kv_cache &c, int B, int k, int mode, float inv_t, double top_p, double inv_td,
                    const float *verify_hidden,
                    const int32_t *n_accept, const int32_t *out_tokens, const float *u_draft, int32_t *drafts,
-                   float *draft_logits, RowStat *draft_stats, const MtpPlan &p, char *ws, int32_t *dev_err,
+                   float *draft_logits, RowStat *draft_stats, NucRow *draft_nucleus, const MtpPlan &p, char *ws,
+                   int32_t *dev_err,
                    hipStream_t s);
 
 }  // namespace gm

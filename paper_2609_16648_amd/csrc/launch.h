@@ -109,18 +109,18 @@ void launch_accept_decide(int B, int k, int V, int mode, float inv_t, double inv
                           const int32_t *drafts, const float *u_accept, const float *u_final,
                           int32_t *n_accept, int32_t *out_tokens, RowSel *sel, hipStream_t s);
 // top-p: the nucleus of rows r = 0..n_rows-1 at logits + r * row_stride, each with nch
-// statistics (chunks or tiles) at st + r * nch; 0 < top_p < 1.  part (may be null):
+// statistics (chunks or tiles) at st + r * nch, into out[r * out_stride]; 0 < top_p < 1.  part (may be null):
 // kNucPartBytes of scratch that lets launches of few rows split their first pass
 constexpr int kNucSplitRows = 256;     // rows x workgroups per row of a split first pass
 constexpr int kNucMaxSplit = 8;
 constexpr size_t kNucPartBytes = (size_t)kNucSplitRows * 4096 * 8;
 void launch_nucleus(const char *name, int n_rows, int V, double inv_td, double top_p, const float *logits,
-                    long row_stride, const RowStat *st, int nch, NucRow *out, unsigned long long *part,
-                    hipStream_t s);
-// sel[b] := a draw from the nucleus nuc[b] of row b (logits + b * row_stride) with the
-// uniform u[b * u_stride], into dst[b * dst_stride]
-void launch_nucleus_select(int B, const float *logits, long row_stride, const NucRow *nuc, const float *u,
-                           int u_stride, int32_t *dst, int dst_stride, RowSel *sel, hipStream_t s);
+                    long row_stride, const RowStat *st, int nch, NucRow *out, int out_stride,
+                    unsigned long long *part, hipStream_t s);
+// sel[b] := a draw from the nucleus nuc[b * nuc_stride] of row b (logits + b * row_stride)
+// with the uniform u[b * u_stride], into dst[b * dst_stride]
+void launch_nucleus_select(int B, const float *logits, long row_stride, const NucRow *nuc, int nuc_stride,
+                           const float *u, int u_stride, int32_t *dst, int dst_stride, RowSel *sel, hipStream_t s);
 void launch_residual_draw(const char *chunk_name, const char *scan_name, int B, int V, float inv_t, const RowSel *sel, double *wsum,
                           double *psum, hipStream_t s);
 

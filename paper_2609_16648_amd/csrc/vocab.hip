@@ -705,7 +705,7 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
                                                               const float *__restrict__ logits, long row_stride,
                                                               const RowStat *__restrict__ st, int nch,
                                                               const unsigned long long *__restrict__ part, int S,
-                                                              NucRow *__restrict__ out) {
+                                                              NucRow *__restrict__ out, int out_stride) {
   __shared__ unsigned long long hist[kNucBins];
   __shared__ float qv[kNucQueue];
   __shared__ int qx[kNucQueue];
@@ -749,7 +749,7 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
     tot = sh_above;
   }
   if (tot == 0) {           // no mass (every logit -inf or NaN): keep every id
-    if (tid == 0) out[r] = NucRow{m, 0.0, 0u, 0x7fffffff};
+    if (tid == 0) out[(long)r * out_stride] = NucRow{m, 0.0, 0u, 0x7fffffff};
     return;
   }
   const double thr = top_p * (double)tot;
@@ -864,12 +864,12 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
     __syncthreads();
     idt = sh_idt;
   }
-  if (tid == 0) out[r] = NucRow{m, (double)(above + (unsigned long long)j * et) * 0x1p-44, key, idt};
+  if (tid == 0) out[(long)r * out_stride] = NucRow{m, (double)(above + (unsigned long long)j * et) * 0x1p-44, key, idt};
 }
 
 void launch_nucleus(const char *name, int n_rows, int V, double inv_td, double top_p, const float *logits,
-                    long row_stride, const RowStat *st, int nch, NucRow *out, unsigned long long *part,
-                    hipStream_t s) {
+                    long row_stride, const RowStat *st, int nch, NucRow *out, int out_stride,
+                    unsigned long long *part, hipStream_t s) {
   if (n_rows <= 0) return;
   TraceScope ts(name, s);
   // fewer than 128 rows leave CUs idle: their first pass is split over up to 8 workgroups per row
@@ -880,15 +880,16 @@ void launch_nucleus(const char *name, int n_rows, int V, double inv_td, double t
     hipLaunchKernelGGL(nucleus_hist_kernel, dim3(n_rows * S), dim3(kNucThreads), 0, s, V, inv_td, logits, row_stride,
                        st, nch, S, part);
   hipLaunchKernelGGL(nucleus_kernel, dim3(n_rows), dim3(kNucThreads), 0, s, V, inv_td, top_p, logits, row_stride, st,
-                     nch, S > 1 ? part : nullptr, S, out);
+                     nch, S > 1 ? part : nullptr, S, out, out_stride);
 }
 
 __global__ void nucleus_select_kernel(int B, const float *__restrict__ logits, long row_stride,
-                                      const NucRow *__restrict__ nuc, const float *__restrict__ u, int u_stride,
+                                      const NucRow *__restrict__ nuc, int nuc_stride, const float *__restrict__ u,
+                                      int u_stride,
                                       int32_t *dst, int dst_stride, RowSel *__restrict__ sel) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= B) return;
-  const NucRow n = nuc[b];
+  const NucRow n = nuc[(long)b * nuc_stride];
   RowSel rs;
   rs.p_row = logits + (long)b * row_stride;
   rs.q_row = nullptr;
@@ -907,11 +908,11 @@ __global__ void nucleus_select_kernel(int B, const float *__restrict__ logits, l
   sel[b] = rs;
 }
 
-void launch_nucleus_select(int B, const float *logits, long row_stride, const NucRow *nuc, const float *u,
-                           int u_stride, int32_t *dst, int dst_stride, RowSel *sel, hipStream_t s) {
+void launch_nucleus_select(int B, const float *logits, long row_stride, const NucRow *nuc, int nuc_stride,
+                           const float *u, int u_stride, int32_t *dst, int dst_stride, RowSel *sel, hipStream_t s) {
   if (B <= 0) return;
-  hipLaunchKernelGGL(nucleus_select_kernel, dim3((B + 63) / 64), dim3(64), 0, s, B, logits, row_stride, nuc, u,
-                     u_stride, dst, dst_stride, sel);
+  hipLaunchKernelGGL(nucleus_select_kernel, dim3((B + 63) / 64), dim3(64), 0, s, B, logits, row_stride, nuc,
+                     nuc_stride, u, u_stride, dst, dst_stride, sel);
 }
 
 // ------------------------------------------------------------------ 3. inverse-CDF draw

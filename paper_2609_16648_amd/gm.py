@@ -87,13 +87,13 @@ def lib() -> ctypes.CDLL:
                                       c_void_p, c_size_t, c_void_p, c_void_p]
     L.gm_spec_accept.restype = c_int
     L.gm_spec_accept.argtypes = [c_int, c_int, c_int, c_int, c_float, c_float, c_void_p, c_void_p, c_void_p,
-                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
-                                 c_void_p]
+                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                 c_size_t, c_void_p]
     L.gm_kv_commit.restype = c_int
     L.gm_kv_commit.argtypes = [P(KVCacheDesc), c_int, c_int, c_void_p, c_void_p, c_void_p]
     L.gm_mtp_draft.restype = c_int
     L.gm_mtp_draft.argtypes = [P(ModelConfig), P(MtpWeights), P(ModelWeights), P(KVCacheDesc), c_int, c_int,
-                               c_int, c_float, c_float, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                               c_int, c_float, c_float, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                c_void_p, c_void_p, c_size_t, c_void_p, c_void_p]
     L.gm_mtp_reconstruct.restype = c_int
     L.gm_mtp_reconstruct.argtypes = [P(ModelConfig), P(MtpWeights), P(ModelWeights), P(KVCacheDesc), c_int, c_int,
@@ -340,6 +340,14 @@ class Record(ctypes.Structure):
     _fields_ = [("topk", ctypes.c_int), ("logp", ctypes.c_void_p), ("ids", ctypes.c_void_p)]
 
 
+NUCLEUS_BYTES = 24   # gm_nucleus: float64 m, float64 mass, uint32 key, int32 last_id
+
+
+def new_nuclei(B: int, k: int, device="cuda") -> torch.Tensor:
+    """Device buffer for gm_nucleus [B][k] (the top-p handoff from mtp_draft to spec_accept)."""
+    return torch.zeros((B, k, NUCLEUS_BYTES), dtype=torch.uint8, device=device)
+
+
 def new_row_stats(B: int, k: int, device="cuda") -> torch.Tensor:
     """Storage for [B][k] gm_row_stats (as bytes)."""
     return torch.zeros((B, k, ROW_STATS_BYTES), dtype=torch.uint8, device=device)
@@ -356,9 +364,11 @@ def decode_row_stats(t: torch.Tensor):
 def spec_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], draft_tokens: torch.Tensor,
                 u_accept: Optional[torch.Tensor], u_final: Optional[torch.Tensor], n_accept: torch.Tensor,
                 out_tokens: torch.Tensor, mode: int, ws: Workspace, temperature: float = 1.0, stream=None,
-                draft_stats: Optional[torch.Tensor] = None, record=None, top_p: float = 1.0):
+                draft_stats: Optional[torch.Tensor] = None, record=None, top_p: float = 1.0,
+                draft_nucleus: Optional[torch.Tensor] = None):
     """record: optional (logp [B, k, topk] bfloat16, ids [B, k, topk] int32) for the cycle record;
-    top_p < 1: the accept rule on the nuclei of p and q (see gm.h)."""
+    top_p < 1: the accept rule on the nuclei of p and q (see gm.h); draft_nucleus: the draft
+    rows' nuclei as mtp_draft wrote them (new_nuclei)."""
     B, k1, V = target_logits.shape
     k = k1 - 1
     _need(target_logits, torch.float32, (B, k1, V), "target_logits")
@@ -369,6 +379,8 @@ def spec_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor
     _need(out_tokens, torch.int32, (B, k1), "out_tokens")
     if draft_stats is not None:
         _need(draft_stats, torch.uint8, (B, k, ROW_STATS_BYTES), "draft_stats")
+    if draft_nucleus is not None:
+        _need(draft_nucleus, torch.uint8, (B, k, NUCLEUS_BYTES), "draft_nucleus")
     rec = None
     if record is not None:
         logp, ids = record
@@ -382,7 +394,7 @@ def spec_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor
     buf = ws.get(n)
     _check(lib().gm_spec_accept(B, k, V, mode, float(temperature), float(top_p), _ptr(target_logits),
                                 _ptr(draft_logits),
-                                _ptr(draft_stats), _ptr(draft_tokens), _ptr(u_accept), _ptr(u_final), _ptr(n_accept),
+                                _ptr(draft_stats), _ptr(draft_nucleus), _ptr(draft_tokens), _ptr(u_accept), _ptr(u_final), _ptr(n_accept),
                                 _ptr(out_tokens), ctypes.byref(rec) if rec is not None else None, _ptr(buf),
                                 buf.numel(), _stream(stream)))
 
@@ -397,8 +409,10 @@ def mtp_draft(model: DeviceModel, mtp: DeviceMtp, mtp_cache: PagedCache, k: int,
               verify_hidden: torch.Tensor, n_accept: torch.Tensor, out_tokens: torch.Tensor,
               u_draft: Optional[torch.Tensor], drafts: torch.Tensor, draft_logits: torch.Tensor, ws: Workspace,
               temperature: float = 1.0, dev_err: Optional[torch.Tensor] = None, stream=None,
-              draft_stats: Optional[torch.Tensor] = None, top_p: float = 1.0):
-    """top_p < 1 (sample mode): each draft is drawn from its row's nucleus (see gm.h)."""
+              draft_stats: Optional[torch.Tensor] = None, top_p: float = 1.0,
+              draft_nucleus: Optional[torch.Tensor] = None):
+    """top_p < 1 (sample mode): each draft is drawn from its row's nucleus (see gm.h), written
+    to draft_nucleus (new_nuclei) when given."""
     B = mtp_cache.B
     s = model.shape
     _need(verify_hidden, torch.float32, (B, k + 1, s.hidden), "verify_hidden")
@@ -406,13 +420,15 @@ def mtp_draft(model: DeviceModel, mtp: DeviceMtp, mtp_cache: PagedCache, k: int,
     _need(draft_logits, torch.float32, (B, k, s.vocab), "draft_logits")
     if draft_stats is not None:
         _need(draft_stats, torch.uint8, (B, k, ROW_STATS_BYTES), "draft_stats")
+    if draft_nucleus is not None:
+        _need(draft_nucleus, torch.uint8, (B, k, NUCLEUS_BYTES), "draft_nucleus")
     cs = mtp_cache.struct()
     n = workspace_size(GM_OP_MTP_DRAFT, model.cfg, B, k, mtp_cache.max_ctx)
     buf = ws.get(n)
     _check(lib().gm_mtp_draft(ctypes.byref(model.cfg), ctypes.byref(mtp.struct), ctypes.byref(model.struct),
                               ctypes.byref(cs), B, k, mode, float(temperature), float(top_p), _ptr(verify_hidden),
                               _ptr(n_accept),
-                              _ptr(out_tokens), _ptr(u_draft), _ptr(drafts), _ptr(draft_logits), _ptr(draft_stats),
+                              _ptr(out_tokens), _ptr(u_draft), _ptr(drafts), _ptr(draft_logits), _ptr(draft_stats), _ptr(draft_nucleus),
                               _ptr(buf),
                               buf.numel(), _ptr(dev_err), _stream(stream)))
 

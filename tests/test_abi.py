@@ -56,7 +56,8 @@ def test_spec_accept_rejects_bad_arguments():
                                   ua=FAKE, uf=FAKE, n=FAKE, out=FAKE, ws=ws, nbytes=1 << 30), **kw)
 
     def call(a):
-        return L.gm_spec_accept(a["B"], a["k"], a["V"], a["mode"], a["T"], a["top_p"], a["tl"], a["dl"], None, a["dt"],
+        return L.gm_spec_accept(a["B"], a["k"], a["V"], a["mode"], a["T"], a["top_p"], a["tl"], a["dl"], None, None,
+                                a["dt"],
                                 a["ua"], a["uf"], a["n"], a["out"], a.get("rec"), a["ws"], a["nbytes"], None)
 
     assert call(args(k=16)) == gm.GM_ERR_INVALID_ARG
@@ -123,19 +124,19 @@ def test_mtp_and_attention_reject_bad_arguments():
     mtp = gm.MtpWeights(FAKE, FAKE, FAKE, FAKE, gm.LayerWeights(*([FAKE] * 8)))
     c = _FakeCache(1, 100)
     st = L.gm_mtp_draft(ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(c.desc), 4, 3,
-                        gm.GM_SAMPLE, 1.0, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, None, FAKE, 1 << 30, None, None)
+                        gm.GM_SAMPLE, 1.0, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, None, None, FAKE, 1 << 30, None, None)
     assert st == gm.GM_ERR_INVALID_ARG and "u_draft" in gm.last_error()
     c2 = _FakeCache(1, 150)                                         # 150 + 2k + 1 > 160
     st = L.gm_mtp_draft(ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(c2.desc), 4, 5,
-                        gm.GM_GREEDY, 1.0, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, None, FAKE, 1 << 30, None, None)
+                        gm.GM_GREEDY, 1.0, 1.0, FAKE, FAKE, FAKE, None, FAKE, FAKE, None, None, FAKE, 1 << 30, None, None)
     assert st == gm.GM_ERR_CAPACITY
     for bad in (0.0, 2.0):
         st = L.gm_mtp_draft(ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(c.desc), 4, 3,
-                            gm.GM_SAMPLE, 1.0, bad, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None, None)
+                            gm.GM_SAMPLE, 1.0, bad, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, FAKE, 1 << 30, None, None)
         assert st == gm.GM_ERR_INVALID_ARG and "top_p" in gm.last_error()
     # top-p draws do not produce the row statistics of the accept handoff
     st = L.gm_mtp_draft(ctypes.byref(cfg), ctypes.byref(mtp), ctypes.byref(w), ctypes.byref(c.desc), 4, 3,
-                        gm.GM_SAMPLE, 1.0, 0.7, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None, None)
+                        gm.GM_SAMPLE, 1.0, 0.7, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None, None)
     assert st == gm.GM_ERR_UNSUPPORTED and "draft_stats" in gm.last_error()
     # reconstruction: K >= 1, inputs, and room for the K chain entries past max_ctx
     rc = lambda cache, K, hid=FAKE, toks=FAKE, dr=FAKE: L.gm_mtp_reconstruct(

@@ -112,3 +112,49 @@ def test_tiny_top_p_is_greedy():
     np.testing.assert_array_equal(n, ng)
     np.testing.assert_array_equal(out, outg)
     assert 0 < n.mean() < k
+
+
+def test_top_p_nucleus_handoff():
+    # gm_mtp_draft's nuclei handed to gm_spec_accept stand in for the accept's own passes
+    # over the draft rows: the same decisions and tokens, bit for bit
+    need_gpu()
+    from helpers import device_cache
+    shape = synth.QWEN3_4B_LAYER
+    W, Wm = synth.model_weights(shape), synth.mtp_weights(shape)
+    B, k, top_p = 32, 3, 0.7
+    g = np.random.default_rng(21)
+    lens = g.integers(1, 600, B)
+    ks, vs = synth.kv_prefix(shape, lens, layer=500)
+    hidden = g.standard_normal((B, k + 1, shape.hidden)).astype(np.float32)
+    n0 = g.integers(0, k + 1, B).astype(np.int32)
+    out0 = g.integers(0, shape.vocab, (B, k + 1)).astype(np.int32)
+    ua, uf, ud = synth.uniforms(B, k, 4, "handoff")
+    model, mtp = gm.DeviceModel(shape, W), gm.DeviceMtp(shape, Wm)
+    cache = device_cache(shape, [(ks, vs)], lens, 2 * k + 2)
+    drafts = torch.zeros((B, k), dtype=torch.int32, device="cuda")
+    dlog = torch.zeros((B, k, shape.vocab), dtype=torch.float32, device="cuda")
+    nuc = gm.new_nuclei(B, k)
+    gm.mtp_draft(model, mtp, cache, k, gm.GM_SAMPLE, t32(hidden), i32(n0), i32(out0), t32(ud), drafts, dlog,
+                 gm.Workspace(), top_p=top_p, draft_nucleus=nuc)
+    zt = t32(_logits((B, k + 1, shape.vocab), "normal", "handoff-t"))
+    res = []
+    for handoff in (None, nuc):
+        n = torch.zeros(B, dtype=torch.int32, device="cuda")
+        out = torch.zeros((B, k + 1), dtype=torch.int32, device="cuda")
+        gm.spec_accept(zt, dlog, drafts, t32(ua), t32(uf), n, out, gm.GM_SAMPLE, gm.Workspace(), top_p=top_p,
+                       draft_nucleus=handoff)
+        torch.cuda.synchronize()
+        res.append((n.cpu().numpy(), out.cpu().numpy()))
+    np.testing.assert_array_equal(res[0][0], res[1][0])
+    np.testing.assert_array_equal(res[0][1], res[1][1])
+    # the handed-over nuclei hold the head's own masses: every draft lies in its nucleus
+    h = nuc.cpu().numpy().reshape(B, k, 24)
+    key = h[..., 16:20].copy().view(np.uint32)[..., 0]
+    last = h[..., 20:24].copy().view(np.int32)[..., 0]
+    z = dlog.cpu().numpy()
+    d = drafts.cpu().numpy()
+    zd = np.take_along_axis(z, d[..., None], -1)[..., 0].astype(np.float32)
+    u = zd.view(np.uint32)
+    okey = np.where(u & 0x80000000, ~u, u | 0x80000000).astype(np.uint32)
+    assert ((okey > key) | ((okey == key) & (d <= last))).all()
+    print("[top-p handoff] mean accepted %.2f" % res[0][0].mean(), flush=True)

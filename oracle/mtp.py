@@ -3,12 +3,12 @@
 Test infrastructure: imported only by the tests, the smoke check and the
 benchmark's CPU-baseline leg.
 
-The head (App. "Models and Draft Heads") drafts one position at a time from
-the hidden state and the token embedding of the position before it: the two
-are normalised by separate RMSNorms, concatenated (hidden first), projected
-2H -> H by a bias-free linear layer and passed through one decoder layer that
-keeps a KV cache of its own, one entry per position.  Embedding and output
-head are the backbone's.  Reading where the paper is silent: one final
+The head (App. "Models and Draft Heads") is recurrent: each step consumes one
+(conditioning hidden, token) pair.  Each half gets its own RMSNorm, the two
+results are joined with the hidden half first, a bias-free linear map takes
+the 2H values to H, and a single decoder layer with a private KV cache (one
+entry per position) follows.  The token embedding and the output head are
+shared with the backbone.  Reading where the paper is silent: one final
 RMSNorm precedes the shared LM head, and the hidden carried along the chain
 is the decoder layer's output before that norm.
 
@@ -36,9 +36,15 @@ alone: depth 1 feeds the recorded start pair at slot s, depth j feeds
 (g_{j-1}, d_{j-1}) at slot s + j - 1, each rotated at its slot + 1, and every
 depth sees only the prefix and its own chain's earlier entries.
 
-Parity beyond the pass-through special cases in the tests is unpinned: the
-paper describes the head's composition in prose only.  The reconstruction is
-further pinned by reproducing the drafting's own distributions.
+Pins (tests/test_oracle_mtp.py): pass-through special cases fix the concat
+order, the shared embedding and head, the final norm and the chain's feed; two
+special cases in which the decoder layer has a closed form that reads its
+cache (uniform attention with W_q = W_k = 0; scores a b cos(P - P') with Q/K in
+the first rotary pair only) fix which (hidden, token) pair fills every extend
+slot, what each row sees, and every entry's rotary position.  The decoder
+layer itself is the target's, pinned against a float64 Hugging Face decoder.
+The reconstruction is further pinned by reproducing the drafting's own
+distributions.
 """
 from __future__ import annotations
 

@@ -138,7 +138,7 @@ extern "C" size_t gm_workspace_size(int op, const gm_model_config *cfg, int B, i
       if (k < 1 || check_config(cfg, B, k) != GM_OK) return 0;
       return plan_mtp(*cfg, B, k, max_ctx).total;
     case GM_OP_DCA_LOSS:
-      if (B < 0 || k < 1 || k > kMaxK || cfg->vocab < 1 || cfg->vocab > kMaxVocab) return 0;
+      if (!cfg || k < 1 || cfg->vocab < 1 || cfg->vocab > kMaxVocab) return 0;
       return dca_workspace(B, k, cfg->vocab);
     default:
       return 0;

@@ -223,3 +223,11 @@ def test_dca_loss_rejects_bad_arguments():
     cfg = gm.ModelConfig()
     cfg.vocab = 151936
     assert gm.workspace_size(gm.GM_OP_DCA_LOSS, cfg, 1024, 3, 0) > gm.workspace_size(gm.GM_OP_DCA_LOSS, cfg, 8, 3, 0)
+
+
+def test_workspace_size_null_config():
+    # every op reports 0 for a NULL config instead of reading through it
+    L = gm.lib()
+    for op in (gm.GM_OP_VERIFY_FORWARD, gm.GM_OP_VERIFY_ATTENTION, gm.GM_OP_SPEC_ACCEPT, gm.GM_OP_MTP_DRAFT,
+               gm.GM_OP_DCA_LOSS, gm.GM_OP_MTP_RECONSTRUCT):
+        assert L.gm_workspace_size(op, None, 8, 3, 1024) == 0

@@ -54,7 +54,7 @@ def log(msg):
 
 
 # ----------------------------------------------------------------------------- accounting
-def accounting(wl, lens, top_p=1.0):
+def accounting(wl, lens, top_p=1.0, record=0, target_stats=False):
     """Algorithmic flops and HBM bytes per step, per kernel name."""
     s, B, k = wl.shape, wl.batch, wl.k
     R, M = k + 1, wl.batch * (k + 1)
@@ -81,10 +81,13 @@ def accounting(wl, lens, top_p=1.0):
         put("gemm_down", gemm(M, H, F, 4, add=True), L)
         put("gemm_lm_head", gemm(M, V, H, 4), 1)
     put("attn_verify", (attn_flops, kv_bytes + 2.0 * 2 * M * qd), L)
-    # the target rows; the draft rows' statistics come from the draft head when it runs in the step
-    # (not under top-p, whose draws produce none)
+    # rows the accept's statistics pass reads: the target rows' statistics come from the verify
+    # forward's LM-head epilogue (unless a cycle record needs the pass's run maxima); the draft
+    # rows' from the draft head when it runs in the step (not under top-p, whose draws produce none)
     handoff = wl.with_mtp and top_p >= 1.0
-    put("accept_row_stats", (0.0, 4.0 * B * ((k + 1) if handoff else (2 * k + 1)) * V), 1)
+    rows = (0 if (target_stats and wl.name != "long_ctx" and not record) else k + 1) + (0 if handoff else k)
+    if rows:
+        put("accept_row_stats", (0.0, 4.0 * B * rows * V), 1)
     if top_p < 1.0:   # three passes over every target and draft row (the selection's bins)
         put("accept_nucleus", (0.0, 3 * 4.0 * B * (2 * k + 1) * V), 1)
     if wl.with_mtp:
@@ -106,7 +109,7 @@ def accounting(wl, lens, top_p=1.0):
 class Step:
     """Device state of one workload and the enqueue of one step."""
 
-    def __init__(self, wl, mode, device="cuda", record=0, top_p=1.0):
+    def __init__(self, wl, mode, device="cuda", record=0, top_p=1.0, target_stats=False):
         import torch
         from paper_2609_16648_amd import gm
         self.torch, self.gm, self.wl = torch, gm, wl
@@ -158,6 +161,9 @@ class Step:
             self.W = synth.model_weights(s, threads=16)
             self.model = gm.DeviceModel(s, self.W, device)
             self.logits = torch.empty((B, k + 1, V), dtype=torch.float32, device=device)
+            # optionally the target rows' softmax statistics from the LM head's epilogue, for the
+            # accept (in place of its pass over the target rows)
+            self.tstats = gm.new_row_stats(B, k + 1, device) if target_stats else None
             self.hidden = torch.empty((B, k + 1, s.hidden), dtype=torch.float32, device=device)
             if wl.with_mtp:
                 # zq stands in for the draft logits the previous step's head wrote; the head
@@ -208,10 +214,12 @@ class Step:
                            record=self.record, top_p=self.top_p)
             gm.kv_commit(self.cache, k, self.n, self.slots)
             return
-        gm.verify_forward(self.model, self.cache, self.tokens, self.logits, self.hidden, self.ws_v)
+        gm.verify_forward(self.model, self.cache, self.tokens, self.logits, self.hidden, self.ws_v,
+                          target_stats=self.tstats)
         handoff = wl.with_mtp and self.top_p >= 1.0
         gm.spec_accept(self.logits, self.zq, self.drafts, self.ua, self.uf, self.n, self.out, self.mode, self.ws_a,
-                       draft_stats=self.zq_stats if handoff else None, record=self.record, top_p=self.top_p)
+                       draft_stats=self.zq_stats if handoff else None, record=self.record, top_p=self.top_p,
+                       target_stats=self.tstats)
         gm.kv_commit(self.cache, k, self.n, self.slots)
         if wl.with_mtp:
             self.mcache.seq_lens.copy_(self.lens0)
@@ -421,6 +429,8 @@ def main():
                     help="also time the draft-path reconstruction of R recorded cycles (the paper's chunks: 1024)")
     ap.add_argument("--top-p", type=float, default=1.0,
                     help="top-p of the accept and the draft (the paper's evaluation decodes at 0.7; 1: off)")
+    ap.add_argument("--target-stats", action="store_true",
+                    help="hand the verify LM head's epilogue statistics to the accept (off: the accept's own pass)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also time a plain device copy of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -434,7 +444,7 @@ def main():
     gm.lib()
     torch.cuda.set_device(0)
     wl = synth.WORKLOADS[args.workload]
-    step = Step(wl, args.mode, record=args.record, top_p=args.top_p)
+    step = Step(wl, args.mode, record=args.record, top_p=args.top_p, target_stats=args.target_stats)
 
     for _ in range(args.warmup):
         step()
@@ -466,7 +476,7 @@ def main():
     committed = int((n + 1).sum())
     value = committed / (ms / 1e3)
 
-    acc = accounting(wl, step.lens, args.top_p)
+    acc = accounting(wl, step.lens, args.top_p, args.record, args.target_stats)
     kernels = {}
     for name, (launches, tot) in sorted(per_kernel.items(), key=lambda kv: -kv[1][1]):
         ms_step = tot / probe_steps
@@ -537,7 +547,8 @@ def main():
             "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
             "config": {"workload": args.workload, "description": DESCRIPTIONS[args.workload],
                        "batch": wl.batch, "k": wl.k, "accept_mode": args.mode, "parallelism": "none (1 GPU)",
-                       "record_topk": args.record, "top_p": args.top_p},
+                       "record_topk": args.record, "top_p": args.top_p,
+                       "target_stats": args.target_stats},
             "roofline": roof, "summary": summary, "kernels": kernels}
     if not args.no_cpu_baseline:
         weights = None

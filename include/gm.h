@@ -197,11 +197,17 @@ size_t gm_workspace_size(int op, const gm_model_config *cfg, int B, int k, int m
  * (row i is the target's distribution for the token after block position i)
  * and hidden [B][k+1][H] float32, the last layer's output before the final
  * RMSNorm (the feature the MTP head consumes).
- * Errors: GM_ERR_CAPACITY if max_ctx + k + 1 > max_pages_per_seq * page_size. */
+ * target_stats [B][k+1] (may be NULL): also the softmax statistics of every
+ * logits row at `temperature` (gm_row_stats), taken in the LM head's epilogue;
+ * gm_spec_accept takes them for the same rows and temperature in place of its
+ * pass over the target rows (Sec. 2.2, Eq. accept-rule: p's normaliser and
+ * arg-max).  temperature is read only when target_stats is given (> 0).
+ * Errors: GM_ERR_CAPACITY if max_ctx + k + 1 > max_pages_per_seq * page_size;
+ * GM_ERR_INVALID_ARG for target_stats with temperature <= 0. */
 gm_status gm_verify_forward(const gm_model_config *cfg, const gm_model_weights *w,
                             const gm_kv_cache *cache, int B, int k, const int32_t *tokens,
-                            float *logits, float *hidden, void *ws, size_t ws_bytes,
-                            int32_t *dev_err, void *stream);
+                            float *logits, float *hidden, float temperature, gm_row_stats *target_stats,
+                            void *ws, size_t ws_bytes, int32_t *dev_err, void *stream);
 
 /* Verify attention of one layer: the query at block position i of sequence b
  * attends causally to cache positions 0 .. m_b + i (the committed prefix and
@@ -241,6 +247,11 @@ gm_status gm_verify_attention(const gm_model_config *cfg, const gm_kv_cache *cac
  *   of softmax(draft_logits[b][i] / T) at this temperature, as gm_mtp_draft
  *   writes them.  Given, they stand in for a pass over the draft rows; the
  *   caller guarantees that they describe these draft_logits.
+ * target_stats [B][k+1] (may be NULL): the statistics of softmax(target_logits[b][i] / T)
+ *   at this temperature, as gm_verify_forward writes them.  Given, they stand in for
+ *   the pass over the target rows (that pass still runs when a record is requested,
+ *   whose selection needs it); the caller guarantees that they describe these
+ *   target_logits.
  * Outputs: n_accept [B] in [0, k]; out_tokens [B][k+1] = d_0..d_{n-1}, final, -1 pad.
  * record (host struct, may be NULL): also writes the cycle record's top-k
  *   log-probabilities of the target rows 0..k-1 (see gm_record), taken in the same
@@ -249,7 +260,8 @@ gm_status gm_verify_attention(const gm_model_config *cfg, const gm_kv_cache *cac
  * The logits rows are read in place; no probability matrix is written. */
 gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature, float top_p,
                          const float *target_logits, const float *draft_logits,
-                         const gm_row_stats *draft_stats, const gm_nucleus *draft_nucleus,
+                         const gm_row_stats *target_stats, const gm_row_stats *draft_stats,
+                         const gm_nucleus *draft_nucleus,
                          const int32_t *draft_tokens, const float *u_accept, const float *u_final,
                          int32_t *n_accept, int32_t *out_tokens, const gm_record *record, void *ws,
                          size_t ws_bytes, void *stream);

@@ -157,7 +157,8 @@ static_assert(sizeof(gm_nucleus) == sizeof(NucRow) && offsetof(gm_nucleus, m) ==
 
 extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature, float top_p,
                                     const float *target_logits,
-                                    const float *draft_logits, const gm_row_stats *draft_stats,
+                                    const float *draft_logits, const gm_row_stats *target_stats,
+                                    const gm_row_stats *draft_stats,
                                     const gm_nucleus *draft_nucleus,
                                     const int32_t *draft_tokens, const float *u_accept,
                                     const float *u_final, int32_t *n_accept, int32_t *out_tokens,
@@ -189,7 +190,15 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
   const float inv_t = 1.0f / temperature;
   const bool rec = record && k > 0;
   float *submax = rec ? (float *)(w + p.submax) : nullptr;
-  launch_row_stats("accept_row_stats", target_logits, V, B * (k + 1), V, inv_t, tstat, s, submax);
+  // p's statistics: the verify forward's own (one per row) when the caller has them and no record
+  // needs the pass's run maxima, else a pass over the target rows
+  int nch_t = stat_chunks(V);
+  if (target_stats && !rec) {
+    tstat = (RowStat *)target_stats;
+    nch_t = 1;
+  } else {
+    launch_row_stats("accept_row_stats", target_logits, V, B * (k + 1), V, inv_t, tstat, s, submax);
+  }
   // q's statistics: the draft head's own (one per row) when the caller has them, else a pass over the rows
   int nch_d = stat_chunks(V);
   const bool top_p_on = mode == GM_SAMPLE && top_p < 1.f;
@@ -209,7 +218,7 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
   if (top_p_on) {
     tnuc = (NucRow *)(w + p.tnuc);
     unsigned long long *part = (unsigned long long *)(w + p.nucpart);
-    launch_nucleus("accept_nucleus", B * (k + 1), V, inv_td, (double)top_p, target_logits, V, tstat, stat_chunks(V),
+    launch_nucleus("accept_nucleus", B * (k + 1), V, inv_td, (double)top_p, target_logits, V, tstat, nch_t,
                    tnuc, 1, part, s);
     if (k > 0 && draft_nucleus) {
       dnuc = (NucRow *)draft_nucleus;
@@ -219,7 +228,8 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
                      s);
     }
   }
-  launch_accept_decide(B, k, V, mode, inv_t, inv_td, target_logits, draft_logits, tstat, dstat, nch_d, tnuc, dnuc,
+  launch_accept_decide(B, k, V, mode, inv_t, inv_td, target_logits, draft_logits, tstat, nch_t, dstat, nch_d, tnuc,
+                       dnuc,
                        draft_tokens, u_accept, u_final, n_accept, out_tokens, sel, s);
   if (rec)
     launch_record_topk(B, k, V, inv_t, record->topk, target_logits, tstat, submax, record->logp, record->ids, s);
@@ -285,8 +295,9 @@ extern "C" gm_status gm_verify_attention(const gm_model_config *cfg, const gm_kv
 
 // ---------------------------------------------------------------- gm_verify_forward
 extern "C" gm_status gm_verify_forward(const gm_model_config *cfg, const gm_model_weights *w, const gm_kv_cache *cache,
-                                       int B, int k, const int32_t *tokens, float *logits, float *hidden, void *ws,
-                                       size_t ws_bytes, int32_t *dev_err, void *stream) {
+                                       int B, int k, const int32_t *tokens, float *logits, float *hidden,
+                                       float temperature, gm_row_stats *target_stats, void *ws, size_t ws_bytes,
+                                       int32_t *dev_err, void *stream) {
   gm_status st = check_config(cfg, B, k);
   if (st != GM_OK) return st;
   if (!w || !w->embed || !w->final_norm || !w->lm_head || !w->layers) return fail(GM_ERR_INVALID_ARG, "null model weights");
@@ -296,10 +307,12 @@ extern "C" gm_status gm_verify_forward(const gm_model_config *cfg, const gm_mode
   if (st != GM_OK) return st;
   if (B == 0) return GM_OK;
   if (!tokens || !logits || !hidden) return fail(GM_ERR_INVALID_ARG, "null tokens / logits / hidden");
+  if (target_stats && !(temperature > 0.f)) return fail(GM_ERR_INVALID_ARG, "target_stats need a temperature > 0");
   const ForwardPlan p = plan_forward(*cfg, B, k, cache->max_ctx);
   st = check_ws(ws, ws_bytes, p.total);
   if (st != GM_OK) return st;
-  run_verify_forward(*cfg, *w, *cache, B, k, tokens, logits, hidden, p, (char *)ws, dev_err, (hipStream_t)stream);
+  run_verify_forward(*cfg, *w, *cache, B, k, tokens, logits, hidden, target_stats ? 1.0f / temperature : 1.0f,
+                     (RowStat *)target_stats, p, (char *)ws, dev_err, (hipStream_t)stream);
   return check_launch("gm_verify_forward");
 }
 

@@ -84,6 +84,8 @@ ForwardPlan plan_forward(const gm_model_config &cfg, int B, int k, int max_ctx) 
   p.attn_plan = plan_attention(cfg, B, k + 1, max_ctx);
   p.attn_ws = c.take(p.attn_plan.total);
   p.part = c.take(part_bytes(cfg, (int)M, false));
+  // the LM head's tile statistics when the caller wants the rows' softmax statistics
+  p.tiles = c.take(sizeof(RowStat) * M * plan_lm_head(cfg.dtype, (int)M, cfg.vocab, cfg.hidden).tiles);
   p.total = c.off;
   return p;
 }
@@ -91,8 +93,8 @@ ForwardPlan plan_forward(const gm_model_config &cfg, int B, int k, int max_ctx) 
 // One target forward over the block of every sequence.  The residual stream
 // lives in `hidden` (float32); it is the last layer's output at the end.
 void run_verify_forward(const gm_model_config &cfg, const gm_model_weights &w, const gm_kv_cache &c, int B, int k,
-                        const int32_t *tokens, float *logits, float *hidden, const ForwardPlan &p, char *ws,
-                        int32_t *dev_err, hipStream_t s) {
+                        const int32_t *tokens, float *logits, float *hidden, float inv_t, RowStat *target_stats,
+                        const ForwardPlan &p, char *ws, int32_t *dev_err, hipStream_t s) {
   const int R = k + 1, M = B * R, H = cfg.hidden, F = cfg.ffn, V = cfg.vocab, dt = cfg.dtype;
   const int qd = cfg.n_heads * cfg.head_dim;
   void *nbuf = ws + p.nbuf, *act = ws + p.act, *q = ws + p.q, *attn = ws + p.attn;
@@ -118,7 +120,14 @@ void run_verify_forward(const gm_model_config &cfg, const gm_model_weights &w, c
     launch_gemm("gemm_gate_up", dt, EPI_SWIGLU, M, F, H, nbuf, H, L.w_gate_up, act, F, part, s);
     gemm_norm("gemm_down", dt, EPI_ADD_F32, M, H, F, act, F, L.w_down, x, part, next_norm(l + 1), eps, nbuf, s);
   }
-  launch_gemm("gemm_lm_head", dt, EPI_STORE_F32, M, V, H, nbuf, H, w.lm_head, logits, V, part, s);
+  if (target_stats) {
+    // the rows' softmax statistics in the LM head's epilogue (per tile of ids), then one per row
+    RowStat *tiles = (RowStat *)(ws + p.tiles);
+    launch_gemm("gemm_lm_head", dt, EPI_STATS, M, V, H, nbuf, H, w.lm_head, logits, V, part, s, tiles, inv_t);
+    launch_tile_combine(M, plan_lm_head(dt, M, V, H).tiles, tiles, target_stats, 1, s);
+  } else {
+    launch_gemm("gemm_lm_head", dt, EPI_STORE_F32, M, V, H, nbuf, H, w.lm_head, logits, V, part, s);
+  }
 }
 
 // ---------------------------------------------------------------- MTP draft

@@ -114,13 +114,14 @@ void launch_gather_rows(int M_out, int R, int C, size_t elem, const void *src, c
 
 // ---------------------------------------------------------------- orchestration
 struct ForwardPlan {
-  size_t nbuf, act, qkv, q, attn, attn_ws, part, total;
+  size_t nbuf, act, qkv, q, attn, attn_ws, part, tiles, total;
   AttnPlan attn_plan;
 };
 ForwardPlan plan_forward(const gm_model_config &cfg, int B, int k, int max_ctx);
+// target_stats (may be null): one RowStat per logits row at 1 / inv_t, from the LM head's epilogue
 void run_verify_forward(const gm_model_config &cfg, const gm_model_weights &w, const gm_kv_cache &c, int B, int k,
-                        const int32_t *tokens, float *logits, float *hidden, const ForwardPlan &p, char *ws,
-                        int32_t *dev_err, hipStream_t s);
+                        const int32_t *tokens, float *logits, float *hidden, float inv_t, RowStat *target_stats,
+                        const ForwardPlan &p, char *ws, int32_t *dev_err, hipStream_t s);
 
 struct MtpPlan {
   size_t u, x, xg, nbuf, act, qkv, q, attn, attn_g, attn_ws, stat, nuc, sel, wsum, psum, nucpart, part, total;

@@ -67,32 +67,6 @@ __device__ __forceinline__ int xcd_remap(int bid, int T) {
   return x * q + (x < rem ? x : rem) + slot;
 }
 
-// Reductions over the 16 lanes of one DPP row (the lanes j of a C-tile row): xor 1
-// and xor 2 inside quads, then the half-row and row mirrors.
-__device__ __forceinline__ int dpp_i(int v, int ctrl_sel) {
-  switch (ctrl_sel) {
-    case 0: return __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);    // quad_perm [1,0,3,2]
-    case 1: return __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);    // quad_perm [2,3,0,1]
-    case 2: return __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false);   // row_half_mirror
-    default: return __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, false);  // row_mirror
-  }
-}
-__device__ __forceinline__ float row16_max(float v) {
-#pragma unroll
-  for (int c = 0; c < 4; ++c) v = fmaxf(v, __int_as_float(dpp_i(__float_as_int(v), c)));
-  return v;
-}
-__device__ __forceinline__ int row16_min(int v) {
-#pragma unroll
-  for (int c = 0; c < 4; ++c) v = min(v, dpp_i(v, c));
-  return v;
-}
-__device__ __forceinline__ float row16_sum(float v) {
-#pragma unroll
-  for (int c = 0; c < 4; ++c) v += __int_as_float(dpp_i(__float_as_int(v), c));
-  return v;
-}
-
 // MT: 16-row tiles per compute wave; NT: 16-column strips per compute wave;
 // WM: compute waves along M (1 or 2); SW: weights loaded non-temporally (one M
 // tile).  Waves 0-3 compute; wave 4 only stages
@@ -231,6 +205,64 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
     }
   }
 
+  // The statistics come first: the barriers they need wait for every outstanding memory
+  // operation, and the logits' stores, issued last, then drain after the waves have left
+  // (the next workgroup on this CU starts streaming meanwhile).
+  if (EPI == EPI_STATS) {
+    // Softmax statistics of this workgroup's kStatCols columns, per row.  The A buffers are
+    // free once the K loop is done: the tile of z / T goes there in parts of RP rows (row
+    // stride LS floats), then each thread reduces one row over the kStatCols columns in
+    // ascending id order -- the max, the first id attaining it, and the float64 sum of
+    // float32 terms exp(z / T - max).  No cross-lane reductions.
+    constexpr int RP = BM >= 256 ? 128 : 64;
+    constexpr int LS = kStatCols + 4;   // a lane's float4 reads of consecutive rows fall on distinct banks
+    static_assert(RP * LS * 4 <= kGemmBufs * BM * BKA * 2, "a part of the tile fits the A buffers");
+    float *tl = reinterpret_cast<float *>(&As[0][0]);
+#pragma unroll
+    for (int h = 0; h < BM / RP; ++h) {
+      __syncthreads();
+      if (w < 4) {
+#pragma unroll
+        for (int a = 0; a < MT; ++a) {
+          const int r0 = wm * 16 * MT + 16 * a;
+          if (r0 < h * RP || r0 >= (h + 1) * RP) continue;
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+              tl[(r0 + 4 * g4 + r - h * RP) * LS + wn * 16 * NT + 16 * t + j] = acc[a][t][r] * g.inv_t;
+        }
+      }
+      __syncthreads();
+      for (int rl = tid; rl < RP; rl += kGemmThreads) {
+        const int m = m0 + h * RP + rl;
+        if (m >= g.M) continue;
+        const float4 *src = reinterpret_cast<const float4 *>(tl + rl * LS);
+        float mx = -INFINITY;
+        int arg = 0;
+#pragma unroll 8
+        for (int c = 0; c < kStatCols / 4; ++c) {
+          const float4 v = src[c];
+          if (v.x > mx) { mx = v.x; arg = 4 * c; }
+          if (v.y > mx) { mx = v.y; arg = 4 * c + 1; }
+          if (v.z > mx) { mx = v.z; arg = 4 * c + 2; }
+          if (v.w > mx) { mx = v.w; arg = 4 * c + 3; }
+        }
+        double sum = 0.0;
+#pragma unroll 8
+        for (int c = 0; c < kStatCols / 4; ++c) {
+          const float4 v = src[c];
+          sum += (double)expf(v.x - mx) + (double)expf(v.y - mx) + (double)expf(v.z - mx) + (double)expf(v.w - mx);
+        }
+        RowStat o;
+        o.max = mx;
+        o.argmax = nt * kStatCols + arg;
+        o.sum = sum;
+        g.stats[(long)m * (g.Nw / kStatCols) + nt] = o;
+      }
+    }
+  }
+
   if (w < 4) {
   // lane holds C[row 16a + 4 g4 + r][col 16t + j] of the wave tile
 #pragma unroll
@@ -261,67 +293,6 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
     }
   }
 
-  }
-
-  if (EPI == EPI_STATS) {
-    // softmax statistics of this workgroup's kStatCols columns, per row: every wave
-    // reduces its own columns over the 16 lanes of a row (branch-free DPP reductions:
-    // the max, then the lowest column attaining it, then the float32 sum of its
-    // terms), the waves of a row meet in LDS (A's buffers are free once the K loop
-    // is done) and combine in float64
-    __syncthreads();
-    float *sm = reinterpret_cast<float *>(&As[0][0]);          // [BM][WN][3]
-    if (w < 4) {
-#pragma unroll
-    for (int a = 0; a < MT; ++a) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float v[NT], vmax = -INFINITY;
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          v[t] = acc[a][t][r] * g.inv_t;
-          vmax = fmaxf(vmax, v[t]);
-        }
-        vmax = row16_max(vmax);
-        int varg = 0x7fffffff;
-#pragma unroll
-        for (int t = NT - 1; t >= 0; --t) varg = v[t] == vmax ? strip[t] * 16 + j : varg;   // strips ascend with t
-        varg = row16_min(varg);
-        float s = 0.f;
-#pragma unroll
-        for (int t = 0; t < NT; ++t) s += expf(v[t] - vmax);
-        s = row16_sum(s);
-        if (j == 0) {
-          float *e = sm + ((wm * 16 * MT + 16 * a + 4 * g4 + r) * WN + wn) * 3;
-          e[0] = vmax;
-          e[1] = s;
-          e[2] = __int_as_float(varg);
-        }
-      }
-    }
-    }
-    __syncthreads();
-    for (int rl = tid; rl < BM; rl += 4 * kWave) {
-      const int m = m0 + rl;
-      if (m >= g.M) continue;
-      const float *e = sm + rl * WN * 3;
-      float M = e[0];
-      int arg = __float_as_int(e[2]);
-#pragma unroll
-      for (int q = 1; q < WN; ++q) {
-        const float mq = e[3 * q];
-        const int aq = __float_as_int(e[3 * q + 2]);
-        if (mq > M || (mq == M && aq < arg)) { M = mq; arg = aq; }
-      }
-      double S = 0.0;
-#pragma unroll
-      for (int q = 0; q < WN; ++q) S += (double)e[3 * q + 1] * exp((double)e[3 * q] - (double)M);
-      RowStat o;
-      o.max = M;
-      o.argmax = arg;
-      o.sum = S;
-      g.stats[(long)m * (g.Nw / kStatCols) + nt] = o;
-    }
   }
 }
 

@@ -101,10 +101,12 @@ constexpr int kRecSub = 256;       // ids per run maximum (one wave's load in th
 constexpr int kRecMaxTopk = 64;
 void launch_record_topk(int B, int k, int V, float inv_t, int topk, const float *logits, const RowStat *tstat,
                         const float *submax, uint16_t *logp, int32_t *ids, hipStream_t s);
-// dstat holds nch_d RowStats per draft row (chunk statistics, or one combined per row);
-// tnuc / dnuc (top-p, else null): the nuclei of the target and draft rows
+// one RowStat per row (at out[r * out_stride]) from `tiles` tile statistics per row
+void launch_tile_combine(int n_rows, int tiles, const RowStat *st, RowStat *out, int out_stride, hipStream_t s);
+// tstat / dstat hold nch_t / nch_d RowStats per target / draft row (chunk statistics, or one
+// combined per row); tnuc / dnuc (top-p, else null): the nuclei of the target and draft rows
 void launch_accept_decide(int B, int k, int V, int mode, float inv_t, double inv_td, const float *tlog,
-                          const float *dlog, const RowStat *tstat, const RowStat *dstat, int nch_d,
+                          const float *dlog, const RowStat *tstat, int nch_t, const RowStat *dstat, int nch_d,
                           const NucRow *tnuc, const NucRow *dnuc,
                           const int32_t *drafts, const float *u_accept, const float *u_final,
                           int32_t *n_accept, int32_t *out_tokens, RowSel *sel, hipStream_t s);

@@ -168,6 +168,43 @@ __device__ __forceinline__ void combine_stats(const RowStat *st, int nch, double
   am = a;
 }
 
+// One RowStat per row from its `tiles` tile statistics (ascending id ranges): the
+// largest max, the lowest id attaining it, and the normaliser rescaled to that max in
+// float64.  One wave per row; each lane takes every 64th tile in order, then fixed
+// shuffle trees combine the lanes, so the result does not depend on timing.
+__global__ __launch_bounds__(256) void tile_combine_kernel(int n_rows, int tiles, const RowStat *__restrict__ st,
+                                                           RowStat *__restrict__ out, int out_stride) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= n_rows) return;
+  const RowStat *t = st + (long)row * tiles;
+  float m = -INFINITY;
+  int am = 0x7fffffff;
+  for (int i = lane; i < tiles; i += kWave)
+    if (t[i].max > m) { m = t[i].max; am = t[i].argmax; }   // ascending ids: the first of equal maxima wins
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float mo = __shfl_xor(m, o, kWave);
+    const int ao = __shfl_xor(am, o, kWave);
+    if (mo > m || (mo == m && ao < am)) { m = mo; am = ao; }
+  }
+  double s = 0.0;
+  for (int i = lane; i < tiles; i += kWave) s += t[i].sum * exp((double)t[i].max - (double)m);
+  s = wave_sum(s);
+  if (lane == 0) {
+    RowStat o;
+    o.max = m;
+    o.argmax = am;
+    o.sum = s;
+    out[(long)row * out_stride] = o;
+  }
+}
+
+void launch_tile_combine(int n_rows, int tiles, const RowStat *st, RowStat *out, int out_stride, hipStream_t s) {
+  if (n_rows <= 0) return;
+  TraceScope ts("tile_combine", s);
+  hipLaunchKernelGGL(tile_combine_kernel, dim3((n_rows + 3) / 4), dim3(256), 0, s, n_rows, tiles, st, out, out_stride);
+}
+
 // ------------------------------------------------------------------ 2. accept decision
 // One wave per sequence.  Lane r <= k combines the chunk statistics of target
 // row r, lane k + 1 + r those of draft row r; lane i < k then evaluates the
@@ -278,14 +315,14 @@ __global__ __launch_bounds__(64) void accept_decide_kernel(int B, int k, int V, 
 }
 
 void launch_accept_decide(int B, int k, int V, int mode, float inv_t, double inv_td, const float *tlog,
-                          const float *dlog, const RowStat *tstat, const RowStat *dstat, int nch_d,
+                          const float *dlog, const RowStat *tstat, int nch_t, const RowStat *dstat, int nch_d,
                           const NucRow *tnuc, const NucRow *dnuc,
                           const int32_t *drafts, const float *u_accept, const float *u_final,
                           int32_t *n_accept, int32_t *out_tokens, RowSel *sel, hipStream_t s) {
   if (B <= 0) return;
   TraceScope ts("accept_decide", s);
   hipLaunchKernelGGL(accept_decide_kernel, dim3(B), dim3(64), 0, s, B, k, V, mode, inv_t, inv_td, tlog, dlog, tstat,
-                     dstat, stat_chunks(V), nch_d, tnuc, dnuc, drafts, u_accept, u_final, n_accept, out_tokens, sel);
+                     dstat, nch_t, nch_d, tnuc, dnuc, drafts, u_accept, u_final, n_accept, out_tokens, sel);
 }
 
 // ------------------------------------------------------------------ cycle record

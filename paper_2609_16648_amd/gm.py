@@ -81,14 +81,14 @@ def lib() -> ctypes.CDLL:
     L.gm_workspace_size.argtypes = [c_int, P(ModelConfig), c_int, c_int, c_int]
     L.gm_verify_forward.restype = c_int
     L.gm_verify_forward.argtypes = [P(ModelConfig), P(ModelWeights), P(KVCacheDesc), c_int, c_int, c_void_p,
-                                    c_void_p, c_void_p, c_void_p, c_size_t, c_void_p, c_void_p]
+                                    c_void_p, c_void_p, c_float, c_void_p, c_void_p, c_size_t, c_void_p, c_void_p]
     L.gm_verify_attention.restype = c_int
     L.gm_verify_attention.argtypes = [P(ModelConfig), P(KVCacheDesc), c_int, c_int, c_int, c_void_p, c_void_p,
                                       c_void_p, c_size_t, c_void_p, c_void_p]
     L.gm_spec_accept.restype = c_int
     L.gm_spec_accept.argtypes = [c_int, c_int, c_int, c_int, c_float, c_float, c_void_p, c_void_p, c_void_p,
                                  c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
-                                 c_size_t, c_void_p]
+                                 c_void_p, c_size_t, c_void_p]
     L.gm_kv_commit.restype = c_int
     L.gm_kv_commit.argtypes = [P(KVCacheDesc), c_int, c_int, c_void_p, c_void_p, c_void_p]
     L.gm_mtp_draft.restype = c_int
@@ -305,18 +305,23 @@ def workspace_size(op: int, cfg: ModelConfig, B: int, k: int, max_ctx: int) -> i
 
 # ------------------------------------------------------------------------ entry points
 def verify_forward(model: DeviceModel, cache: PagedCache, tokens: torch.Tensor, logits: torch.Tensor,
-                   hidden: torch.Tensor, ws: Workspace, dev_err: Optional[torch.Tensor] = None, stream=None):
+                   hidden: torch.Tensor, ws: Workspace, dev_err: Optional[torch.Tensor] = None, stream=None,
+                   target_stats: Optional[torch.Tensor] = None, temperature: float = 1.0):
+    """target_stats: optional [B, k+1] row statistics (new_row_stats) of the logits at `temperature`,
+    taken in the LM head's epilogue, for spec_accept(target_stats=...)."""
     B, k1 = tokens.shape
     s = model.shape
     _need(tokens, torch.int32, (B, k1), "tokens")
     _need(logits, torch.float32, (B, k1, s.vocab), "logits")
     _need(hidden, torch.float32, (B, k1, s.hidden), "hidden")
+    if target_stats is not None:
+        _need(target_stats, torch.uint8, (B, k1, ROW_STATS_BYTES), "target_stats")
     cs = cache.struct()
     n = workspace_size(GM_OP_VERIFY_FORWARD, model.cfg, B, k1 - 1, cache.max_ctx)
     buf = ws.get(n)
     _check(lib().gm_verify_forward(ctypes.byref(model.cfg), ctypes.byref(model.struct), ctypes.byref(cs), B, k1 - 1,
-                                   _ptr(tokens), _ptr(logits), _ptr(hidden), _ptr(buf), buf.numel(), _ptr(dev_err),
-                                   _stream(stream)))
+                                   _ptr(tokens), _ptr(logits), _ptr(hidden), float(temperature), _ptr(target_stats),
+                                   _ptr(buf), buf.numel(), _ptr(dev_err), _stream(stream)))
 
 
 def verify_attention(cfg: ModelConfig, cache: PagedCache, layer: int, q: torch.Tensor, out: torch.Tensor,
@@ -365,10 +370,11 @@ def spec_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor
                 u_accept: Optional[torch.Tensor], u_final: Optional[torch.Tensor], n_accept: torch.Tensor,
                 out_tokens: torch.Tensor, mode: int, ws: Workspace, temperature: float = 1.0, stream=None,
                 draft_stats: Optional[torch.Tensor] = None, record=None, top_p: float = 1.0,
-                draft_nucleus: Optional[torch.Tensor] = None):
+                draft_nucleus: Optional[torch.Tensor] = None, target_stats: Optional[torch.Tensor] = None):
     """record: optional (logp [B, k, topk] bfloat16, ids [B, k, topk] int32) for the cycle record;
     top_p < 1: the accept rule on the nuclei of p and q (see gm.h); draft_nucleus: the draft
-    rows' nuclei as mtp_draft wrote them (new_nuclei)."""
+    rows' nuclei as mtp_draft wrote them (new_nuclei); target_stats: the target rows' statistics
+    as verify_forward wrote them."""
     B, k1, V = target_logits.shape
     k = k1 - 1
     _need(target_logits, torch.float32, (B, k1, V), "target_logits")
@@ -381,6 +387,8 @@ def spec_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor
         _need(draft_stats, torch.uint8, (B, k, ROW_STATS_BYTES), "draft_stats")
     if draft_nucleus is not None:
         _need(draft_nucleus, torch.uint8, (B, k, NUCLEUS_BYTES), "draft_nucleus")
+    if target_stats is not None:
+        _need(target_stats, torch.uint8, (B, k1, ROW_STATS_BYTES), "target_stats")
     rec = None
     if record is not None:
         logp, ids = record
@@ -393,7 +401,7 @@ def spec_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor
     n = workspace_size(GM_OP_SPEC_ACCEPT, cfg, B, k, 0)
     buf = ws.get(n)
     _check(lib().gm_spec_accept(B, k, V, mode, float(temperature), float(top_p), _ptr(target_logits),
-                                _ptr(draft_logits),
+                                _ptr(draft_logits), _ptr(target_stats),
                                 _ptr(draft_stats), _ptr(draft_nucleus), _ptr(draft_tokens), _ptr(u_accept), _ptr(u_final), _ptr(n_accept),
                                 _ptr(out_tokens), ctypes.byref(rec) if rec is not None else None, _ptr(buf),
                                 buf.numel(), _stream(stream)))

@@ -56,7 +56,7 @@ def test_spec_accept_rejects_bad_arguments():
                                   ua=FAKE, uf=FAKE, n=FAKE, out=FAKE, ws=ws, nbytes=1 << 30), **kw)
 
     def call(a):
-        return L.gm_spec_accept(a["B"], a["k"], a["V"], a["mode"], a["T"], a["top_p"], a["tl"], a["dl"], None, None,
+        return L.gm_spec_accept(a["B"], a["k"], a["V"], a["mode"], a["T"], a["top_p"], a["tl"], a["dl"], None, None, None,
                                 a["dt"],
                                 a["ua"], a["uf"], a["n"], a["out"], a.get("rec"), a["ws"], a["nbytes"], None)
 
@@ -98,10 +98,10 @@ def test_verify_forward_rejects_bad_arguments():
     cfg = gm.model_config(shape)
     keep, w = _weights(2)
 
-    def call(cfg_=cfg, cache=None, B=4, k=3, nbytes=1 << 30):
+    def call(cfg_=cfg, cache=None, B=4, k=3, nbytes=1 << 30, T=1.0, stats=None):
         cache = cache or _FakeCache(2, 100)
         return L.gm_verify_forward(ctypes.byref(cfg_), ctypes.byref(w), ctypes.byref(cache.desc), B, k, FAKE, FAKE,
-                                   FAKE, FAKE, nbytes, None, None)
+                                   FAKE, T, stats, FAKE, nbytes, None, None)
 
     assert call(cache=_FakeCache(2, 157)) == gm.GM_ERR_CAPACITY      # 157 + 4 > 10 pages of 16
     assert "exceed" in gm.last_error()
@@ -113,6 +113,7 @@ def test_verify_forward_rejects_bad_arguments():
     assert call(cfg_=bad) == gm.GM_ERR_INVALID_ARG
     big_group = gm.model_config(synth.ModelShape(2, 256, 32, 2, 64, 1024, 1024, dtype="f32"))  # 16 * 4 rows ok
     assert call(cfg_=big_group, k=4) == gm.GM_ERR_UNSUPPORTED                               # 16 * 5 > 64
+    assert call(stats=FAKE, T=0.0) == gm.GM_ERR_INVALID_ARG and "temperature" in gm.last_error()
     assert call(B=0) == gm.GM_OK
 
 

@@ -146,3 +146,133 @@ def test_qwen_layer_bf16_block_is_causal(qwen_layer):
     np.testing.assert_array_equal(l0[:, :k], l1[:, :k])
     np.testing.assert_array_equal(h0[:, :k], h1[:, :k])
     assert (np.abs(l0[:, k] - l1[:, k]).max(-1) > 0).all()
+
+
+# ------------------------------------------------------------------ target statistics handoff
+def _stats_definition(z, temperature):
+    """gm_row_stats of rows of float32 logits by definition: max of z * (1/T) in float32,
+    the lowest id attaining it, sum of exp(z/T - max) in float64."""
+    inv_t = np.float32(1.0) / np.float32(temperature)
+    v = z.astype(np.float32) * inv_t
+    m = v.max(-1)
+    return m, v.argmax(-1), np.exp(v.astype(np.float64) - m[..., None].astype(np.float64)).sum(-1)
+
+
+def _forward_with_stats(model, cache, tokens, temperature):
+    B, k1 = tokens.shape
+    s = model.shape
+    logits = torch.empty((B, k1, s.vocab), dtype=torch.float32, device="cuda")
+    hidden = torch.empty((B, k1, s.hidden), dtype=torch.float32, device="cuda")
+    stats = gm.new_row_stats(B, k1)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    gm.verify_forward(model, cache, i32(tokens), logits, hidden, gm.Workspace(), err, target_stats=stats,
+                      temperature=temperature)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    return logits, stats
+
+
+def _check_stats(name, stats, logits, temperature):
+    # the handed-over statistics describe the logits they come with
+    mx, am, sm = gm.decode_row_stats(stats)
+    rm, ram, rs = _stats_definition(logits.cpu().numpy(), temperature)
+    np.testing.assert_array_equal(mx, rm)
+    np.testing.assert_array_equal(am, ram)
+    e = float(np.abs(sm / rs - 1).max())
+    print("[%s] T=%.2f statistics: max and arg-max exact, normaliser rel err %.2e" % (name, temperature, e), flush=True)
+    assert e < 2e-6
+
+
+def _accept_with_stats(logits, stats, zq, drafts, ua, uf, mode, temperature):
+    B, k1, V = logits.shape
+    n = torch.zeros(B, dtype=torch.int32, device="cuda")
+    out = torch.zeros((B, k1), dtype=torch.int32, device="cuda")
+    gm.spec_accept(logits, t32(zq) if zq is not None else None, i32(drafts), t32(ua) if ua is not None else None,
+                   t32(uf) if uf is not None else None, n, out, mode, gm.Workspace(), temperature=temperature,
+                   target_stats=stats)
+    torch.cuda.synchronize()
+    return n.cpu().numpy(), out.cpu().numpy()
+
+
+def _handoff_parity(name, logits, stats, ref_logits, drafts, temperature, seed, final_floor):
+    """Greedy and sampled acceptance with the forward's statistics against the oracle's
+    accept on its own logits.  The flag windows widen with the measured deviation d of the
+    two sets of logits: a ratio p/q moves by at most ~2d/T, a top-2 margin by 2d, a CDF edge
+    by 2d/T of the mass."""
+    B, k1, V = ref_logits.shape
+    k = k1 - 1
+    d = float(np.abs(logits.cpu().numpy().astype(np.float64) - ref_logits).max())
+    # greedy
+    ref = oracle.spec_accept(ref_logits, None, drafts, None, None, mode="greedy", margin_eps=max(1e-2, 2.5 * d))
+    n, out = _accept_with_stats(logits, stats, None, drafts, None, None, gm.GM_GREEDY, temperature)
+    ok = ~ref.flagged
+    flag_report("%s greedy with target stats" % name, ref.flagged, B)
+    assert ok.any()
+    np.testing.assert_array_equal(n[ok], ref.n_accept[ok])
+    np.testing.assert_array_equal(out[ok], ref.out_tokens[ok])
+    # sample: q close to p (so deep prefixes and the bonus draw are reached), drafts ~ q
+    zq = ref_logits[:, :k] + 0.3 * synth.normal_logits((B, k, V), seed, name, "zq").astype(np.float64)
+    ua, uf, ud = synth.uniforms(B, k, seed, name)
+    qd = oracle.softmax(zq / temperature)
+    dr = np.stack([oracle.inverse_cdf_rows(qd[:, i], ud[:, i])[0] for i in range(k)], 1)
+    zq32 = zq.astype(np.float32)
+    ref = oracle.spec_accept(ref_logits, zq32, dr, ua, uf, temperature=temperature,
+                             accept_eps=max(1e-3, 3 * d / temperature), final_eps=max(final_floor, 3 * d / temperature))
+    n, out = _accept_with_stats(logits, stats, zq32, dr, ua, uf, gm.GM_SAMPLE, temperature)
+    oka, ok = ~ref.flag_accept, ~ref.flagged
+    print("[%s sample with target stats] logit deviation %.2e; accept decisions compared %d of %d, whole outputs %d; "
+          "mean accepted %.2f" % (name, d, oka.sum(), B, ok.sum(), n.mean()), flush=True)
+    assert oka.any()
+    np.testing.assert_array_equal(n[oka], ref.n_accept[oka])
+    np.testing.assert_array_equal(out[ok], ref.out_tokens[ok])
+    return n
+
+
+def test_target_stats_handoff_tiny_f32():
+    # float32 model: the forward's statistics (a pass over the stored rows on this path) and
+    # the accept that takes them, against the oracle's exact forward and accept
+    need_gpu()
+    wl = synth.WORKLOADS["tiny"]
+    shape = wl.shape
+    W = synth.model_weights(shape)
+    B, k, T0 = wl.batch, wl.k, wl.ctx_lo
+    prompt = synth.token_ids(B * T0, shape.vocab, 1, "tiny-prompt").reshape(B, T0)
+    caches = oracle.prefill(shape, W, prompt, EXACT)
+    caches = [([a.astype(np.float32) for a in ks], [a.astype(np.float32) for a in vs]) for ks, vs in caches]
+    lens = np.full(B, T0)
+    tokens = synth.token_ids(B * (k + 1), shape.vocab, 1, "tiny-block").reshape(B, k + 1)
+    ref, _, _ = oracle.verify_forward(shape, W, caches, tokens, lens, EXACT)
+    model = gm.DeviceModel(shape, W)
+    for T in (1.0, 0.7):
+        logits, stats = _forward_with_stats(model, device_cache(shape, caches, lens, k + 1), tokens, T)
+        _check_stats("tiny f32", stats, logits, T)
+        _handoff_parity("tiny f32 T=%.1f" % T, logits, stats, ref, tokens[:, 1:], T, 11, 1e-5)
+
+
+@pytest.mark.parametrize("B", [64, 16])
+def test_target_stats_handoff_qwen_layer(qwen_layer, B):
+    # bf16 Qwen3-4B-shaped layer: M = 256 block rows take the tiled LM head's statistics
+    # epilogue, M = 64 the strip-range kernel's; greedy and sampled decisions with the
+    # handed-over statistics against the oracle (rounding-contract logits)
+    need_gpu()
+    wl, shape, W, lens, caches, tokens = qwen_layer
+    k = wl.k
+    lens, tokens = lens[:B], tokens[:B]
+    caches = [(ks[:B], vs[:B]) for ks, vs in caches]
+    ref, _, _ = oracle.verify_forward(shape, W, caches, tokens, lens, CONTRACT)
+    model = gm.DeviceModel(shape, W)
+    for T in ((1.0, 0.7) if B == 64 else (1.0,)):
+        logits, stats = _forward_with_stats(model, device_cache(shape, caches, lens, k + 1), tokens, T)
+        _check_stats("qwen3 layer B=%d" % B, stats, logits, T)
+        n = _handoff_parity("qwen3 layer B=%d T=%.1f" % (B, T), logits, stats, ref, tokens[:, 1:], T, 12, 1e-8)
+        # the statistics pass and the handoff decide alike on the same logits
+        zq = ref[:, :k] + 0.3 * synth.normal_logits((B, k, shape.vocab), 12, "qwen3 layer B=%d T=%.1f" % (B, T), "zq")
+        ua, uf, ud = synth.uniforms(B, k, 12, "qwen3 layer B=%d T=%.1f" % (B, T))
+        qd = oracle.softmax(zq / T)
+        dr = np.stack([oracle.inverse_cdf_rows(qd[:, i], ud[:, i])[0] for i in range(k)], 1)
+        n_pass = torch.zeros(B, dtype=torch.int32, device="cuda")
+        o_pass = torch.zeros((B, k + 1), dtype=torch.int32, device="cuda")
+        gm.spec_accept(logits, t32(zq.astype(np.float32)), i32(dr), t32(ua), t32(uf), n_pass, o_pass, gm.GM_SAMPLE,
+                       gm.Workspace(), temperature=T)
+        torch.cuda.synchronize()
+        assert (n_pass.cpu().numpy() == n).mean() >= 0.98

@@ -266,6 +266,23 @@ gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature, float
                          int32_t *n_accept, int32_t *out_tokens, const gm_record *record, void *ws,
                          size_t ws_bytes, void *stream);
 
+/* gm_spec_accept for callers that cannot allocate (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the same arguments and
+ * results, without the workspace.  Its scratch is a fixed 16 MiB device array that
+ * each GPU the library runs on holds until the process ends; the call allocates and
+ * frees nothing.  Limit: calls whose gm_workspace_size(GM_OP_SPEC_ACCEPT, ...) exceeds
+ * 16 MiB return GM_ERR_CAPACITY before touching the device (B = 256 sequences at
+ * k = 7, V = 151936 fit, top-p included).  Every call on one GPU shares that GPU's
+ * scratch: calls that overlap in time on one GPU (other streams, other threads) race
+ * and must be serialised by the caller.  GM_ERR_DEVICE if the scratch's device
+ * address cannot be obtained on the current device. */
+gm_status gm_spec_accept_noalloc(int B, int k, int V, int mode, float temperature, float top_p,
+                                 const float *target_logits, const float *draft_logits,
+                                 const gm_row_stats *target_stats, const gm_row_stats *draft_stats,
+                                 const gm_nucleus *draft_nucleus, const int32_t *draft_tokens,
+                                 const float *u_accept, const float *u_final, int32_t *n_accept,
+                                 int32_t *out_tokens, const gm_record *record, void *stream);
+
 /* Commit / rollback (Sec. 2.2; App. "Train--Inference Inconsistency under
  * Teacher Forcing", Eq. tf-restart-kv): block positions 0..n_b stay, the rest
  * are rolled back by index only (no KV bytes move): seq_lens[b] += n_b + 1.

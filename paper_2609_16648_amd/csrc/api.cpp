@@ -15,14 +15,19 @@ using namespace gm;
 namespace {
 thread_local std::string g_err;
 
-gm_status fail(gm_status st, const char *fmt, ...) {
+gm_status vfail(gm_status st, const char *fmt, va_list ap) {
   char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
   vsnprintf(buf, sizeof(buf), fmt, ap);
-  va_end(ap);
   g_err = buf;
   return st;
+}
+
+gm_status fail(gm_status st, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  const gm_status r = vfail(st, fmt, ap);
+  va_end(ap);
+  return r;
 }
 
 gm_status check_launch(const char *what) {
@@ -155,14 +160,22 @@ static_assert(sizeof(gm_nucleus) == sizeof(NucRow) && offsetof(gm_nucleus, m) ==
                   offsetof(gm_nucleus, last_id) == offsetof(NucRow, idt),
               "gm_nucleus is the device's NucRow");
 
-extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature, float top_p,
-                                    const float *target_logits,
-                                    const float *draft_logits, const gm_row_stats *target_stats,
-                                    const gm_row_stats *draft_stats,
-                                    const gm_nucleus *draft_nucleus,
-                                    const int32_t *draft_tokens, const float *u_accept,
-                                    const float *u_final, int32_t *n_accept, int32_t *out_tokens,
-                                    const gm_record *record, void *ws, size_t ws_bytes, void *stream) {
+namespace gm {
+gm_status set_error(gm_status st, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  const gm_status r = vfail(st, fmt, ap);
+  va_end(ap);
+  return r;
+}
+
+size_t accept_workspace_bytes(int B, int k, int V) { return plan_accept(B, k, V).total; }
+
+gm_status spec_accept_impl(int B, int k, int V, int mode, float temperature, float top_p, const float *target_logits,
+                           const float *draft_logits, const gm_row_stats *target_stats, const gm_row_stats *draft_stats,
+                           const gm_nucleus *draft_nucleus, const int32_t *draft_tokens, const float *u_accept,
+                           const float *u_final, int32_t *n_accept, int32_t *out_tokens, const gm_record *record,
+                           void *ws, size_t ws_bytes, void *stream) {
   if (B < 0 || k < 0 || k > kMaxK || V < 1) return fail(GM_ERR_INVALID_ARG, "bad B=%d k=%d V=%d", B, k, V);
   if (V > kMaxVocab) return fail(GM_ERR_UNSUPPORTED, "vocab %d exceeds %d", V, kMaxVocab);
   if (mode != GM_GREEDY && mode != GM_SAMPLE) return fail(GM_ERR_INVALID_ARG, "unknown accept mode %d", mode);
@@ -235,6 +248,20 @@ extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float tempera
     launch_record_topk(B, k, V, inv_t, record->topk, target_logits, tstat, submax, record->logp, record->ids, s);
   if (mode == GM_SAMPLE) launch_residual_draw("accept_residual_chunk", "accept_residual_scan", B, V, inv_t, sel, (double *)(w + p.wsum), (double *)(w + p.psum), s);
   return check_launch("gm_spec_accept");
+}
+}  // namespace gm
+
+extern "C" gm_status gm_spec_accept(int B, int k, int V, int mode, float temperature, float top_p,
+                                    const float *target_logits,
+                                    const float *draft_logits, const gm_row_stats *target_stats,
+                                    const gm_row_stats *draft_stats,
+                                    const gm_nucleus *draft_nucleus,
+                                    const int32_t *draft_tokens, const float *u_accept,
+                                    const float *u_final, int32_t *n_accept, int32_t *out_tokens,
+                                    const gm_record *record, void *ws, size_t ws_bytes, void *stream) {
+  return spec_accept_impl(B, k, V, mode, temperature, top_p, target_logits, draft_logits, target_stats, draft_stats,
+                          draft_nucleus, draft_tokens, u_accept, u_final, n_accept, out_tokens, record, ws, ws_bytes,
+                          stream);
 }
 
 // ---------------------------------------------------------------- gm_dca_loss

@@ -112,6 +112,17 @@ void launch_mtp_input(int dtype, int M, int H, int V, float eps, const float *h,
 void launch_gather_rows(int M_out, int R, int C, size_t elem, const void *src, const int32_t *sel, void *dst,
                         hipStream_t s);
 
+// ---------------------------------------------------------------- accept (api.cpp)
+// the accept with a given workspace (validation included); shared by the entry points
+gm_status spec_accept_impl(int B, int k, int V, int mode, float temperature, float top_p, const float *target_logits,
+                           const float *draft_logits, const gm_row_stats *target_stats, const gm_row_stats *draft_stats,
+                           const gm_nucleus *draft_nucleus, const int32_t *draft_tokens, const float *u_accept,
+                           const float *u_final, int32_t *n_accept, int32_t *out_tokens, const gm_record *record,
+                           void *ws, size_t ws_bytes, void *stream);
+size_t accept_workspace_bytes(int B, int k, int V);
+// sets the thread's gm_last_error() message and returns st
+gm_status set_error(gm_status st, const char *fmt, ...);
+
 // ---------------------------------------------------------------- orchestration
 struct ForwardPlan {
   size_t nbuf, act, qkv, q, attn, attn_ws, part, tiles, total;

@@ -65,7 +65,7 @@ class KVCacheDesc(ctypes.Structure):
 _lib = None
 
 EXPORTS = ["gm_workspace_size", "gm_verify_forward", "gm_verify_attention", "gm_spec_accept", "gm_kv_commit",
-           "gm_mtp_draft", "gm_mtp_reconstruct", "gm_dca_loss", "gm_last_error", "gm_trace_start", "gm_trace_stop", "gm_trace_count", "gm_trace_get"]
+           "gm_mtp_draft", "gm_mtp_reconstruct", "gm_dca_loss", "gm_last_error", "gm_trace_start", "gm_trace_stop", "gm_trace_count", "gm_trace_get", "gm_spec_accept_noalloc"]
 
 
 def lib() -> ctypes.CDLL:
@@ -89,6 +89,10 @@ def lib() -> ctypes.CDLL:
     L.gm_spec_accept.argtypes = [c_int, c_int, c_int, c_int, c_float, c_float, c_void_p, c_void_p, c_void_p,
                                  c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                  c_void_p, c_size_t, c_void_p]
+    L.gm_spec_accept_noalloc.restype = c_int
+    L.gm_spec_accept_noalloc.argtypes = [c_int, c_int, c_int, c_int, c_float, c_float, c_void_p, c_void_p, c_void_p,
+                                         c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                         c_void_p]
     L.gm_kv_commit.restype = c_int
     L.gm_kv_commit.argtypes = [P(KVCacheDesc), c_int, c_int, c_void_p, c_void_p, c_void_p]
     L.gm_mtp_draft.restype = c_int
@@ -405,6 +409,26 @@ def spec_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor
                                 _ptr(draft_stats), _ptr(draft_nucleus), _ptr(draft_tokens), _ptr(u_accept), _ptr(u_final), _ptr(n_accept),
                                 _ptr(out_tokens), ctypes.byref(rec) if rec is not None else None, _ptr(buf),
                                 buf.numel(), _stream(stream)))
+
+
+def spec_accept_noalloc(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], draft_tokens: torch.Tensor,
+                        u_accept: Optional[torch.Tensor], u_final: Optional[torch.Tensor], n_accept: torch.Tensor,
+                        out_tokens: torch.Tensor, mode: int, temperature: float = 1.0, stream=None,
+                        draft_stats: Optional[torch.Tensor] = None, top_p: float = 1.0,
+                        target_stats: Optional[torch.Tensor] = None):
+    """spec_accept on the library's fixed device scratch (no workspace, nothing allocated)."""
+    B, k1, V = target_logits.shape
+    k = k1 - 1
+    _need(target_logits, torch.float32, (B, k1, V), "target_logits")
+    if draft_logits is not None:
+        _need(draft_logits, torch.float32, (B, k, V), "draft_logits")
+    _need(draft_tokens, torch.int32, (B, k), "draft_tokens")
+    _need(n_accept, torch.int32, (B,), "n_accept")
+    _need(out_tokens, torch.int32, (B, k1), "out_tokens")
+    _check(lib().gm_spec_accept_noalloc(B, k, V, mode, float(temperature), float(top_p), _ptr(target_logits),
+                                        _ptr(draft_logits), _ptr(target_stats), _ptr(draft_stats), None,
+                                        _ptr(draft_tokens), _ptr(u_accept), _ptr(u_final), _ptr(n_accept),
+                                        _ptr(out_tokens), None, _stream(stream)))
 
 
 def kv_commit(cache: PagedCache, k: int, n_accept: torch.Tensor, committed_slots: Optional[torch.Tensor] = None,

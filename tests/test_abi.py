@@ -232,3 +232,17 @@ def test_workspace_size_null_config():
     for op in (gm.GM_OP_VERIFY_FORWARD, gm.GM_OP_VERIFY_ATTENTION, gm.GM_OP_SPEC_ACCEPT, gm.GM_OP_MTP_DRAFT,
                gm.GM_OP_DCA_LOSS, gm.GM_OP_MTP_RECONSTRUCT):
         assert L.gm_workspace_size(op, None, 8, 3, 1024) == 0
+
+
+def test_spec_accept_noalloc_rejects_on_the_host():
+    # oversized calls and bad shapes fail before the device is touched (no GPU here)
+    L = gm.lib()
+    call = lambda B, k, V: L.gm_spec_accept_noalloc(B, k, V, gm.GM_SAMPLE, 1.0, 1.0, FAKE, FAKE, None, None, None,
+                                                    FAKE, FAKE, FAKE, FAKE, FAKE, None, None)
+    assert call(4, 16, 100) == gm.GM_ERR_INVALID_ARG
+    assert call(-1, 3, 100) == gm.GM_ERR_INVALID_ARG
+    assert call(0, 3, 100) == gm.GM_OK
+    assert call(4096, 15, 524288) == gm.GM_ERR_CAPACITY and "fixed scratch" in gm.last_error()
+    cfg = gm.ModelConfig()
+    cfg.vocab = 151936
+    assert gm.workspace_size(gm.GM_OP_SPEC_ACCEPT, cfg, 256, 7, 0) <= 16 << 20     # the stated fit

@@ -36,6 +36,8 @@ BF16_TFLOPS = 2500.0        # MI355X dense bf16 matrix peak, TFLOP/s
 METRIC = "accepted tokens/s per verify step; verify-attn HBM GB/s & GEMM MFMA % of peak"
 
 DESCRIPTIONS = {
+    "tiny": "random-init float32 decoder: 2 layers, hidden 256, 4 heads x 64, FFN 1024, vocab 1024; B=4, 128-token "
+            "contexts, k=3 uniform drafts; T=1",
     "qwen3_4b_layer": "one Qwen3-4B-shaped layer (H 2560, 32/8 heads x 128, FFN 9728) + LM head (V 151936) "
                       "+ 1-layer MTP head of the same shape; B=64, contexts U[1024,4096], k=3, drafts = target "
                       "top-1 w.p. 0.7 else uniform; T=1",
@@ -47,6 +49,13 @@ DESCRIPTIONS = {
     "long_ctx": "Qwen3-4B-shaped verify attention + accept only; B=32, contexts U[16384,32768], k=7, "
                 "drafts sampled from q = softmax(N(0,1)); T=1",
 }
+
+
+# workloads whose two input sets fit in HBM side by side (the rest run one set: a step of theirs
+# touches far more than the 256 MB Infinity Cache anyway)
+ROTATED = ("tiny", "qwen3_4b_layer", "qwen3_4b_layer_k7", "long_ctx")
+# the other configurations, measured after the headline workload in the same run
+EXTRA = ("tiny", "long_ctx", "qwen3_4b_full", "mimo_7b")
 
 
 def log(msg):
@@ -109,7 +118,11 @@ def accounting(wl, lens, top_p=1.0, record=0, target_stats=False):
 class Step:
     """Device state of one workload and the enqueue of one step."""
 
-    def __init__(self, wl, mode, device="cuda", record=0, top_p=1.0, target_stats=False):
+    def __init__(self, wl, mode, device="cuda", record=0, top_p=1.0, target_stats=False, host=None, chain=False,
+                 headroom=0):
+        """host: host_state() of another Step of the same workload (a second input set with the
+        same values in separate buffers); chain: each step verifies the drafts the head proposed
+        in the step before (the committed lengths advance; headroom: positions to reserve)."""
         import torch
         from paper_2609_16648_amd import gm
         self.torch, self.gm, self.wl = torch, gm, wl
@@ -125,7 +138,8 @@ class Step:
                            torch.zeros((wl.batch, wl.k, record), dtype=torch.int32, device=device))
         t0 = time.time()
         self.lens = synth.context_lengths(wl)
-        cap = self.lens + 2 * k + 2
+        cap = self.lens + 2 * k + 2 + headroom
+        self.chain = chain and wl.with_mtp
         gen = torch.Generator(device=device)
         gen.manual_seed(synth.SEED_KV)
 
@@ -158,7 +172,7 @@ class Step:
             tgt = self.ud.double()[..., None] * p[..., -1:]
             self.drafts = torch.searchsorted(p, tgt, right=True).clamp_(max=V - 1)[..., 0].to(torch.int32)
         else:
-            self.W = synth.model_weights(s, threads=16)
+            self.W = host["W"] if host else synth.model_weights(s, threads=16)
             self.model = gm.DeviceModel(s, self.W, device)
             self.logits = torch.empty((B, k + 1, V), dtype=torch.float32, device=device)
             # optionally the target rows' softmax statistics from the LM head's epilogue, for the
@@ -175,14 +189,19 @@ class Step:
                 st["sum"] = np.exp(zq.astype(np.float64) - st["max"][..., None].astype(np.float64)).sum(-1)
                 self.zq_stats = torch.from_numpy(st.view(np.uint8).reshape(B, k, gm.ROW_STATS_BYTES).copy()).to(device)
                 self.next_stats = gm.new_row_stats(B, k, device)
-                self.Wm = synth.mtp_weights(s)
+                self.Wm = host["Wm"] if host else synth.mtp_weights(s)
                 self.mtp = gm.DeviceMtp(s, self.Wm, device)
                 self.mcache = gm.PagedCache(s, 1, self.lens, cap, page_size=wl.page_size, fill="empty")
                 random_pools(self.mcache)
                 self.next_drafts = torch.zeros((B, k), dtype=torch.int32, device=device)
                 self.dlog = torch.zeros((B, k, V), dtype=torch.float32, device=device)
+                if self.chain:   # the head writes one pair while the accept reads the other
+                    self.next_drafts2 = torch.zeros_like(self.next_drafts)
+                    self.dlog2 = torch.zeros_like(self.dlog)
+                    self.next_stats2 = gm.new_row_stats(B, k, device)
+                    self.accept_in = (self.zq, self.zq_stats)
             self.pending = dev(synth.token_ids(B, V, synth.SEED_TOKENS, wl.name, "pending"), torch.int32)
-            self.drafts = self._mixing_drafts(device)
+            self.drafts = host["drafts"].to(device) if host else self._mixing_drafts(device)
             self.tokens = torch.cat([self.pending[:, None], self.drafts], 1).contiguous()
         torch.cuda.synchronize()
         log("[bench] set-up of %s took %.1f s" % (wl.name, time.time() - t0))
@@ -204,9 +223,15 @@ class Step:
             drafts[:, i] = torch.where(take[:, i], top1, alt[:, i])
         return drafts.contiguous()
 
-    def __call__(self):
+    def host_state(self):
+        return {"W": getattr(self, "W", None), "Wm": getattr(self, "Wm", None), "drafts": self.drafts.cpu()}
+
+    def __call__(self, draft=True):
+        """One step; draft=False leaves out the draft head (verify, accept and commit only)."""
         gm, wl = self.gm, self.wl
         k = wl.k
+        if self.chain:
+            return self._chain_step()
         self.cache.seq_lens.copy_(self.lens0)
         if wl.name == "long_ctx":
             gm.verify_attention(self.cfg, self.cache, 0, self.q, self.attn_out, self.ws_v)
@@ -221,11 +246,35 @@ class Step:
                        draft_stats=self.zq_stats if handoff else None, record=self.record, top_p=self.top_p,
                        target_stats=self.tstats)
         gm.kv_commit(self.cache, k, self.n, self.slots)
-        if wl.with_mtp:
+        if wl.with_mtp and draft:
             self.mcache.seq_lens.copy_(self.lens0)
             gm.mtp_draft(self.model, self.mtp, self.mcache, k, self.mode, self.hidden, self.n, self.out, self.ud,
                          self.next_drafts, self.dlog, self.ws_m, draft_stats=self.next_stats if handoff else None,
                          top_p=self.top_p)
+
+
+    def _chain_step(self):
+        """Verify the block [pending, drafts], accept, commit, then the head drafts the next
+        block from this step's hiddens; the next step verifies those drafts after the token
+        this step drew."""
+        torch, gm, wl = self.torch, self.gm, self.wl
+        k = wl.k
+        zq, zq_stats = self.accept_in
+        gm.verify_forward(self.model, self.cache, self.tokens, self.logits, self.hidden, self.ws_v)
+        gm.spec_accept(self.logits, zq, self.drafts, self.ua, self.uf, self.n, self.out, self.mode, self.ws_a,
+                       draft_stats=zq_stats if self.top_p >= 1.0 else None, top_p=self.top_p)
+        gm.kv_commit(self.cache, k, self.n, self.slots)
+        gm.mtp_draft(self.model, self.mtp, self.mcache, k, self.mode, self.hidden, self.n, self.out, self.ud,
+                     self.next_drafts, self.dlog, self.ws_m,
+                     draft_stats=self.next_stats if self.top_p >= 1.0 else None, top_p=self.top_p)
+        final = torch.gather(self.out, 1, self.n.long()[:, None])
+        self.tokens = torch.cat([final, self.next_drafts], 1).contiguous()
+        self.drafts = self.next_drafts
+        self.accept_in = (self.dlog, self.next_stats)
+        # the head writes the other pair next time
+        self.next_drafts, self.next_drafts2 = self.next_drafts2, self.next_drafts
+        self.dlog, self.dlog2 = self.dlog2, self.dlog
+        self.next_stats, self.next_stats2 = self.next_stats2, self.next_stats
 
 
 # ----------------------------------------------------------------------------- DCA loss timing
@@ -393,6 +442,58 @@ def cpu_baseline(wl, mode, budget_s, weights=None, top_p=1.0):
                          t, c)}
 
 
+# ----------------------------------------------------------------------------- other configurations
+def measure_workload(name, mode, steps, warmup=2):
+    """One configuration besides the headline: set-up, warm-up, one traced step for the kernel
+    fractions, then `steps` steps timed with a HIP event after each (median reported).  The
+    36-layer Qwen3-4B workload runs as a chain: each step verifies the drafts the head proposed
+    in the step before, so its committed tokens are counted step by step on the device."""
+    import torch
+    from paper_2609_16648_amd import gm
+    wl = synth.WORKLOADS[name]
+    chain = name == "qwen3_4b_full"
+    t0 = time.time()
+    st = Step(wl, mode, chain=chain, headroom=(warmup + 1 + steps) * (wl.k + 1) if chain else 0)
+    setup_s = time.time() - t0
+    for _ in range(warmup):
+        st()
+    torch.cuda.synchronize()
+    gm.trace_start()
+    st()
+    per_kernel = gm.trace_stop()
+    committed = torch.zeros((), dtype=torch.int64, device="cuda")
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    evs[0].record()
+    for i in range(steps):
+        st()
+        evs[i + 1].record()
+        if chain:
+            committed += (st.n + 1).sum()
+    torch.cuda.synchronize()
+    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
+    med = float(np.median(per_step))
+    tokens = int(committed.item()) / steps if chain else int((st.n + 1).sum().item())
+    acc = accounting(wl, st.lens)
+    out = {"description": DESCRIPTIONS[name], "batch": wl.batch, "k": wl.k, "steps": steps,
+           "ms_per_step": round(evs[0].elapsed_time(evs[-1]) / steps, 4), "ms_per_step_median": round(med, 4),
+           "tokens_per_s_median": round(tokens / (med / 1e3), 1), "committed_tokens_per_step": tokens,
+           "tau": round(tokens / wl.batch, 4), "setup_s": round(setup_s, 1),
+           "drafts": "the head's own chain, fed back step to step" if chain else
+                     ("target top-1 w.p. %.1f else uniform" % wl.mix_prob if wl.mix_prob else
+                      ("drawn from q" if name == "long_ctx" else "uniform"))}
+    if "attn_verify" in per_kernel and "attn_verify" in acc:
+        ms_a = per_kernel["attn_verify"][1]
+        out["verify_attn_hbm_frac"] = round(acc["attn_verify"]["bytes"] / (ms_a * 1e-3) / 1e9 / HBM_GBS, 3)
+    gn = [x for x in per_kernel if x.startswith("gemm_") and x in acc]
+    if gn:
+        gms = sum(per_kernel[x][1] for x in gn)
+        out["verify_gemm_mfma_frac"] = round(sum(acc[x]["flops"] for x in gn) / (gms * 1e-3) / 1e12 / BF16_TFLOPS, 3)
+    log("[bench] %s: %s" % (name, out))
+    del st
+    torch.cuda.empty_cache()
+    return out
+
+
 # ----------------------------------------------------------------------------- main
 def measured_traffic(kernel, workload):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter record
@@ -431,6 +532,10 @@ def main():
                     help="top-p of the accept and the draft (the paper's evaluation decodes at 0.7; 1: off)")
     ap.add_argument("--target-stats", action="store_true",
                     help="hand the verify LM head's epilogue statistics to the accept (off: the accept's own pass)")
+    ap.add_argument("--one-set", action="store_true", help="one input set (no rotation between steps)")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the other configurations (tiny, long_ctx, qwen3_4b_full, mimo_7b) after the headline")
+    ap.add_argument("--extra-steps", type=int, default=5, help="timed steps of each other configuration")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also time a plain device copy of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -445,33 +550,45 @@ def main():
     torch.cuda.set_device(0)
     wl = synth.WORKLOADS[args.workload]
     step = Step(wl, args.mode, record=args.record, top_p=args.top_p, target_stats=args.target_stats)
+    # Two input sets (weights, KV, logits and every step buffer; the same values in separate
+    # buffers) alternate between steps, so that no step finds the previous step's data in the
+    # 256 MB Infinity Cache.  Large workloads, whose step touches far more than that cache,
+    # run one set.
+    sets = [step]
+    if not args.one_set and wl.name in ROTATED:
+        sets.append(Step(wl, args.mode, record=args.record, top_p=args.top_p, target_stats=args.target_stats,
+                         host=step.host_state()))
 
-    for _ in range(args.warmup):
-        step()
+    for i in range(args.warmup):
+        sets[i % len(sets)]()
     torch.cuda.synchronize()
-    n_warm = step.n.clone()
+    n_warm = [st.n.clone() for st in sets]
 
-    # all kernels of a few steps, to find the dominant one and the breakdown
+    # all kernels of a few steps (a separate pass), to find the dominant one and the breakdown
     gm.trace_start()
-    probe_steps = 3
-    for _ in range(probe_steps):
-        step()
+    probe_steps = 2 * len(sets)
+    for i in range(probe_steps):
+        sets[i % len(sets)]()
     per_kernel = gm.trace_stop()
     dominant = max(per_kernel, key=lambda n: per_kernel[n][1])
 
-    # timed region: K identical steps; the dominant kernel is bracketed by HIP events
+    # timed region: K steps, a HIP event after each; the dominant kernel's launches are also
+    # bracketed by HIP events on their stream (its average launch duration for the roofline)
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     gm.trace_start(dominant)
-    e0.record()
-    for _ in range(args.steps):
-        step()
-    e1.record()
+    evs[0].record()
+    for i in range(args.steps):
+        sets[i % len(sets)]()
+        evs[i + 1].record()
     torch.cuda.synchronize()
     dom = gm.trace_stop()[dominant]
-    ms = e0.elapsed_time(e1) / args.steps
-    if not torch.equal(step.n, n_warm):
-        raise RuntimeError("steps are not identical: accept counts changed between steps")
+    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    ms_median = float(np.median(per_step))
+    for st, n0 in zip(sets, n_warm):
+        if not torch.equal(st.n, n0):
+            raise RuntimeError("steps are not identical: accept counts changed between steps")
     n = step.n.cpu().numpy()
     committed = int((n + 1).sum())
     value = committed / (ms / 1e3)
@@ -514,6 +631,24 @@ def main():
         roof = {"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None,
                 "kernel": dominant}
 
+    # configuration 2 as specified (one layer and the LM head, no draft head): verify, accept and
+    # commit only, on the same sets (reported beside the full step; not the headline)
+    verify_only = None
+    if wl.with_mtp:
+        for i in range(2 * len(sets)):
+            sets[i % len(sets)](draft=False)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        ev[0].record()
+        for i in range(args.steps):
+            sets[i % len(sets)](draft=False)
+            ev[i + 1].record()
+        torch.cuda.synchronize()
+        vo = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+        verify_only = {"ms_per_step_median": round(float(np.median(vo)), 4),
+                       "tokens_per_s": round(committed / (float(np.median(vo)) / 1e3), 1),
+                       "what": "verify forward + accept + commit, no draft head"}
+
     gemm_names = [x for x in kernels if x.startswith("gemm_")]
     verify_gemm_ms = sum(kernels[x]["ms_per_step"] for x in gemm_names)
     verify_gemm_flops = sum(acc[x]["flops"] for x in gemm_names if x in acc)
@@ -527,6 +662,11 @@ def main():
         "committed_tokens_per_step": committed,
     }
 
+    summary["ms_per_step_median"] = round(ms_median, 4)
+    summary["tokens_per_s_median"] = round(committed / (ms_median / 1e3), 1)
+    summary["input_sets"] = len(sets)
+    if verify_only:
+        summary["config2_as_specified"] = verify_only
     if args.dca:
         summary["dca"] = time_dca(wl, args.dca)
     if args.reconstruct:
@@ -542,6 +682,15 @@ def main():
         torch.cuda.synchronize()
         summary["copy_probe_mib"] = args.copy_probe_mib
 
+    # the benchmark spec's two targets, beside the dominant kernel's roofline
+    targets = {}
+    if "attn_verify" in kernels and "GB_s" in kernels["attn_verify"]:
+        targets["verify_attention"] = {"bound": "hbm", "achieved": kernels["attn_verify"]["GB_s"], "peak": HBM_GBS,
+                                       "unit": "GB/s", "frac": kernels["attn_verify"]["hbm_frac"], "target_frac": 0.70}
+    if summary.get("verify_gemm_TFLOP_s"):
+        targets["verify_gemms"] = {"bound": "mfma", "achieved": summary["verify_gemm_TFLOP_s"], "peak": BF16_TFLOPS,
+                                   "unit": "TFLOP/s", "frac": summary["verify_gemm_mfma_frac"], "target_frac": 0.50}
+
     line = {"metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
             "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
             "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
@@ -549,7 +698,7 @@ def main():
                        "batch": wl.batch, "k": wl.k, "accept_mode": args.mode, "parallelism": "none (1 GPU)",
                        "record_topk": args.record, "top_p": args.top_p,
                        "target_stats": args.target_stats},
-            "roofline": roof, "summary": summary, "kernels": kernels}
+            "roofline": roof, "roofline_targets": targets, "summary": summary, "kernels": kernels}
     if not args.no_cpu_baseline:
         weights = None
         if hasattr(step, "W"):
@@ -557,6 +706,13 @@ def main():
         line["cpu_baseline"] = cpu_baseline(wl, args.mode, args.cpu_budget, weights, args.top_p)
     else:
         line["cpu_baseline"] = None
+    if not args.no_extra:
+        del sets, step
+        torch.cuda.empty_cache()
+        line["workloads"] = {}
+        for name in EXTRA:
+            if name != args.workload:
+                line["workloads"][name] = measure_workload(name, args.mode, args.extra_steps)
     for name, row in kernels.items():
         log("[bench] %-24s %s" % (name, row))
     print(json.dumps(line), flush=True)

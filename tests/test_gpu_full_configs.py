@@ -55,6 +55,58 @@ def _write_sampled(cache, shape, lens, S, layer_tag):
     return kv
 
 
+def _first_flagged(ref_logits, got_logits, drafts, n_ref, mode, zq=None, ua=None):
+    """Per sampled sequence, the first examined decision that the measured deviation d of the
+    GPU's logits (max over the row) could move, as a block row; -1 if none.
+    greedy -- rows 0..n_ref are examined (accepting d_i, rejecting, or taking the final argmax);
+      row r is flagged if its top-2 margin is under 2 d;
+    sample -- the accept tests of rows 0..min(n_ref, k - 1) are examined (the last one rejects
+      when n_ref < k); test r is flagged if |u - min(1, p/q)| < max(1e-3, 3 d) (a ratio moves by
+      about 2d/T when every logit moves by at most d).  The final draw over ~1.5e5 ids is never
+      compared at this depth: the deviation moves every CDF edge by more than an id's mass."""
+    Sn, k1, V = ref_logits.shape
+    k = k1 - 1
+    dev = np.abs(got_logits.astype(np.float64) - ref_logits).max(axis=-1)      # [S, k + 1]
+    first = np.full(Sn, -1)
+    for i in range(Sn):
+        last = int(n_ref[i]) if mode == "greedy" else min(int(n_ref[i]), k - 1)
+        for r in range(last + 1):
+            if mode == "greedy":
+                top2 = np.partition(ref_logits[i, r], V - 2)[-2:]
+                bad = (top2[1] - top2[0]) < 2 * dev[i, r]
+            else:
+                p = oracle.softmax(ref_logits[i, r])
+                qd = oracle.softmax(zq[i, r].astype(np.float64))
+                ratio = min(1.0, p[drafts[i, r]] / qd[drafts[i, r]])
+                bad = abs(float(ua[i, r]) - ratio) < max(1e-3, 3 * dev[i, r])
+            if bad:
+                first[i] = r
+                break
+    return first, dev
+
+
+def _compare_decisions(name, mode, first, n_ref, out_ref, n_got, out_got):
+    """Bit-exact decisions up to each sequence's first flagged one: with none flagged, the accepted
+    count and tokens (greedy: the final argmax too); else the drafts accepted before it."""
+    compared, whole = 0, 0
+    for i in range(len(first)):
+        f = int(first[i])
+        if f < 0:
+            assert n_got[i] == n_ref[i], (name, mode, i, n_got[i], n_ref[i])
+            m = int(n_ref[i]) + (1 if mode == "greedy" else 0)
+            np.testing.assert_array_equal(out_got[i, :m], out_ref[i, :m])
+            compared += min(int(n_ref[i]) + 1, out_ref.shape[1] - 1 if mode != "greedy" else out_ref.shape[1])
+            whole += 1
+        else:
+            assert n_got[i] >= f, (name, mode, i, n_got[i], f)
+            np.testing.assert_array_equal(out_got[i, :f], out_ref[i, :f])
+            compared += f
+    _log("%s %s accept: %d sampled sequences, %d examined decisions compared bit for bit, %d sequences with none "
+         "flagged, %d with a flagged decision" % (name, mode, len(first), compared, whole, len(first) - whole))
+    assert compared > 0
+    return compared
+
+
 @pytest.mark.parametrize("name", ["qwen3_4b_full", "mimo_7b"])
 def test_full_model_step_sampled(name):
     need_gpu()
@@ -62,8 +114,11 @@ def test_full_model_step_sampled(name):
     t0 = time.time()
     wl = synth.WORKLOADS[name]
     s, B, k = wl.shape, wl.batch, wl.k
+    V = s.vocab
     lens = synth.context_lengths(wl)
-    S = sorted({int(np.argmax(lens)), int(np.argmin(lens)), 1, 2, 3, 5})
+    g = synth.stream(synth.SEED_TOKENS, name, "sampled-sequences")
+    others = [int(x) for x in g.permutation(B) if x not in (int(np.argmax(lens)), int(np.argmin(lens)))][:14]
+    S = sorted({int(np.argmax(lens)), int(np.argmin(lens))} | set(others))
     W = synth.model_weights(s, threads=16)
     Wm = synth.mtp_weights(s)
     _log("%s: weights drawn in %.1f s" % (name, time.time() - t0))
@@ -71,18 +126,29 @@ def test_full_model_step_sampled(name):
     cache = gm.PagedCache(s, s.n_layers, lens, lens + 2 * k + 2, page_size=wl.page_size, fill="empty")
     _device_fill(cache, synth.SEED_KV)
     kv = _write_sampled(cache, s, lens, S, lambda l: l)
-    _log("%s: weights and KV on the device after %.1f s (sampled sequences %s, contexts %s)"
-         % (name, time.time() - t0, S, lens[S].tolist()))
+    _log("%s: weights and KV on the device after %.1f s (%d sampled sequences, contexts %d..%d)"
+         % (name, time.time() - t0, len(S), lens[S].min(), lens[S].max()))
 
-    tokens = synth.token_ids(B * (k + 1), s.vocab, synth.SEED_TOKENS, name, "full-block").reshape(B, k + 1)
-    logits = torch.empty((B, k + 1, s.vocab), dtype=torch.float32, device="cuda")
+    # block: a pending token, then drafts drawn from seeded draft distributions q (so that
+    # sampled acceptance reaches past the first draft)
+    pending = synth.token_ids(B, V, synth.SEED_TOKENS, name, "full-pending")
+    zq = synth.normal_logits((B, k, V), synth.SEED_DRAFT, name, "full-zq")
+    ua, uf, ud = synth.uniforms(B, k, synth.SEED_UNIFORM, name, "full")
+    q = oracle.softmax(zq.astype(np.float64))
+    drafts = np.stack([oracle.inverse_cdf_rows(q[:, i], ud[:, i])[0] for i in range(k)], 1).astype(np.int32)
+    del q
+    tokens = np.concatenate([pending[:, None], drafts], 1)
+    logits = torch.empty((B, k + 1, V), dtype=torch.float32, device="cuda")
     hidden = torch.empty((B, k + 1, s.hidden), dtype=torch.float32, device="cuda")
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     ws = gm.Workspace()
     gm.verify_forward(model, cache, i32(tokens), logits, hidden, ws, err)
     n = torch.zeros(B, dtype=torch.int32, device="cuda")
     out = torch.zeros((B, k + 1), dtype=torch.int32, device="cuda")
-    gm.spec_accept(logits, None, i32(tokens[:, 1:]), None, None, n, out, gm.GM_GREEDY, gm.Workspace())
+    gm.spec_accept(logits, None, i32(drafts), None, None, n, out, gm.GM_GREEDY, gm.Workspace())
+    ns = torch.zeros(B, dtype=torch.int32, device="cuda")
+    outs = torch.zeros((B, k + 1), dtype=torch.int32, device="cuda")
+    gm.spec_accept(logits, t32(zq), i32(drafts), t32(ua), t32(uf), ns, outs, gm.GM_SAMPLE, gm.Workspace())
     slots = torch.zeros((B, k + 1), dtype=torch.int32, device="cuda")
     gm.kv_commit(cache, k, n, slots)
     torch.cuda.synchronize()
@@ -90,6 +156,7 @@ def test_full_model_step_sampled(name):
     got_l = logits[S].cpu().numpy()
     got_h = hidden[S].cpu().numpy()
     n_all, out_all = n.cpu().numpy(), out.cpu().numpy()
+    ns_all, outs_all = ns.cpu().numpy(), outs.cpu().numpy()
     np.testing.assert_array_equal(cache.seq_lens.cpu().numpy(), lens + n_all + 1)
     _, ref_slots = oracle.kv_commit(lens, n_all, k, cache.block_table_host, wl.page_size)
     np.testing.assert_array_equal(slots.cpu().numpy(), ref_slots)
@@ -104,21 +171,24 @@ def test_full_model_step_sampled(name):
          "(after %.1f s)" % (name, e_l, e_h, e_x, e_cx, time.time() - t0))
     # bf16 rounding noise grows with depth: float32 accumulation flips ~0.1% of the roundings the
     # contract mirrors in every layer, and the flips add up like a random walk (measured 2.7e-3 at
-    # one layer, 1.3e-2 at 12 and 2.2e-2 at 36 for this shape).  The float64 contract oracle is
-    # itself 2.6e-2 from the exact result at 36 layers: the GPU must be no farther from it.
+    # one layer, 1.3e-2 at 12 and 2.2e-2 at 36 for this shape).  At 36 layers the float64 contract
+    # oracle is itself about 2.6e-2 from the exact result, beyond the 2e-2 bound of the bf16
+    # tolerance; the GPU is held to being no farther from it than that intrinsic noise.
     L = s.n_layers
+    _log("%s: 2e-2 bound vs exact: %s (GPU %.3e; the float64 contract oracle itself %.3e)"
+         % (name, "met" if e_x < 2e-2 else "MISSED", e_x, e_cx))
     assert e_l < 5e-3 * np.sqrt(L) and e_h < 5e-3 * np.sqrt(L)
     assert e_x < 1.2 * e_cx + 2e-3
-    # greedy decisions: a position is flagged where the oracle's top-2 margin is under twice the
-    # deviation the GPU's logits of that row actually show
-    res = oracle.spec_accept(ref.astype(np.float32), None, tokens[S, 1:], None, None, mode="greedy")
-    dev = np.abs(got_l - ref).max(axis=-1)                     # [len(S), k + 1]
-    top2 = np.sort(ref, axis=-1)[..., -2:]
-    flagged = ((top2[..., 1] - top2[..., 0]) < 2 * dev).any(axis=-1)
-    flag_report("%s greedy accept, sampled sequences" % name, flagged, len(S))
-    ok = ~flagged
-    np.testing.assert_array_equal(n_all[S][ok], res.n_accept[ok])
-    np.testing.assert_array_equal(out_all[S][ok], res.out_tokens[ok])
+
+    # decisions, greedy and sampled at T = 1, up to each sequence's first flagged examined row
+    res_g = oracle.spec_accept(ref, None, drafts[S], None, None, mode="greedy")
+    first, dev = _first_flagged(ref, got_l, drafts[S], res_g.n_accept, "greedy")
+    _log("%s: logit deviation of the sampled rows: median %.3e, max %.3e" % (name, np.median(dev), dev.max()))
+    _compare_decisions(name, "greedy", first, res_g.n_accept, res_g.out_tokens, n_all[S], out_all[S])
+    res_s = oracle.spec_accept(ref, zq[S], drafts[S], ua[S], uf[S])
+    first, _ = _first_flagged(ref, got_l, drafts[S], res_s.n_accept, "sample", zq[S], ua[S])
+    _compare_decisions(name, "sample", first, res_s.n_accept, res_s.out_tokens, ns_all[S], outs_all[S])
+    _log("%s: mean accepted drafts over the batch: greedy %.2f, sample %.2f" % (name, n_all.mean(), ns_all.mean()))
     del kv, ref, ref_h, ref_x, ref_hx
     gc.collect()
 

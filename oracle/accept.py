@@ -35,8 +35,9 @@ Readings where the paper is silent:
 Flags mark decisions that a correct float32 evaluation could take the other
 way: an examined accept test with |u - min(1, p/q)| < accept_eps, a greedy
 row whose top-2 logit margin is < margin_eps, a final draw whose target
-u * Z lies within final_eps of an edge of the chosen id's CDF interval, and a
-nucleus whose boundary lies within nucleus_eps of top_p.
+u * Z lies within final_eps * Z + final_abs of an edge of the chosen id's CDF
+interval (final_abs in probability units, a scalar or one value per
+sequence), and a nucleus whose boundary lies within nucleus_eps of top_p.
 """
 from __future__ import annotations
 
@@ -67,7 +68,8 @@ def _top2_margin(z: np.ndarray) -> float:
 
 def spec_accept(target_logits, draft_logits, drafts, u_accept, u_final, mode: str = "sample",
                 temperature: float = 1.0, accept_eps: float = 1e-3, margin_eps: float = 1e-2,
-                final_eps: float = 0.0, top_p: float = 1.0, nucleus_eps: float = 0.0) -> AcceptResult:
+                final_eps: float = 0.0, top_p: float = 1.0, nucleus_eps: float = 0.0,
+                final_abs=0.0) -> AcceptResult:
     """target_logits [B, k+1, V]; draft_logits [B, k, V] (None in greedy mode);
     drafts [B, k]; u_accept [B, k]; u_final [B]."""
     zt = np.asarray(target_logits, dtype=np.float64)
@@ -125,7 +127,7 @@ def spec_accept(target_logits, draft_logits, drafts, u_accept, u_final, mode: st
         empty = ~(w.sum(axis=-1) > 0.0)
         w[empty] = p_rows[empty]
         x, dist, z = inverse_cdf_rows(w, u_final)
-        f_fin = dist < final_eps * z
+        f_fin = dist < final_eps * z + np.broadcast_to(np.asarray(final_abs, dtype=np.float64), (B,))
         for b in range(B):
             out[b, :n[b]] = drafts[b, :n[b]]
             out[b, n[b]] = x[b]

@@ -1,7 +1,8 @@
 """GPU parity of gm_spec_accept and gm_kv_commit against the oracle on the same
 seeded logits.  Accept counts and committed slots must match bit for bit
 outside the flag windows (|u - min(1, p/q)| < 1e-3, top-2 margin < 1e-2, and
-a final draw within 1e-8 Z of a CDF edge); the flagged count is printed."""
+a final draw whose u * Z lies within the derived float32 bound ``draw_window``
+of a CDF edge, ~7e-6 of the row's mass at T = 1); the flagged count is printed."""
 import numpy as np
 import pytest
 import scipy.stats
@@ -9,11 +10,10 @@ import torch
 
 import oracle
 import synth
-from helpers import need_gpu, t32, i32, flag_report
+from helpers import need_gpu, t32, i32, flag_report, draw_window
 from paper_2609_16648_amd import gm
 
 pytestmark = pytest.mark.gpu
-FINAL_EPS = 1e-8
 
 
 def _sampled_drafts(zq, u_draft):
@@ -50,9 +50,9 @@ def _run(zt, zq, drafts, ua, uf, mode, draft_stats=None):
 
 
 def _compare(name, ref, n, out):
-    ok = ~ref.flagged
+    ok, oka = ~ref.flagged, ~ref.flag_accept     # a flagged final draw leaves the accept count comparable
     flag_report(name, ref.flagged, len(n))
-    np.testing.assert_array_equal(n[ok], ref.n_accept[ok])
+    np.testing.assert_array_equal(n[oka], ref.n_accept[oka])
     np.testing.assert_array_equal(out[ok], ref.out_tokens[ok])
     # flagged sequences still have valid structure
     for b in np.flatnonzero(ref.flagged):
@@ -67,7 +67,7 @@ def test_sample_accept_matches_oracle(B, k, V):
     zq = synth.normal_logits((B, k, V), 3, "q", B, k, V)
     ua, uf, ud = synth.uniforms(B, k, 4, B, k, V)
     drafts = _sampled_drafts(zq, ud)
-    ref = oracle.spec_accept(zt, zq, drafts, ua, uf, final_eps=FINAL_EPS)
+    ref = oracle.spec_accept(zt, zq, drafts, ua, uf, final_abs=draw_window(zt, zq))
     n, out = _run(zt, zq, drafts, ua, uf, gm.GM_SAMPLE)
     _compare("sample B=%d k=%d V=%d" % (B, k, V), ref, n, out)
     assert ref.flagged.mean() < 0.05
@@ -82,7 +82,7 @@ def test_sample_accept_with_draft_stats(B, k, V):
     zq = synth.normal_logits((B, k, V), 3, "qs", B, k, V)
     ua, uf, ud = synth.uniforms(B, k, 4, "s", B, k, V)
     drafts = _sampled_drafts(zq, ud)
-    ref = oracle.spec_accept(zt, zq, drafts, ua, uf, final_eps=FINAL_EPS)
+    ref = oracle.spec_accept(zt, zq, drafts, ua, uf, final_abs=draw_window(zt, zq))
     n, out = _run(zt, zq, drafts, ua, uf, gm.GM_SAMPLE, draft_stats=_host_row_stats(zq))
     _compare("sample with draft stats B=%d k=%d V=%d" % (B, k, V), ref, n, out)
     n2, out2 = _run(zt, zq, drafts, ua, uf, gm.GM_SAMPLE)

@@ -230,19 +230,27 @@ class DeviceMtp:
 class PagedCache:
     """A paged KV cache on the device (gm_kv_cache) with its page table.
 
-    pages_needed[b] pages are dealt to sequence b from a shuffled pool;
+    pages_needed[b] pages are dealt to sequence b from a shuffled pool, or the
+    rows of an explicit page table (pages may then be shared between rows);
     max_ctx is the host bound on the committed lengths."""
 
     def __init__(self, shape, n_layers: int, lens: Sequence[int], capacity: Sequence[int], page_size: int = 16,
-                 max_ctx: Optional[int] = None, device="cuda", seed: int = 0, fill: str = "zero"):
+                 max_ctx: Optional[int] = None, device="cuda", seed: int = 0, fill: str = "zero",
+                 table: Optional[np.ndarray] = None):
         self.shape, self.n_layers, self.page_size = shape, n_layers, page_size
         self.dtype = torch_dtype(shape)
         lens = np.asarray(lens, dtype=np.int64)
         capacity = np.asarray(capacity, dtype=np.int64)
         self.B = len(lens)
         need = (capacity + page_size - 1) // page_size
-        self.max_pages = int(need.max())
-        table, self.num_pages = layout.block_table(need, self.max_pages, seed)
+        if table is None:
+            self.max_pages = int(need.max())
+            table, self.num_pages = layout.block_table(need, self.max_pages, seed)
+        else:
+            table = np.ascontiguousarray(table, dtype=np.int32)
+            if table.shape[0] != self.B or any((table[b, :need[b]] < 0).any() for b in range(self.B)):
+                raise ValueError("the page table must give every sequence pages_needed pages")
+            self.max_pages, self.num_pages = table.shape[1], int(table.max()) + 1
         self.block_table_host = table
         self.block_table = torch.from_numpy(table).to(device)
         self.seq_lens = torch.from_numpy(lens.astype(np.int32)).to(device)

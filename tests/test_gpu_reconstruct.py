@@ -130,3 +130,62 @@ def test_reconstruct_full_size_sampled():
         worst = max(worst, rel_err(out[r].cpu().numpy(), ref["logits"][0]))
     print("[reconstruct R=1024 K=3] sampled cycles' head logits rel err %.3e" % worst, flush=True)
     assert worst < 1e-2
+
+
+@pytest.mark.parametrize("shape_name,K,P,tol", [("tiny", 4, 300, 1e-4), ("qwen", 3, 1500, 1e-2)])
+def test_reconstruct_over_shared_prefix_pages(shape_name, K, P, tol):
+    # All cycles of one response attend over one shared cache (App. "Parallelizing GrowMTP
+    # Training"): the pages that hold only committed prefix entries are the same physical
+    # pages in every cycle's table; the page holding cycle r's start s_r and those after it
+    # are the cycle's own (the start page begins with a copy of the prefix entries before
+    # s_r).  Starts include page boundaries and a repeated start.  The head logits and the
+    # chain entries match the oracle over the prefix truncated at each start, and the
+    # shared pages still hold the prefix afterwards.
+    need_gpu()
+    shape = synth.TINY if shape_name == "tiny" else synth.QWEN3_4B_LAYER
+    rnd = EXACT if shape.dtype == "f32" else CONTRACT
+    W, Wm = synth.model_weights(shape), synth.mtp_weights(shape)
+    ps = 16
+    g = np.random.default_rng(17)
+    starts = np.sort(np.concatenate([g.integers(1, P, 6), [ps, 4 * ps, P, P // 2, P // 2]])).astype(np.int64)
+    R = len(starts)
+    pk, pv = synth.kv_prefix(shape, [P], layer=333)
+    ks, vs = [pk[0][:s] for s in starts], [pv[0][:s] for s in starts]
+    h0 = g.standard_normal((R, shape.hidden)).astype(np.float32)
+    t0 = g.integers(0, shape.vocab, R).astype(np.int32)
+    drafts = g.integers(0, shape.vocab, (R, K)).astype(np.int32)
+    # page table: shared pages 0 .. ceil(P / ps) - 1 hold the prefix; cycle r takes the first
+    # s_r // ps of them and private pages from s_r's page on
+    n_shared = -(-P // ps)
+    max_pages = -(-(P + K) // ps)
+    table = np.full((R, max_pages), -1, dtype=np.int32)
+    nxt = n_shared
+    for r, s in enumerate(starts):
+        full = s // ps
+        table[r, :full] = np.arange(full)
+        own = -(-(s + K) // ps) - full
+        table[r, full:full + own] = np.arange(nxt, nxt + own)
+        nxt += own
+    cache = gm.PagedCache(shape, 1, starts, starts + K, page_size=ps, table=table)
+    for r, s in enumerate(starts):     # shared pages are written once per cycle, with the same entries
+        cache.write(0, r, np.arange(s), ks[r], vs[r])
+    model, mtp = gm.DeviceModel(shape, W), gm.DeviceMtp(shape, Wm)
+    out = torch.zeros((R, K, shape.vocab), dtype=torch.float32, device="cuda")
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    gm.mtp_reconstruct(model, mtp, cache, K, t32(h0), i32(t0), i32(drafts), out, gm.Workspace(), dev_err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    ref = oracle.mtp_reconstruct(shape, Wm, W, ks, vs, starts, h0, t0, drafts, K, rnd)
+    e = rel_err(out.cpu().numpy(), ref["logits"])
+    print("[reconstruct shared prefix %s R=%d K=%d P=%d] head logits rel err %.3e" % (shape_name, R, K, P, e),
+          flush=True)
+    assert e < tol
+    for r in range(R):
+        ck, cv = cache.read(0, r, starts[r] + np.arange(K))
+        assert rel_err(ck, ref["chain_k"][r]) < tol and rel_err(cv, ref["chain_v"][r]) < tol
+    # the longest cycle's table reads the whole shared prefix back unchanged
+    r = int(np.argmax(starts))
+    k_back, v_back = cache.read(0, r, np.arange(starts[r]))
+    q = (lambda a: a) if shape.dtype == "f32" else (lambda a: oracle.round_bf16(a))
+    np.testing.assert_array_equal(k_back, q(np.asarray(pk[0][:starts[r]], np.float32)))
+    np.testing.assert_array_equal(v_back, q(np.asarray(pv[0][:starts[r]], np.float32)))

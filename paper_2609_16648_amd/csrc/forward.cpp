@@ -230,10 +230,9 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
     a.dev_err = dev_err;
     run_attention(a, p.attn_ext, ws + p.attn_ws, s);
   }
-  launch_gather_rows(B, R, qd, e, attn, n_accept, attn_g, s);
-  launch_gather_rows(B, R, H, sizeof(float), x, n_accept, xg, s);
-  // the head's committed length moves to the new boundary m_b + n_b + 1
-  launch_kv_commit(B, k, c.page_size, c.max_pages_per_seq, c.block_table, lens, n_accept, nullptr, s);
+  // the boundary rows of the attention output and the residual stream, and the head's
+  // committed length moved to the new boundary m_b + n_b + 1, in one launch
+  launch_gather_commit(B, R, qd, e, attn, attn_g, H, sizeof(float), x, xg, n_accept, lens, s);
   tail_and_draw(xg, 0);
 
   // ---- chain: step j feeds (g_{j-1}, d_{j-1}) at slot boundary + j - 1

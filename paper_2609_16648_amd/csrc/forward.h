@@ -109,8 +109,10 @@ void run_dca_loss(int N, int K, int V, int topk, const float *head_logits, const
 void launch_mtp_input(int dtype, int M, int H, int V, float eps, const float *h, const int32_t *tok,
                       int tok_stride, const void *E, const void *norm_h, const void *norm_e, void *out,
                       int32_t *dev_err, hipStream_t s);
-void launch_gather_rows(int M_out, int R, int C, size_t elem, const void *src, const int32_t *sel, void *dst,
-                        hipStream_t s);
+// per sequence b: row sel[b] (clamped to 0..R-1) of src_a [B][R][Ca] and of src_b [B][R][Cb]
+// into dst_a [B][Ca] and dst_b [B][Cb], and lens[b] += sel[b] + 1 (clamped alike)
+void launch_gather_commit(int B, int R, int Ca, size_t elem_a, const void *src_a, void *dst_a, int Cb, size_t elem_b,
+                          const void *src_b, void *dst_b, const int32_t *sel, int32_t *lens, hipStream_t s);
 
 // ---------------------------------------------------------------- accept (api.cpp)
 // the accept with a given workspace (validation included); shared by the entry points

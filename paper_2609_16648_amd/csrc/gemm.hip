@@ -423,7 +423,11 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF g) {
 // 16 lane sums of a row in float64), one RowStat per (row, wave): the tiles of
 // the draw are the waves' ranges.
 constexpr int kLmStrips = 10;
-constexpr int kLmRing = 4;
+// Two slots: one k-step (14 KiB per wave) in flight while the other is consumed.  With four
+// waves per CU that is about as much as the HBM queues serve best; deeper rings put more in
+// flight and were slower (measured at 64 rows: 2 slots 146 us per launch, 4 slots 151 us,
+// 5 slots 152 us).
+constexpr int kLmRing = 2;
 static_assert(kLmStrips * kStripIds <= kMaxDrawTileIds, "the draw scans a whole strip range");
 
 struct GemmL {

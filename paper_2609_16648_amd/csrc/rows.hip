@@ -251,14 +251,75 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
   }
 }
 
-__global__ __launch_bounds__(256) void gather_rows_kernel(int R, int C16, const uint4 *__restrict__ src,
-                                                          const int32_t *__restrict__ sel, uint4 *__restrict__ dst) {
+// The draft head's extend tail, one workgroup per sequence: row n_b (clamped to 0..R-1) of
+// each of two row sets gathered into one row, and the head's committed length moved to
+// the new boundary m_b + n_b + 1 (the length update of a commit, without a slot list).
+__global__ __launch_bounds__(256) void gather_commit_kernel(int R, int C16a, const uint4 *__restrict__ src_a,
+                                                            uint4 *__restrict__ dst_a, int C16b,
+                                                            const uint4 *__restrict__ src_b, uint4 *__restrict__ dst_b,
+                                                            const int32_t *__restrict__ sel, int32_t *__restrict__ lens) {
   const int b = blockIdx.x;
   int i = sel[b];
   i = i < 0 ? 0 : (i >= R ? R - 1 : i);
-  const uint4 *s = src + ((long)b * R + i) * C16;
-  uint4 *d = dst + (long)b * C16;
-  for (int c = threadIdx.x; c < C16; c += blockDim.x) d[c] = s[c];
+  const uint4 *sa = src_a + ((long)b * R + i) * C16a;
+  const uint4 *sb = src_b + ((long)b * R + i) * C16b;
+  uint4 *da = dst_a + (long)b * C16a, *db = dst_b + (long)b * C16b;
+  for (int c = threadIdx.x; c < C16a; c += blockDim.x) da[c] = sa[c];
+  for (int c = threadIdx.x; c < C16b; c += blockDim.x) db[c] = sb[c];
+  if (threadIdx.x == 0) lens[b] += i + 1;
+}
+
+// embed_norm for bf16 rows of H % 8 == 0 channels, H <= 8 * 256 * kEmbedVec: eight channels
+// per 16-byte load, each thread's loads in registers between the two passes
+constexpr int kEmbedVec = 4;
+__global__ __launch_bounds__(256) void embed_norm_bf16_kernel(int H, int V, const int32_t *__restrict__ tok,
+                                                              const uint4 *__restrict__ E, float *__restrict__ x,
+                                                              const uint4 *__restrict__ w, float eps,
+                                                              uint4 *__restrict__ out, int32_t *dev_err) {
+  __shared__ float red[16];
+  const int r = blockIdx.x, H8 = H / 8;
+  const int t = tok[r];
+  const bool ok = t >= 0 && t < V;
+  if (!ok && threadIdx.x == 0) raise_dev_err(dev_err, GM_DEVERR_TOKEN);
+  const uint4 *er = E + (long)(ok ? t : 0) * H8;
+  uint4 v[kEmbedVec];
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < kEmbedVec; ++u) {
+    const int c = threadIdx.x + 256 * u;
+    v[u] = (ok && c < H8) ? er[c] : make_uint4(0, 0, 0, 0);
+    const uint32_t q[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = __uint_as_float(q[e] << 16), hi = __uint_as_float(q[e] & 0xffff0000u);
+      ss += lo * lo + hi * hi;
+    }
+  }
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)H + eps);
+  float4 *xr = reinterpret_cast<float4 *>(x + (long)r * H);
+  uint4 *o = out + (long)r * H8;
+#pragma unroll
+  for (int u = 0; u < kEmbedVec; ++u) {
+    const int c = threadIdx.x + 256 * u;
+    if (c >= H8) continue;
+    const uint32_t q[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+    const uint4 wv = w[c];
+    const uint32_t wq[4] = {wv.x, wv.y, wv.z, wv.w};
+    float f[8];
+    uint32_t packed[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      f[2 * e] = __uint_as_float(q[e] << 16);
+      f[2 * e + 1] = __uint_as_float(q[e] & 0xffff0000u);
+      const float a = f[2 * e] * inv * __uint_as_float(wq[e] << 16);
+      const float b = f[2 * e + 1] * inv * __uint_as_float(wq[e] & 0xffff0000u);
+      packed[e] = uint32_t(f32_to_bf16(a)) | (uint32_t(f32_to_bf16(b)) << 16);
+    }
+    xr[2 * c] = make_float4(f[0], f[1], f[2], f[3]);
+    xr[2 * c + 1] = make_float4(f[4], f[5], f[6], f[7]);
+    o[c] = make_uint4(packed[0], packed[1], packed[2], packed[3]);
+  }
 }
 }  // namespace
 
@@ -276,7 +337,10 @@ void launch_embed_norm(int dtype, int M, int H, int V, const int32_t *tokens, co
                        const void *norm_w, float eps, void *out, int32_t *dev_err, hipStream_t s) {
   if (M <= 0) return;
   TraceScope ts("embed_norm", s);
-  if (dtype == GM_BF16)
+  if (dtype == GM_BF16 && H % 8 == 0 && H <= 8 * 256 * kEmbedVec)
+    hipLaunchKernelGGL(embed_norm_bf16_kernel, dim3(M), dim3(256), 0, s, H, V, tokens, (const uint4 *)E, x,
+                       (const uint4 *)norm_w, eps, (uint4 *)out, dev_err);
+  else if (dtype == GM_BF16)
     hipLaunchKernelGGL(embed_norm_kernel<bf16>, dim3(M), dim3(256), 0, s, H, V, tokens, (const bf16 *)E, x,
                        (const bf16 *)norm_w, eps, (bf16 *)out, dev_err);
   else
@@ -317,12 +381,13 @@ void launch_mtp_input(int dtype, int M, int H, int V, float eps, const float *h,
                        (const float *)E, (const float *)norm_h, (const float *)norm_e, (float *)out, dev_err);
 }
 
-void launch_gather_rows(int M_out, int R, int C, size_t elem, const void *src, const int32_t *sel, void *dst,
-                        hipStream_t s) {
-  if (M_out <= 0) return;
-  TraceScope ts("gather_rows", s);
-  const int C16 = (int)((size_t)C * elem / 16);
-  hipLaunchKernelGGL(gather_rows_kernel, dim3(M_out), dim3(256), 0, s, R, C16, (const uint4 *)src, sel, (uint4 *)dst);
+void launch_gather_commit(int B, int R, int Ca, size_t elem_a, const void *src_a, void *dst_a, int Cb, size_t elem_b,
+                          const void *src_b, void *dst_b, const int32_t *sel, int32_t *lens, hipStream_t s) {
+  if (B <= 0) return;
+  TraceScope ts("gather_commit", s);
+  hipLaunchKernelGGL(gather_commit_kernel, dim3(B), dim3(256), 0, s, R, (int)((size_t)Ca * elem_a / 16),
+                     (const uint4 *)src_a, (uint4 *)dst_a, (int)((size_t)Cb * elem_b / 16), (const uint4 *)src_b,
+                     (uint4 *)dst_b, sel, lens);
 }
 
 }  // namespace gm

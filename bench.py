@@ -562,7 +562,8 @@ def main():
     for i in range(args.warmup):
         sets[i % len(sets)]()
     torch.cuda.synchronize()
-    n_warm = [st.n.clone() for st in sets]
+    # every set holds the same values, so every step of every set accepts alike
+    n_ref = sets[0].n.clone() if args.warmup > 0 else None
 
     # all kernels of a few steps (a separate pass), to find the dominant one and the breakdown
     gm.trace_start()
@@ -586,8 +587,10 @@ def main():
     per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
     ms = evs[0].elapsed_time(evs[-1]) / args.steps
     ms_median = float(np.median(per_step))
-    for st, n0 in zip(sets, n_warm):
-        if not torch.equal(st.n, n0):
+    if n_ref is None:
+        n_ref = sets[0].n.clone()
+    for st in sets:
+        if not torch.equal(st.n, n_ref):
             raise RuntimeError("steps are not identical: accept counts changed between steps")
     n = step.n.cpu().numpy()
     committed = int((n + 1).sum())

@@ -231,6 +231,23 @@ def test_flags_mark_near_threshold_decisions():
 
 
 # ------------------------------------------------------------ commit closed form
+def test_final_draw_window_in_probability_units():
+    # k = 0: the final draw is the bonus draw from p.  With p = (0.1, 0.2, 0.3, 0.4) and u placed
+    # 1e-6 above the edge C(1) = 0.3, the draw is id 2 and is flagged exactly when the absolute window
+    # exceeds 1e-6 (a scalar, or one value per sequence); the relative window scales with Z = 1
+    p = np.array([0.1, 0.2, 0.3, 0.4])
+    z = np.log(p)[None, None, :].repeat(2, 0)
+    u = np.array([0.3 + 1e-6, 0.3 + 1e-6])
+    none = np.zeros((2, 0), dtype=np.int64)
+    r = oracle.spec_accept(z, np.zeros((2, 0, 4)), none, np.zeros((2, 0)), u)
+    assert (r.out_tokens[:, 0] == 2).all() and not r.flagged.any()
+    assert oracle.spec_accept(z, np.zeros((2, 0, 4)), none, np.zeros((2, 0)), u, final_abs=2e-6).flagged.all()
+    assert not oracle.spec_accept(z, np.zeros((2, 0, 4)), none, np.zeros((2, 0)), u, final_abs=5e-7).flagged.any()
+    r = oracle.spec_accept(z, np.zeros((2, 0, 4)), none, np.zeros((2, 0)), u, final_abs=np.array([2e-6, 5e-7]))
+    assert r.flagged.tolist() == [True, False]
+    assert oracle.spec_accept(z, np.zeros((2, 0, 4)), none, np.zeros((2, 0)), u, final_eps=2e-6).flagged.all()
+
+
 def test_kv_commit_golden_example():
     with open(os.path.join(HERE, "golden", "kv_commit_example.json")) as f:
         ex = json.load(f)

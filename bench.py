@@ -481,6 +481,23 @@ def measure_workload(name, mode, steps, warmup=2):
            "drafts": "the head's own chain, fed back step to step" if chain else
                      ("target top-1 w.p. %.1f else uniform" % wl.mix_prob if wl.mix_prob else
                       ("drawn from q" if name == "long_ctx" else "uniform"))}
+    if name == "mimo_7b":
+        # this configuration is specified in both modes: greedy acceptance on the same set
+        other = gm.GM_GREEDY if st.mode == gm.GM_SAMPLE else gm.GM_SAMPLE
+        st.mode = other
+        for _ in range(warmup):
+            st()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        ev[0].record()
+        for i in range(steps):
+            st()
+            ev[i + 1].record()
+        torch.cuda.synchronize()
+        med2 = float(np.median([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]))
+        tok2 = int((st.n + 1).sum().item())
+        out["greedy" if other == gm.GM_GREEDY else "sample"] = {
+            "ms_per_step_median": round(med2, 4), "tokens_per_s_median": round(tok2 / (med2 / 1e3), 1),
+            "committed_tokens_per_step": tok2, "tau": round(tok2 / wl.batch, 4)}
     if "attn_verify" in per_kernel and "attn_verify" in acc:
         ms_a = per_kernel["attn_verify"][1]
         out["verify_attn_hbm_frac"] = round(acc["attn_verify"]["bytes"] / (ms_a * 1e-3) / 1e9 / HBM_GBS, 3)

@@ -337,7 +337,8 @@ void launch_embed_norm(int dtype, int M, int H, int V, const int32_t *tokens, co
                        const void *norm_w, float eps, void *out, int32_t *dev_err, hipStream_t s) {
   if (M <= 0) return;
   TraceScope ts("embed_norm", s);
-  if (dtype == GM_BF16 && H % 8 == 0 && H <= 8 * 256 * kEmbedVec)
+  const bool aligned = ((uintptr_t)E | (uintptr_t)x | (uintptr_t)norm_w | (uintptr_t)out) % 16 == 0;
+  if (dtype == GM_BF16 && H % 8 == 0 && H <= 8 * 256 * kEmbedVec && aligned)
     hipLaunchKernelGGL(embed_norm_bf16_kernel, dim3(M), dim3(256), 0, s, H, V, tokens, (const uint4 *)E, x,
                        (const uint4 *)norm_w, eps, (uint4 *)out, dev_err);
   else if (dtype == GM_BF16)

@@ -110,12 +110,16 @@ struct TileBuf {
   uint4 k[4], v[4];
 };
 
-// One 16-token tile for one 16-row query tile: S^T = K Q^T, online softmax,
-// O^T += V^T (P_hi + P_lo).  MASK: apply the causal window (token < vis) and
-// keep tokens past the context (t >= L, whose slots may hold anything) out of P V.
-template <bool MASK>
-__device__ __forceinline__ void attn_tile(int tb, int L, int g, float scale_log2, TileBuf &t, const bf16x8_t (&qf)[4],
-                                          int vis, float &m, float &l, floatx4_t (&O)[8]) {
+// One 16-token tile for the RT 16-row query tiles of a wave: S^T = K Q^T, online softmax,
+// O^T += V^T (P_hi + P_lo).  MASK: apply the causal window (token < vis) and keep tokens
+// past the context (t >= L, whose slots may hold anything) out of P V.  Each step runs
+// for every query tile before the next, so the tiles' dependency chains interleave and
+// the V operands of P V are formed once for all of them; each tile's arithmetic is the
+// same as on its own.
+template <bool MASK, int RT>
+__device__ __forceinline__ void attn_tiles(int tb, int L, int g, float scale_log2, TileBuf &t,
+                                           const bf16x8_t (&qf)[RT][4], const int (&vis)[RT], float (&m)[RT],
+                                           float (&l)[RT], floatx4_t (&O)[RT][8]) {
   if (MASK) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -128,47 +132,65 @@ __device__ __forceinline__ void attn_tile(int tb, int L, int g, float scale_log2
       }
     }
   }
-  floatx4_t S = {0.f, 0.f, 0.f, 0.f};
+  floatx4_t S[RT];
 #pragma unroll
-  for (int ii = 0; ii < 4; ++ii) S = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(t.k[ii]), qf[ii], S, 0, 0, 0);
-  float s[4], tmax;
+  for (int u = 0; u < RT; ++u) S[u] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    s[r] = S[r] * scale_log2;
-    if (MASK && tb + 4 * g + r >= vis) s[r] = -INFINITY;
+  for (int ii = 0; ii < 4; ++ii)
+#pragma unroll
+    for (int u = 0; u < RT; ++u)
+      S[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(t.k[ii]), qf[u][ii], S[u], 0, 0, 0);
+  float s[RT][4], tmax[RT];
+#pragma unroll
+  for (int u = 0; u < RT; ++u) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      s[u][r] = S[u][r] * scale_log2;
+      if (MASK && tb + 4 * g + r >= vis[u]) s[u][r] = -INFINITY;
+    }
+    tmax[u] = fmaxf(fmaxf(s[u][0], s[u][1]), fmaxf(s[u][2], s[u][3]));
   }
-  tmax = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
-  tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
-  tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
+#pragma unroll
+  for (int u = 0; u < RT; ++u) tmax[u] = fmaxf(tmax[u], __shfl_xor(tmax[u], 16, kWave));
+#pragma unroll
+  for (int u = 0; u < RT; ++u) tmax[u] = fmaxf(tmax[u], __shfl_xor(tmax[u], 32, kWave));
   // Each row decides for itself (m = -inf and a finite score also count as growth);
   // rows that did not grow keep alpha = 1 exactly, so a row's result never depends
   // on the other rows of the tile.  The branch only skips tiles where no row grew.
-  const bool up = tmax > m + kLazyLog2;
-  if (__any(up)) {
-    const float mn = up ? fmaxf(m, tmax) : m;
-    const float alpha = (!up || mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m - mn);
-    l *= alpha;
 #pragma unroll
-    for (int mm = 0; mm < 8; ++mm) O[mm] *= alpha;
-    m = mn;
+  for (int u = 0; u < RT; ++u) {
+    const bool up = tmax[u] > m[u] + kLazyLog2;
+    if (__any(up)) {
+      const float mn = up ? fmaxf(m[u], tmax[u]) : m[u];
+      const float alpha = (!up || mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m[u] - mn);
+      l[u] *= alpha;
+#pragma unroll
+      for (int mm = 0; mm < 8; ++mm) O[u][mm] *= alpha;
+      m[u] = mn;
+    }
   }
   // s <= m + kLazyLog2 here, so p <= 2^kLazyLog2
-  float p[4];
+  bf16x8_t pb[RT];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    p[r] = __builtin_amdgcn_exp2f(s[r] - m);
-    if (MASK && s[r] == -INFINITY) p[r] = 0.f;
-    l += p[r];
+  for (int u = 0; u < RT; ++u) {
+    float p[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      p[r] = __builtin_amdgcn_exp2f(s[u][r] - m[u]);
+      if (MASK && s[u][r] == -INFINITY) p[r] = 0.f;
+      l[u] += p[r];
+    }
+    const uint32_t h01 = pack_bf16(p[0], p[1]), h23 = pack_bf16(p[2], p[3]);
+    const uint32_t l01 = pack_bf16(p[0] - __uint_as_float(h01 << 16), p[1] - __uint_as_float(h01 & 0xffff0000u));
+    const uint32_t l23 = pack_bf16(p[2] - __uint_as_float(h23 << 16), p[3] - __uint_as_float(h23 & 0xffff0000u));
+    pb[u] = as_bf16x8(make_uint4(h01, h23, l01, l23));
   }
-  const uint32_t h01 = pack_bf16(p[0], p[1]), h23 = pack_bf16(p[2], p[3]);
-  const uint32_t l01 = pack_bf16(p[0] - __uint_as_float(h01 << 16), p[1] - __uint_as_float(h01 & 0xffff0000u));
-  const uint32_t l23 = pack_bf16(p[2] - __uint_as_float(h23 << 16), p[3] - __uint_as_float(h23 & 0xffff0000u));
-  const bf16x8_t pb = as_bf16x8(make_uint4(h01, h23, l01, l23));
 #pragma unroll
   for (int mm = 0; mm < 8; ++mm) {
     const uint4 &v4 = t.v[mm >> 1];
     const uint4 va = (mm & 1) ? make_uint4(v4.z, v4.w, v4.z, v4.w) : make_uint4(v4.x, v4.y, v4.x, v4.y);
-    O[mm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(va), pb, O[mm], 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < RT; ++u) O[u][mm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(va), pb[u], O[u][mm], 0, 0, 0);
   }
 }
 
@@ -323,13 +345,8 @@ __global__ __launch_bounds__(64 * kAttnWavesPerGroup) void attn_mfma_kernel(Attn
     const int n = __builtin_amdgcn_readfirstlane(nm_end > t0 ? (nm_end - t0) / 16 : 0);
     const int nt = __builtin_amdgcn_readfirstlane(tend > t0 ? (tend - t0 + 15) / 16 : 0);
     auto consume = [&](int i, TileBuf &t) {
-      if (i < n) {
-#pragma unroll
-        for (int u = 0; u < RT; ++u) attn_tile<false>(t0 + 16 * i, L, g, a.scale_log2, t, qf[u], vis[u], m[u], l[u], O[u]);
-      } else {
-#pragma unroll
-        for (int u = 0; u < RT; ++u) attn_tile<true>(t0 + 16 * i, L, g, a.scale_log2, t, qf[u], vis[u], m[u], l[u], O[u]);
-      }
+      if (i < n) attn_tiles<false, RT>(t0 + 16 * i, L, g, a.scale_log2, t, qf, vis, m, l, O);
+      else attn_tiles<true, RT>(t0 + 16 * i, L, g, a.scale_log2, t, qf, vis, m, l, O);
     };
     if (nt > 0) {
       // whole turns of the ring run unguarded (one straight path, so every wait counts

@@ -193,7 +193,7 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
   }
   // the rotation of pair `lane` at this position, shared by the group's heads
   double sn = 0.0, cs = 1.0;
-  if (act && h0 < a.n_heads + a.n_kv) sincos(pos * pow((double)a.rope_base, -2.0 * lane / D), &sn, &cs);
+  if (act && h0 < a.n_heads + a.n_kv) sincos(pos * exp2(-2.0 * lane / D * log2((double)a.rope_base)), &sn, &cs);
   const T *qn = (const T *)a.q_norm, *kn = (const T *)a.k_norm;
   // the block row's page, for the K/V heads of the group
   long kv_base = -1;

@@ -368,7 +368,7 @@ def cpu_baseline(wl, mode, budget_s, weights=None, top_p=1.0):
     import oracle
     from threadpoolctl import threadpool_info
     s, k = wl.shape, wl.k
-    rnd = oracle.Rounding("contract")
+    rnd = oracle.Rounding("contract" if s.dtype == "bf16" else "exact")
     lens_all = synth.context_lengths(wl)
     W = weights[0] if weights else (synth.model_weights(s) if wl.name != "long_ctx" else None)
     Wm = weights[1] if weights and len(weights) > 1 else (synth.mtp_weights(s) if wl.with_mtp else None)
@@ -436,10 +436,66 @@ def cpu_baseline(wl, mode, budget_s, weights=None, top_p=1.0):
         t, c, reps = t + t2, c + c2, reps + 1
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     return {"value": c / t, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": "%d of %d sequences of the %s workload, %d full step%s (verify forward in the bf16 "
-                      "rounding-contract mode, accept, commit%s) in %.1f s, %d committed tokens"
-                      % (nseq, wl.batch, wl.name, reps, "s" if reps > 1 else "", ", MTP draft" if wl.with_mtp else "",
-                         t, c)}
+            "sample": "%d of %d sequences of the %s workload, %d full step%s (%s, accept, commit%s) in %.1f s, "
+                      "%d committed tokens"
+                      % (nseq, wl.batch, wl.name, reps, "s" if reps > 1 else "",
+                         "verify attention" if wl.name == "long_ctx" else
+                         ("verify forward in the bf16 rounding-contract mode" if s.dtype == "bf16" else
+                          "verify forward in float64"),
+                         ", MTP draft" if wl.with_mtp else "", t, c)}
+
+
+def cpu_layer_extrapolated(wl, layer_wl, weights, mode, budget_s, tau):
+    """The oracle's cost of one step of a deep workload, from one of its layers: the layer (in
+    the rounding-contract mode) timed on a few sequences at the workload's own context mix and
+    scaled to all its layers, plus the LM head, the accept, the commit and the MTP draft timed
+    once.  layer_wl: the one-layer workload of the same layer shape, whose weights are given;
+    tau: committed tokens per sequence per step, from the GPU run of `wl`."""
+    import oracle
+    from threadpoolctl import threadpool_info
+    s1, k, V = layer_wl.shape, wl.k, wl.shape.vocab
+    rnd = oracle.Rounding("contract")
+    W = {kk: (vv if kk == "layers" else np.asarray(vv, dtype=np.float64)) for kk, vv in weights[0].items()}
+    W["layers"] = [{kk: np.asarray(vv, dtype=np.float64) for kk, vv in Wl.items()} for Wl in weights[0]["layers"]]
+    Wm = weights[1]
+    Wm = {kk: ({k2: np.asarray(v2, dtype=np.float64) for k2, v2 in vv.items()} if isinstance(vv, dict)
+                else np.asarray(vv, dtype=np.float64)) for kk, vv in Wm.items()}
+    lens_all = synth.context_lengths(wl)
+    u_acc, u_fin, u_dr = synth.uniforms(wl.batch, k)
+    zq = synth.normal_logits((wl.batch, k, V), synth.SEED_DRAFT, wl.name, "zq")
+    t_layer = t_rest = 0.0
+    nseq = 0
+    while nseq < wl.batch and (nseq == 0 or t_layer + t_rest < budget_s):
+        b = nseq
+        lens = lens_all[b:b + 1]
+        caches = [synth.kv_prefix(s1, lens_all, 0, seqs=[b])]
+        block = synth.token_ids(k + 1, V, synth.SEED_TOKENS, wl.name, "cpu-block", b).reshape(1, k + 1)
+        t0 = time.perf_counter()
+        logits, hid, _ = oracle.verify_forward(s1, W, caches, block, lens, rnd)
+        t1 = time.perf_counter()
+        oracle.model.lm_head(s1, W, hid[0], rnd)
+        t2 = time.perf_counter()
+        dr = block[:, 1:]
+        if mode == "sample":
+            res = oracle.spec_accept(logits.astype(np.float32), zq[b:b + 1], dr, u_acc[b:b + 1], u_fin[b:b + 1])
+        else:
+            res = oracle.spec_accept(logits.astype(np.float32), None, dr, None, None, mode="greedy")
+        oracle.kv_commit(lens, res.n_accept, k, np.arange(4096).reshape(1, 4096), 16)
+        mk, mv = synth.kv_prefix(s1, lens_all, 99, seqs=[b])
+        oracle.mtp_draft(s1, Wm, W, mk, mv, lens, hid, res.n_accept, res.out_tokens, u_dr[b:b + 1], k, mode, 1.0,
+                         rnd)
+        t3 = time.perf_counter()
+        head = t2 - t1
+        t_layer += (t1 - t0) - head        # the layer alone: the forward less its LM head
+        t_rest += head + (t3 - t2)
+        nseq += 1
+    t_step = wl.shape.n_layers * t_layer + t_rest
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": tau * nseq / t_step, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": "extrapolated: one of the %d layers timed on %d of %d sequences of this workload's context mix "
+                      "(%.1f s), scaled to %d layers, plus the LM head, accept, commit and MTP draft timed once per "
+                      "sequence (%.1f s); committed tokens per sequence per step from the GPU run (%.2f)"
+                      % (wl.shape.n_layers, nseq, wl.batch, t_layer, wl.shape.n_layers, t_rest, tau)}
 
 
 # ----------------------------------------------------------------------------- other configurations
@@ -719,8 +775,8 @@ def main():
                        "record_topk": args.record, "top_p": args.top_p,
                        "target_stats": args.target_stats},
             "roofline": roof, "roofline_targets": targets, "summary": summary, "kernels": kernels}
+    weights = None
     if not args.no_cpu_baseline:
-        weights = None
         if hasattr(step, "W"):
             weights = (step.W, step.Wm) if wl.with_mtp else (step.W,)
         line["cpu_baseline"] = cpu_baseline(wl, args.mode, args.cpu_budget, weights, args.top_p)
@@ -733,6 +789,16 @@ def main():
         for name in EXTRA:
             if name != args.workload:
                 line["workloads"][name] = measure_workload(name, args.mode, args.extra_steps)
+        # the oracle beside them, on bounded samples: the small configurations directly, the
+        # 36-layer Qwen3-4B shape from one of its layers (the layer workload's weights)
+        if not args.no_cpu_baseline:
+            for name, budget in (("tiny", 3.0), ("long_ctx", 8.0)):
+                if name in line["workloads"]:
+                    line["workloads"][name]["cpu_baseline"] = cpu_baseline(synth.WORKLOADS[name], args.mode, budget)
+            if "qwen3_4b_full" in line["workloads"] and weights is not None and wl.name == "qwen3_4b_layer":
+                w3 = line["workloads"]["qwen3_4b_full"]
+                w3["cpu_baseline"] = cpu_layer_extrapolated(synth.WORKLOADS["qwen3_4b_full"], wl, weights, args.mode,
+                                                            10.0, w3["tau"])
     for name, row in kernels.items():
         log("[bench] %-24s %s" % (name, row))
     print(json.dumps(line), flush=True)

@@ -1,8 +1,8 @@
 """GPU parity of the top-p variant of gm_spec_accept (the evaluation setting of
 App. "Evaluation Configuration": rejection sampling at T = 1, top-p 0.7) against
 the oracle on the same seeded logits.  The drafts are samples of the head's
-nucleus.  Accept counts and committed tokens must match bit for bit outside the
-flag windows (|u - min(1, p/q)| < 1e-3, a final draw within the derived float32
+nucleus (and, in the handoff test, the oracle's own draft head's draws).  Accept
+counts and committed tokens must match bit for bit outside the flag windows (|u - min(1, p/q)| < 1e-3, a final draw within the derived float32
 bound ``draw_window`` of a CDF edge, and a nucleus whose boundary lies within
 5e-9 of top_p); the flagged count is printed."""
 import numpy as np
@@ -171,8 +171,8 @@ def test_top_p_nucleus_handoff():
 
 
 def _chain_flags(zt, zq, d_ref, n_ref, dev, ua, uf, ud, top_p, window):
-    """Per sequence, how far the oracle's draft-and-accept chain stays comparable when the GPU's
-    draft logits sit within dev[b, j] (max over the row) of the oracle's.  Walks the examined
+    """Per sequence, how far the oracle's draft-and-accept chain (at T = 1) stays comparable when
+    the GPU's draft logits sit within dev[b, j] (max over the row) of the oracle's.  Walks the examined
     events in order -- draw j, accept test j, then the final draw -- and stops at the first one
     that such a deviation D could move:
       * the draw of d_j from the nucleus of q_j: the nucleus changes if the logit just below its

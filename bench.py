@@ -115,6 +115,54 @@ def accounting(wl, lens, top_p=1.0, record=0, target_stats=False):
 
 
 # ----------------------------------------------------------------------------- workloads
+class StepEvents:
+    """HIP timing events on torch's current stream that record without the system-scope fence
+    of a default event (hipEventDisableSystemFence).  Only their timestamps are read; the
+    fence's cache write-back would leave the stream idle for several microseconds at every
+    record, inside the timed region."""
+    _FLAG = 0x20000000
+
+    def __init__(self, n):
+        import ctypes
+        import torch
+        self._c, self._torch = ctypes, torch
+        hip = ctypes.CDLL("libamdhip64.so.7")   # resolves to the HIP runtime torch has loaded
+        hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+        hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self._hip = hip
+        self._ev = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            self._check(hip.hipEventCreateWithFlags(ctypes.byref(e), self._FLAG), "CreateWithFlags")
+            self._ev.append(e)
+
+    @staticmethod
+    def _check(rc, what):
+        if rc != 0:
+            raise RuntimeError("hipEvent%s failed with HIP error %d" % (what, rc))
+
+    def record(self, i):
+        self._check(self._hip.hipEventRecord(self._ev[i], self._torch.cuda.current_stream().cuda_stream), "Record")
+
+    def elapsed(self, i, j):
+        """Milliseconds from event i to event j (waits for j)."""
+        ms = self._c.c_float()
+        self._check(self._hip.hipEventSynchronize(self._ev[j]), "Synchronize")
+        self._check(self._hip.hipEventElapsedTime(self._c.byref(ms), self._ev[i], self._ev[j]), "ElapsedTime")
+        return ms.value
+
+    def per_step(self):
+        return [self.elapsed(i, i + 1) for i in range(len(self._ev) - 1)]
+
+    def close(self):
+        for e in self._ev:
+            self._hip.hipEventDestroy(e)
+        self._ev = []
+
+
 class Step:
     """Device state of one workload and the enqueue of one step."""
 
@@ -151,6 +199,7 @@ class Step:
                                    page_size=wl.page_size, fill="empty")
         random_pools(self.cache)
         self.lens0 = self.cache.seq_lens.clone()
+        self.lens_both = None
         V = s.vocab
         u_acc, u_fin, u_dr = synth.uniforms(B, k)
         dev = lambda a, dt=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).to(device=device, dtype=dt)
@@ -193,6 +242,10 @@ class Step:
                 self.mtp = gm.DeviceMtp(s, self.Wm, device)
                 self.mcache = gm.PagedCache(s, 1, self.lens, cap, page_size=wl.page_size, fill="empty")
                 random_pools(self.mcache)
+                # both caches' lengths in one tensor: one copy per step puts them back
+                both = torch.stack([self.cache.seq_lens, self.mcache.seq_lens])
+                self.cache.seq_lens, self.mcache.seq_lens = both[0], both[1]
+                self.lens_both, self.lens_both0 = both, both.clone()
                 self.next_drafts = torch.zeros((B, k), dtype=torch.int32, device=device)
                 self.dlog = torch.zeros((B, k, V), dtype=torch.float32, device=device)
                 if self.chain:   # the head writes one pair while the accept reads the other
@@ -232,7 +285,10 @@ class Step:
         k = wl.k
         if self.chain:
             return self._chain_step()
-        self.cache.seq_lens.copy_(self.lens0)
+        if self.lens_both is not None:
+            self.lens_both.copy_(self.lens_both0)
+        else:
+            self.cache.seq_lens.copy_(self.lens0)
         if wl.name == "long_ctx":
             gm.verify_attention(self.cfg, self.cache, 0, self.q, self.attn_out, self.ws_v)
             gm.spec_accept(self.zt, self.zq, self.drafts, self.ua, self.uf, self.n, self.out, self.mode, self.ws_a,
@@ -247,7 +303,6 @@ class Step:
                        target_stats=self.tstats)
         gm.kv_commit(self.cache, k, self.n, self.slots)
         if wl.with_mtp and draft:
-            self.mcache.seq_lens.copy_(self.lens0)
             gm.mtp_draft(self.model, self.mtp, self.mcache, k, self.mode, self.hidden, self.n, self.out, self.ud,
                          self.next_drafts, self.dlog, self.ws_m, draft_stats=self.next_stats if handoff else None,
                          top_p=self.top_p)
@@ -518,20 +573,22 @@ def measure_workload(name, mode, steps, warmup=2):
     st()
     per_kernel = gm.trace_stop()
     committed = torch.zeros((), dtype=torch.int64, device="cuda")
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
-    evs[0].record()
+    evs = StepEvents(steps + 1)
+    evs.record(0)
     for i in range(steps):
         st()
-        evs[i + 1].record()
+        evs.record(i + 1)
         if chain:
             committed += (st.n + 1).sum()
     torch.cuda.synchronize()
-    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
+    per_step = evs.per_step()
+    ms_all = evs.elapsed(0, steps) / steps
+    evs.close()
     med = float(np.median(per_step))
     tokens = int(committed.item()) / steps if chain else int((st.n + 1).sum().item())
     acc = accounting(wl, st.lens)
     out = {"description": DESCRIPTIONS[name], "batch": wl.batch, "k": wl.k, "steps": steps,
-           "ms_per_step": round(evs[0].elapsed_time(evs[-1]) / steps, 4), "ms_per_step_median": round(med, 4),
+           "ms_per_step": round(ms_all, 4), "ms_per_step_median": round(med, 4),
            "tokens_per_s_median": round(tokens / (med / 1e3), 1), "committed_tokens_per_step": tokens,
            "tau": round(tokens / wl.batch, 4), "setup_s": round(setup_s, 1),
            "drafts": "the head's own chain, fed back step to step" if chain else
@@ -543,13 +600,14 @@ def measure_workload(name, mode, steps, warmup=2):
         st.mode = other
         for _ in range(warmup):
             st()
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
-        ev[0].record()
+        ev = StepEvents(steps + 1)
+        ev.record(0)
         for i in range(steps):
             st()
-            ev[i + 1].record()
+            ev.record(i + 1)
         torch.cuda.synchronize()
-        med2 = float(np.median([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]))
+        med2 = float(np.median(ev.per_step()))
+        ev.close()
         tok2 = int((st.n + 1).sum().item())
         out["greedy" if other == gm.GM_GREEDY else "sample"] = {
             "ms_per_step_median": round(med2, 4), "tokens_per_s_median": round(tok2 / (med2 / 1e3), 1),
@@ -646,19 +704,24 @@ def main():
     per_kernel = gm.trace_stop()
     dominant = max(per_kernel, key=lambda n: per_kernel[n][1])
 
-    # timed region: K steps, a HIP event after each; the dominant kernel's launches are also
-    # bracketed by HIP events on their stream (its average launch duration for the roofline)
+    # timed region: K steps, a HIP event after each; launches of the dominant kernel are also
+    # bracketed by HIP events on their stream (its average launch duration for the roofline).
+    # Each pair of events leaves the stream idle for a few microseconds, so only every
+    # (L + 1)-th of its launches is bracketed, L its launches per step: about one per step,
+    # each of its L places in the step in turn.
+    dom_per_step = max(1, per_kernel[dominant][0] // probe_steps)
     torch.cuda.synchronize()
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    gm.trace_start(dominant)
-    evs[0].record()
+    evs = StepEvents(args.steps + 1)
+    gm.trace_start(dominant, every=dom_per_step + 1)
+    evs.record(0)
     for i in range(args.steps):
         sets[i % len(sets)]()
-        evs[i + 1].record()
+        evs.record(i + 1)
     torch.cuda.synchronize()
     dom = gm.trace_stop()[dominant]
-    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
-    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    per_step = evs.per_step()
+    ms = evs.elapsed(0, args.steps) / args.steps
+    evs.close()
     ms_median = float(np.median(per_step))
     if n_ref is None:
         n_ref = sets[0].n.clone()
@@ -703,6 +766,7 @@ def main():
         roof["kernel"] = dominant
         roof["avg_launch_ms"] = round(dom_ms, 4)
         roof["launches"] = dom[0]
+        roof["launch_sample"] = "every %d-th launch of the timed region" % (dom_per_step + 1)
     else:
         roof = {"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None,
                 "kernel": dominant}
@@ -714,13 +778,14 @@ def main():
         for i in range(2 * len(sets)):
             sets[i % len(sets)](draft=False)
         torch.cuda.synchronize()
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-        ev[0].record()
+        ev = StepEvents(args.steps + 1)
+        ev.record(0)
         for i in range(args.steps):
             sets[i % len(sets)](draft=False)
-            ev[i + 1].record()
+            ev.record(i + 1)
         torch.cuda.synchronize()
-        vo = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+        vo = ev.per_step()
+        ev.close()
         verify_only = {"ms_per_step_median": round(float(np.median(vo)), 4),
                        "tokens_per_s": round(committed / (float(np.median(vo)) / 1e3), 1),
                        "what": "verify forward + accept + commit, no draft head"}

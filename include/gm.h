@@ -372,7 +372,12 @@ const char *gm_last_error(void);
 /* Kernel timing.  While tracing is on, every kernel the library launches
  * whose name matches `filter` (all kernels when NULL) is bracketed by a pair
  * of HIP events on its stream.  gm_trace_stop() waits for the recorded events
- * and sums their durations per kernel name. */
+ * and sums their durations per kernel name.  The events record timestamps
+ * only (no system-scope fence); each still leaves the stream idle for a few
+ * microseconds.  gm_trace_every(n) (n >= 1, else GM_ERR_INVALID_ARG; default
+ * 1) brackets only every n-th matching launch, counted from gm_trace_start, so
+ * that a timing sample perturbs fewer launches. */
+gm_status gm_trace_every(int n);
 gm_status gm_trace_start(const char *filter);
 gm_status gm_trace_stop(void);
 int gm_trace_count(void);

@@ -1,11 +1,13 @@
 // Kernel timing with HIP events (gm_trace_*): while tracing is on, each
-// launch whose kernel name matches the filter is bracketed by two events on
-// its stream; stopping waits for them and sums the durations per name.
+// launch whose kernel name matches the filter (or every n-th of them, after
+// gm_trace_every(n)) is bracketed by two events on its stream; stopping waits
+// for them and sums the durations per name.
 #include <mutex>
 #include <string>
 #include <vector>
 
 #include "../../include/gm.h"
+#include "forward.h"
 #include "launch.h"
 
 namespace gm {
@@ -22,6 +24,8 @@ struct Sum {
 std::mutex g_mu;
 bool g_on = false;
 bool g_filtered = false;
+int g_every = 1;       // bracket every g_every-th matching launch
+long g_matched = 0;    // matching launches since gm_trace_start
 std::string g_filter;
 std::vector<Rec> g_recs;
 std::vector<hipEvent_t> g_pool;
@@ -33,8 +37,10 @@ hipEvent_t take_event() {
     g_pool.pop_back();
     return e;
   }
+  // timestamps only: no system-scope fence on record, whose cache write-back would leave the
+  // stream idle for several microseconds on each side of a traced launch
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 }  // namespace
@@ -43,6 +49,7 @@ TraceScope::TraceScope(const char *name, hipStream_t s) : slot(-1), stream(s) {
   if (!g_on) return;
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_on || (g_filtered && g_filter != name)) return;
+  if (g_matched++ % g_every != 0) return;
   Rec r{name, take_event(), take_event()};
   if (!r.a || !r.b) return;
   (void)hipEventRecord(r.a, s);
@@ -67,7 +74,15 @@ extern "C" gm_status gm_trace_start(const char *filter) {
   g_sums.clear();
   g_filtered = filter != nullptr;
   g_filter = filter ? filter : "";
+  g_matched = 0;
   g_on = true;
+  return GM_OK;
+}
+
+extern "C" gm_status gm_trace_every(int n) {
+  if (n < 1) return set_error(GM_ERR_INVALID_ARG, "gm_trace_every: n must be >= 1");
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_every = n;
   return GM_OK;
 }
 

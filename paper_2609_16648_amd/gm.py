@@ -65,7 +65,7 @@ class KVCacheDesc(ctypes.Structure):
 _lib = None
 
 EXPORTS = ["gm_workspace_size", "gm_verify_forward", "gm_verify_attention", "gm_spec_accept", "gm_kv_commit",
-           "gm_mtp_draft", "gm_mtp_reconstruct", "gm_dca_loss", "gm_last_error", "gm_trace_start", "gm_trace_stop", "gm_trace_count", "gm_trace_get", "gm_spec_accept_noalloc"]
+           "gm_mtp_draft", "gm_mtp_reconstruct", "gm_dca_loss", "gm_last_error", "gm_trace_every", "gm_trace_start", "gm_trace_stop", "gm_trace_count", "gm_trace_get", "gm_spec_accept_noalloc"]
 
 
 def lib() -> ctypes.CDLL:
@@ -107,6 +107,8 @@ def lib() -> ctypes.CDLL:
                               c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
     L.gm_last_error.restype = ctypes.c_char_p
     L.gm_last_error.argtypes = []
+    L.gm_trace_every.restype = c_int
+    L.gm_trace_every.argtypes = [c_int]
     L.gm_trace_start.restype = c_int
     L.gm_trace_start.argtypes = [ctypes.c_char_p]
     L.gm_trace_stop.restype = c_int
@@ -516,7 +518,10 @@ def dca_loss(head_logits: torch.Tensor, rec_logp: torch.Tensor, rec_ids: torch.T
 
 
 # ------------------------------------------------------------------------ kernel timing
-def trace_start(filter_name: Optional[str] = None):
+def trace_start(filter_name: Optional[str] = None, every: int = 1):
+    """Starts tracing the launches of `filter_name` (all kernels when None), every `every`-th
+    matching launch."""
+    _check(lib().gm_trace_every(every))
     _check(lib().gm_trace_start(filter_name.encode() if filter_name else None))
 
 

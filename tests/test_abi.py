@@ -234,6 +234,15 @@ def test_workspace_size_null_config():
         assert L.gm_workspace_size(op, None, 8, 3, 1024) == 0
 
 
+def test_trace_sampling_argument():
+    # the sampling stride is checked on the host (no GPU here)
+    L = gm.lib()
+    assert L.gm_trace_every(0) == gm.GM_ERR_INVALID_ARG and "gm_trace_every" in gm.last_error()
+    assert L.gm_trace_every(-3) == gm.GM_ERR_INVALID_ARG
+    assert L.gm_trace_every(4) == gm.GM_OK
+    assert L.gm_trace_every(1) == gm.GM_OK
+
+
 def test_spec_accept_noalloc_rejects_on_the_host():
     # oversized calls and bad shapes fail before the device is touched (no GPU here)
     L = gm.lib()

@@ -59,6 +59,8 @@ constexpr int kGemmBufs = 3;              // A chunks in LDS (the loader runs tw
 // lgkmcnt 11:8; the other counters left at their maximum, i.e. not waited on)
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 constexpr int kVmcnt0 = waitcnt_vm(0);
+// instruction classes of __builtin_amdgcn_sched_group_barrier
+constexpr int kSchedMfma = 0x008, kSchedDsRead = 0x100;
 
 // logical tile index of workgroup `bid`: workgroups are dealt round-robin to
 // the 8 XCDs; consecutive logical indices (same weight strip) share an XCD
@@ -80,6 +82,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
   constexpr int SPC = BKA / 32;               // k32 steps per chunk
   constexpr int D = NT >= 4 ? 4 : 8;          // W prefetch depth (k32 steps)
   static_assert(EPI != EPI_STATS || 16 * NT * WN == kStatCols, "tile statistics cover one workgroup's columns");
+  constexpr int PA = MT >= 8 ? 4 : MT;        // A fragments read ahead (all of them up to 64 rows)
   constexpr int ITER = D > SPC ? D : SPC;     // k32 steps per unrolled iteration
   constexpr int CB = BKA / 8;                 // 16-byte column blocks per A row of a chunk
   constexpr int SWZ = CB < 16 ? CB - 1 : 15;  // XOR swizzle of the column block by the row
@@ -188,18 +191,31 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
           ring[(u + D - 1) % D][t] = load_w<SW>(wbase[t] + (long)min(s + D - 1, nsteps - 1) * kWStep);
         __builtin_amdgcn_sched_barrier(0);
         const uint4 (&wv)[NT] = ring[u % D];
+        // A fragments from LDS, PA reads ahead of the MFMAs that use them; left to itself the
+        // compiler keeps only two in flight and waits out their latency before every pair
         bf16x8_t af[MT];
-#pragma unroll
-        for (int a = 0; a < MT; ++a) {
+        auto read_a = [&](int a) {
           const int rr = wm * 16 * MT + 16 * a + j;
           const int p = ((ko >> 3) + g4) ^ (rr & SWZ);
           af[a] = as_bf16x8(*reinterpret_cast<const uint4 *>(&As[buf][rr * BKA + 8 * p]));
-        }
+        };
 #pragma unroll
-        for (int a = 0; a < MT; ++a)
+        for (int a = 0; a < PA; ++a) read_a(a);
+#pragma unroll
+        for (int a = 0; a < MT; ++a) {
+          if (a + PA < MT) read_a(a + PA);
 #pragma unroll
           for (int t = 0; t < NT; ++t)
             acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], as_bf16x8(wv[t]), acc[a][t], 0, 0, 0);
+        }
+        if (PA < MT) {   // the order above, held against the scheduler: PA reads, then a read per MFMA group
+          __builtin_amdgcn_sched_group_barrier(kSchedDsRead, PA, 0);
+#pragma unroll
+          for (int a = 0; a < MT; ++a) {
+            if (a + PA < MT) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, NT, 0);
+          }
+        }
         if ((u % SPC) == SPC - 1) __syncthreads();   // barrier s / SPC + 1: done with this chunk
       }
     }

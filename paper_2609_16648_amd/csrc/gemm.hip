@@ -430,20 +430,28 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF g) {
 // ------------------------------------------------------------------ LM head, M <= 64
 // Persistent strip ranges: as many waves as the chip holds, each owning a
 // contiguous range of 16-column weight strips (at most kLmStrips, balanced to
-// within one strip over all waves) over the whole K.  Every wave is on its own:
-// the weight tiles and the activation fragments (64 rows, read from L2 in the
-// A-operand order) stream through a kLmRing-step register ring with
-// unconditional loads, and there is no LDS and no barrier, so no wave ever
-// waits for another.  EPI_STATS: the softmax statistics of Y / T are taken per
+// within one strip over all waves) over the whole K.  A wave streams its weight
+// tiles through a kLmRing-step register ring with unconditional loads (every
+// wave loads kLmStrips strips, the last one again where its range is shorter,
+// so the four waves of a workgroup keep pace).  The activation fragments (64
+// rows) are shared by the workgroup's four waves: each stages a quarter of every
+// kLmChunk-step chunk in LDS, in the A-operand order, with direct-to-LDS loads one
+// chunk ahead, and one barrier per chunk hands the chunk over (measured at 64
+// rows: 144-147 us per launch against 152-158 us with every wave reading its own
+// fragments from L2).  EPI_STATS: the softmax statistics of Y / T are taken per
 // row over the wave's own range (float32 terms, summed per lane in float32, the
 // 16 lane sums of a row in float64), one RowStat per (row, wave): the tiles of
 // the draw are the waves' ranges.
 constexpr int kLmStrips = 10;
-// Two slots: one k-step (14 KiB per wave) in flight while the other is consumed.  With four
-// waves per CU that is about as much as the HBM queues serve best; deeper rings put more in
-// flight and were slower (measured at 64 rows: 2 slots 146 us per launch, 4 slots 151 us,
-// 5 slots 152 us).
+// Two slots: one k-step (10 KiB of weights per wave) in flight while the other is consumed.
+// With four waves per CU that is about as much as the HBM queues serve best; deeper rings put
+// more in flight and were slower (measured at 64 rows: 2 slots 146 us per launch, 4 slots
+// 151 us, 5 slots 152 us).
 constexpr int kLmRing = 2;
+// k-steps per activation chunk (4 KiB per k-step for 64 rows; two chunk buffers).  Two-step
+// chunks, two ahead, took 151-153 us; an odd count makes the ring slot of a step dynamic.
+constexpr int kLmChunk = 4;
+static_assert(kLmChunk % kLmRing == 0, "a chunk covers whole ring turns");
 static_assert(kLmStrips * kStripIds <= kMaxDrawTileIds, "the draw scans a whole strip range");
 
 struct GemmL {
@@ -459,16 +467,18 @@ struct GemmL {
 template <int EPI>
 __global__ __launch_bounds__(256) void lm_strips_kernel(GemmL g) {
   const int lane = threadIdx.x & 63, j = lane & 15, g4 = lane >> 4;
-  const int wid = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
-  if (wid >= g.geo.tiles) return;
-  const int s0 = tile_first_strip(g.geo, wid), n = tile_first_strip(g.geo, wid + 1) - s0;   // 1 .. kLmStrips
-  const int ksteps = g.K / 32;   // a multiple of kLmRing
+  const int wv = threadIdx.x >> 6;
+  const int wid = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + wv);
+  // a wave past the last range still stages its share of the activations and meets the
+  // barriers (streaming strip 0), then leaves before the epilogue
+  const bool active = wid < g.geo.tiles;
+  const int s0 = active ? tile_first_strip(g.geo, wid) : 0;
+  const int n = active ? tile_first_strip(g.geo, wid + 1) - s0 : 1;   // 1 .. kLmStrips
+  const int ksteps = g.K / 32;   // a multiple of kLmChunk
+  const int nchunks = ksteps / kLmChunk;
   const uint16_t *wb[kLmStrips];
 #pragma unroll
   for (int t = 0; t < kLmStrips; ++t) wb[t] = g.W + w_tile(s0 + min(t, n - 1), 0, ksteps) + lane * 8;
-  const uint16_t *ab[4];   // A fragment of row tile a: row 16 a + j (rows past M re-read row M - 1), k 8 g4 ..
-#pragma unroll
-  for (int a = 0; a < 4; ++a) ab[a] = g.X + (long)min(16 * a + j, g.M - 1) * g.ldx + 8 * g4;
 
   floatx4_t acc[4][kLmStrips];
 #pragma unroll
@@ -476,34 +486,62 @@ __global__ __launch_bounds__(256) void lm_strips_kernel(GemmL g) {
 #pragma unroll
     for (int t = 0; t < kLmStrips; ++t) acc[a][t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  uint4 ra[kLmRing][4], rw[kLmRing][kLmStrips];
-  auto load = [&](int slot, int step) {
+  // Activation chunk c in As[c % 2], 1 KiB per (k-step st, row tile a) at (4 st + a) KiB:
+  // lane l holds row 16 a + (l & 15) (rows past M re-read row M - 1), k 8 (l >> 4) ..
+  // of that step, i.e. the A operand as the MFMA takes it.  Wave w stages the loads
+  // u = kLmChunk w .. kLmChunk (w + 1) - 1.
+  __shared__ uint16_t As[2][kLmChunk * 4 * 512];
+  auto issue_a = [&](int c) {
+    const int cc = min(c, nchunks - 1);   // past the end: the last chunk again, into the free buffer
+    uint16_t *dst = &As[c % 2][0];
+#pragma unroll
+    for (int q = 0; q < kLmChunk; ++q) {
+      const int u = wv * kLmChunk + q, st = u >> 2, a = u & 3;
+      const uint16_t *src = g.X + (long)min(16 * a + j, g.M - 1) * g.ldx + (kLmChunk * cc + st) * 32 + 8 * g4;
+      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)(dst + u * 512), 16, 0, 0);
+    }
+  };
+  uint4 rw[kLmRing][kLmStrips];
+  auto load_w_step = [&](int slot, int step) {
 #pragma unroll
     for (int t = 0; t < kLmStrips; ++t) rw[slot][t] = load_w<true>(wb[t] + (long)step * kWStep);
-#pragma unroll
-    for (int a = 0; a < 4; ++a) ra[slot][a] = *reinterpret_cast<const uint4 *>(ab[a] + step * 32);
   };
-#pragma unroll
-  for (int d = 0; d < kLmRing - 1; ++d) {   // in slot order: the ring's waits count on it
-    __builtin_amdgcn_sched_barrier(0);
-    load(d, d);
-  }
+  // The load order fixes the waits: A(0), the weights of steps 0 .. kLmRing - 2; then per
+  // chunk c: A(c + 1), and per step s the weights of step s + kLmRing - 1.
   __builtin_amdgcn_sched_barrier(0);
-  for (int s0k = 0; s0k < ksteps; s0k += kLmRing) {
+  issue_a(0);
 #pragma unroll
-    for (int d = 0; d < kLmRing; ++d) {
-      // refill the slot consumed last step (a re-read of the last step near the end)
+  for (int d = 0; d < kLmRing - 1; ++d) load_w_step(d, d);
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm((kLmRing - 1) * kLmStrips));   // A(0) landed
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  for (int c = 0; c < nchunks; ++c) {
+#pragma unroll
+    for (int d = 0; d < kLmChunk; ++d) {
+      const int s = kLmChunk * c + d;
       __builtin_amdgcn_sched_barrier(0);
-      load((d + kLmRing - 1) % kLmRing, min(s0k + d + kLmRing - 1, ksteps - 1));
+      if (d == 0) issue_a(c + 1);   // into the buffer of chunk c - 1, released by the last barrier
+      load_w_step((d + kLmRing - 1) % kLmRing, min(s + kLmRing - 1, ksteps - 1));
       __builtin_amdgcn_sched_barrier(0);
+      bf16x8_t af[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+        af[a] = as_bf16x8(*reinterpret_cast<const uint4 *>(&As[c % 2][(d * 4 + a) * 512 + lane * 8]));
 #pragma unroll
       for (int a = 0; a < 4; ++a)
 #pragma unroll
         for (int t = 0; t < kLmStrips; ++t)
-          acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ra[d][a]), as_bf16x8(rw[d][t]), acc[a][t], 0,
-                                                              0, 0);
+          acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], as_bf16x8(rw[d % kLmRing][t]), acc[a][t], 0, 0, 0);
     }
+    // A(c + 1) landed: issued after it, the weights of this chunk's kLmChunk steps
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(kLmChunk * kLmStrips));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
   }
+  __builtin_amdgcn_s_waitcnt(kVmcnt0);   // the clamped re-reads past the end, before the waves leave
+  if (!active) return;
 
   // lane holds C[row 16 a + 4 g4 + r][col 16 (s0 + t) + j]
 #pragma unroll
@@ -530,7 +568,6 @@ __global__ __launch_bounds__(256) void lm_strips_kernel(GemmL g) {
     __shared__ float sh_part[4][64 * 17];   // [row][lane group j], padded
     __shared__ int sh_arg[4][64 * 17];
     __shared__ float sh_rmax[4][64];
-    const int wv = threadIdx.x >> 6;
     float *pf = sh_part[wv], *rmax = sh_rmax[wv];
     int *pa = sh_arg[wv];
 #pragma unroll
@@ -674,7 +711,7 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
 // kernel's waves (bf16, M <= 64), else tiles of 8 strips (128 ids).
 TileGeom plan_lm_head(int dtype, int M, int V, int K, bool *strips_kernel) {
   if (strips_kernel) *strips_kernel = false;
-  if (dtype != GM_BF16 || M > 64 || V % kStripIds || K % (32 * kLmRing)) return fixed_tiles(V);
+  if (dtype != GM_BF16 || M > 64 || V % kStripIds || K % (32 * kLmChunk)) return fixed_tiles(V);
   const int S = V / kStripIds;
   int waves = lm_resident_waves();
   if (waves > S) waves = S;

@@ -452,6 +452,7 @@ constexpr int kLmRing = 2;
 // chunks, two ahead, took 151-153 us; an odd count makes the ring slot of a step dynamic.
 constexpr int kLmChunk = 4;
 static_assert(kLmChunk % kLmRing == 0, "a chunk covers whole ring turns");
+static_assert(kLmChunk * kLmStrips <= 63, "the chunk's wait counts its weight loads in the 6-bit vmcnt");
 static_assert(kLmStrips * kStripIds <= kMaxDrawTileIds, "the draw scans a whole strip range");
 
 struct GemmL {

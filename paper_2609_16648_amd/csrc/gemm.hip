@@ -52,7 +52,8 @@ struct GemmS {
 
 __device__ __forceinline__ float silu(float x) { return x / (1.f + expf(-x)); }
 
-constexpr int kGemmThreads = 5 * kWave;   // four compute waves and one A-staging wave
+// CW compute waves and one A-staging wave
+template <int CW> constexpr int gemm_threads() { return (CW + 1) * kWave; }
 constexpr int kStatCols = kMaxTileStrips * kStripIds;   // columns per statistics tile of the tiled GEMM
 constexpr int kGemmBufs = 3;              // A chunks in LDS (the loader runs two ahead)
 // s_waitcnt immediates (gfx9 encoding: vmcnt bits 3:0 and 15:14, expcnt 6:4,
@@ -71,12 +72,15 @@ __device__ __forceinline__ int xcd_remap(int bid, int T) {
 
 // MT: 16-row tiles per compute wave; NT: 16-column strips per compute wave;
 // WM: compute waves along M (1 or 2); SW: weights loaded non-temporally (one M
-// tile).  Waves 0-3 compute; wave 4 only stages
-// the A chunks in LDS.  The wait counter of loads is per wave, so the loader's
-// waits for A never drain the compute waves' weight ring.
-template <int MT, int NT, int WM, int EPI, bool SW>
-__global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
-  constexpr int WN = 4 / WM;
+// tile); CW: compute waves (4, or 7 for wide outputs: two per SIMD on three of
+// the SIMDs, 224-column tiles, the last tile of a launch clamped to the
+// output).  Waves 0 .. CW - 1 compute; wave CW only stages the A chunks in LDS.
+// The wait counter of loads is per wave, so the loader's waits for A never
+// drain the compute waves' weight ring.
+template <int MT, int NT, int WM, int EPI, bool SW, int CW>
+__global__ __launch_bounds__(gemm_threads<CW>()) void gemm_stream_kernel(GemmS g) {
+  static_assert(CW % WM == 0, "compute waves tile the rows evenly");
+  constexpr int WN = CW / WM;
   constexpr int BM = 16 * MT * WM;            // rows per workgroup
   constexpr int BKA = (BM >= 256 ? 16384 : 8192) / BM;   // k per LDS chunk of A (16 KiB; 32 KiB at 256 rows)
   constexpr int SPC = BKA / 32;               // k32 steps per chunk
@@ -94,7 +98,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
   __shared__ uint16_t As[kGemmBufs][BM * BKA];
 
   const int tid = threadIdx.x, lane = tid & 63;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // 4: the loader wave
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // CW: the loader wave
   const int wm = w % WM, wn = w / WM;
   const int j = lane & 15, g4 = lane >> 4;
   const int T = g.n_tiles * g.m_tiles * g.splits;
@@ -131,7 +135,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
   // finished chunk c - 1".  Chunk c lives in As[c % 3]; the buffer was last used
   // by chunk c - 3, finished before barrier c - 2, so the loader starts chunk c
   // right after barrier c - 2 and has two chunks of compute time to land it.
-  if (w == 4) {
+  if (w == CW) {
     // Direct-to-LDS loads: lane l of load u fills the 16 bytes at u KiB + 16 l of the
     // chunk, i.e. row e / CB, block e % CB (e = 64 u + l); the lane fetches the
     // global block that the swizzle puts there.  No registers hold A, and this
@@ -164,7 +168,8 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
     const int kt_total = g.K / 32;
     const uint16_t *wbase[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) wbase[t] = g.W + w_tile(strip[t], k_begin / 32, kt_total) + lane * 8;
+    for (int t = 0; t < NT; ++t)   // strips past the output (the last 224-column tile) re-read the last one
+      wbase[t] = g.W + w_tile(CW == 4 ? strip[t] : min(strip[t], g.Nw / 16 - 1), k_begin / 32, kt_total) + lane * 8;
     // Slot d of the ring holds step d mod D.  Each step first refills the slot
     // consumed by the step before (its registers are dead), then consumes its
     // own: a load never targets a register still waiting for its reader, so the
@@ -237,7 +242,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
 #pragma unroll
     for (int h = 0; h < BM / RP; ++h) {
       __syncthreads();
-      if (w < 4) {
+      if (w < CW) {
 #pragma unroll
         for (int a = 0; a < MT; ++a) {
           const int r0 = wm * 16 * MT + 16 * a;
@@ -250,7 +255,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
         }
       }
       __syncthreads();
-      for (int rl = tid; rl < RP; rl += kGemmThreads) {
+      for (int rl = tid; rl < RP; rl += gemm_threads<CW>()) {
         const int m = m0 + h * RP + rl;
         if (m >= g.M) continue;
         const float4 *src = reinterpret_cast<const float4 *>(tl + rl * LS);
@@ -279,7 +284,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
     }
   }
 
-  if (w < 4) {
+  if (w < CW) {
   // lane holds C[row 16a + 4 g4 + r][col 16t + j] of the wave tile
 #pragma unroll
   for (int a = 0; a < MT; ++a) {
@@ -299,6 +304,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_stream_kernel(GemmS g) {
       } else {
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
+          if (CW != 4 && strip[t] >= g.Nw / 16) continue;
           const long o = (long)m * g.ldy + strip[t] * 16 + j;
           const float v = acc[a][t][r];
           if (EPI == EPI_STORE_F32 || EPI == EPI_STATS) ((float *)g.Y)[o] = v;
@@ -643,19 +649,30 @@ int lm_resident_waves() {
   return v;
 }
 
-template <int MT, int NT, int WM, int EPI>
+template <int MT, int NT, int WM, int EPI, int CW>
 void launch_stream(const GemmS &g, hipStream_t s) {
   const dim3 grid(g.n_tiles * g.m_tiles * g.splits);
-  if (g.m_tiles == 1) hipLaunchKernelGGL((gemm_stream_kernel<MT, NT, WM, EPI, true>), grid, dim3(kGemmThreads), 0, s, g);
-  else hipLaunchKernelGGL((gemm_stream_kernel<MT, NT, WM, EPI, false>), grid, dim3(kGemmThreads), 0, s, g);
+  if (g.m_tiles == 1)
+    hipLaunchKernelGGL((gemm_stream_kernel<MT, NT, WM, EPI, true, CW>), grid, dim3(gemm_threads<CW>()), 0, s, g);
+  else
+    hipLaunchKernelGGL((gemm_stream_kernel<MT, NT, WM, EPI, false, CW>), grid, dim3(gemm_threads<CW>()), 0, s, g);
 }
 
 template <int EPI>
-void launch_stream_shape(int shape, const GemmS &g, hipStream_t s) {
-  switch (shape) {   // every tile is 128 columns wide: one tile-statistics block each
-    case 0: launch_stream<4, 2, 1, EPI>(g, s); break;    // 64 x 128 tiles
-    case 1: launch_stream<8, 2, 1, EPI>(g, s); break;    // 128 x 128 tiles
-    default: launch_stream<16, 2, 1, EPI>(g, s); break;  // 256 x 128 tiles
+void launch_stream_shape(int shape, int cw, const GemmS &g, hipStream_t s) {
+  // four compute waves: 128-column tiles, one tile-statistics block each; seven (plain
+  // stores and the residual add only): 224-column tiles
+  if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_ADD_F32 || EPI == EPI_STORE_ACT) {
+    if (cw == 7) {
+      if (shape == 1) launch_stream<8, 2, 1, EPI, 7>(g, s);   // 128 x 224 tiles
+      else launch_stream<16, 2, 1, EPI, 7>(g, s);             // 256 x 224 tiles
+      return;
+    }
+  }
+  switch (shape) {
+    case 0: launch_stream<4, 2, 1, EPI, 4>(g, s); break;    // 64 x 128 tiles
+    case 1: launch_stream<8, 2, 1, EPI, 4>(g, s); break;    // 128 x 128 tiles
+    default: launch_stream<16, 2, 1, EPI, 4>(g, s); break;  // 256 x 128 tiles
   }
 }
 }  // namespace
@@ -705,6 +722,17 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
   if (splits < 1 || epi == EPI_STATS) splits = 1;   // tile statistics need whole dot products
   p.splits = splits;
   p.part_bytes = splits > 1 ? (size_t)splits * M * p.Nw * sizeof(float) : 0;
+  // Wide outputs at 128- and 256-row tiles with no K split take seven compute waves and
+  // 224-column tiles: two waves per SIMD overlap one's LDS fragment reads with the other's
+  // MFMAs, and a workgroup re-reads its activations for 224 columns instead of 128
+  // (measured on the LM head, V 151936, at 96 / 128 / 200 / 256 rows: 176 / 183 / 249 /
+  // 258 us against 187 / 196 / 271 / 280 us with four).
+  p.cw = 4;
+  if (p.shape != 0 && splits == 1 && p.n_tiles >= target &&
+      (epi == EPI_STORE_F32 || epi == EPI_ADD_F32 || epi == EPI_STORE_ACT)) {
+    p.cw = 7;
+    p.n_tiles = (p.Nw + 7 * cols / 4 - 1) / (7 * cols / 4);
+  }
   return p;
 }
 
@@ -742,11 +770,11 @@ int launch_gemm(const char *name, int dtype, int epi, int M, int N, int K, const
     {
       TraceScope ts(name, s);
       switch (epi) {
-        case EPI_STORE_F32: launch_stream_shape<EPI_STORE_F32>(p.shape, g, s); break;
-        case EPI_ADD_F32: launch_stream_shape<EPI_ADD_F32>(p.shape, g, s); break;
-        case EPI_STORE_ACT: launch_stream_shape<EPI_STORE_ACT>(p.shape, g, s); break;
-        case EPI_SWIGLU: launch_stream_shape<EPI_SWIGLU>(p.shape, g, s); break;
-        case EPI_STATS: launch_stream_shape<EPI_STATS>(p.shape, g, s); break;
+        case EPI_STORE_F32: launch_stream_shape<EPI_STORE_F32>(p.shape, p.cw, g, s); break;
+        case EPI_ADD_F32: launch_stream_shape<EPI_ADD_F32>(p.shape, p.cw, g, s); break;
+        case EPI_STORE_ACT: launch_stream_shape<EPI_STORE_ACT>(p.shape, p.cw, g, s); break;
+        case EPI_SWIGLU: launch_stream_shape<EPI_SWIGLU>(p.shape, p.cw, g, s); break;
+        case EPI_STATS: launch_stream_shape<EPI_STATS>(p.shape, p.cw, g, s); break;
       }
     }
     if (p.splits > 1 && defer_reduce) return p.splits;

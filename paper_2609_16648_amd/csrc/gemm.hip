@@ -9,8 +9,9 @@
 //    from HBM into registers, through a prefetch ring several k-steps deep;
 //    W never touches LDS.
 //  * Activations (small, L2-resident) are staged in LDS in 16 or 32 KiB
-//    chunks, three deep, by a fifth wave of direct-to-LDS loads, one barrier
-//    per chunk, shared by the 4 compute waves.
+//    chunks, three deep, by one extra wave of direct-to-LDS loads, one barrier
+//    per chunk, shared by the 4 compute waves (7 for wide outputs, two per
+//    SIMD, so that one wave's LDS reads overlap another's MFMAs).
 //  * Small N is split along K (deterministic two-pass reduction: float32
 //    partials, then a reduce kernel that sums the splits in order and applies
 //    the epilogue) so that a launch fills the 256 CUs.

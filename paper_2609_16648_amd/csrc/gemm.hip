@@ -23,6 +23,7 @@
 //    same wave, so silu(gate) * up is formed in registers).
 // float32 path: a plain LDS-tiled FMA kernel on row-major weights.
 #include <atomic>
+#include <type_traits>
 
 #include "common.h"
 #include "forward.h"
@@ -514,45 +515,53 @@ __global__ __launch_bounds__(256) void lm_strips_kernel(GemmL g) {
       __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)(dst + u * 512), 16, 0, 0);
     }
   };
-  uint4 rw[kLmRing][kLmStrips];
-  auto load_w_step = [&](int slot, int step) {
+  // The K loop for a wave that streams NS strips: kLmStrips where its range has that many,
+  // else kLmStrips - 1 (the last strip of a shorter range again where it has fewer), so
+  // that a CU's four waves load 37-38 strips per k-step rather than 40.  The load order
+  // fixes the waits: A(0), the weights of steps 0 .. kLmRing - 2; then per chunk c: A(c + 1),
+  // and per step s the weights of step s + kLmRing - 1.
+  auto k_loop = [&](auto ns_tag) {
+    constexpr int NS = decltype(ns_tag)::value;
+    uint4 rw[kLmRing][NS];
+    auto load_w_step = [&](int slot, int step) {
 #pragma unroll
-    for (int t = 0; t < kLmStrips; ++t) rw[slot][t] = load_w<true>(wb[t] + (long)step * kWStep);
-  };
-  // The load order fixes the waits: A(0), the weights of steps 0 .. kLmRing - 2; then per
-  // chunk c: A(c + 1), and per step s the weights of step s + kLmRing - 1.
-  __builtin_amdgcn_sched_barrier(0);
-  issue_a(0);
-#pragma unroll
-  for (int d = 0; d < kLmRing - 1; ++d) load_w_step(d, d);
-  __builtin_amdgcn_sched_barrier(0);
-  __builtin_amdgcn_s_waitcnt(waitcnt_vm((kLmRing - 1) * kLmStrips));   // A(0) landed
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_sched_barrier(0);
-  for (int c = 0; c < nchunks; ++c) {
-#pragma unroll
-    for (int d = 0; d < kLmChunk; ++d) {
-      const int s = kLmChunk * c + d;
-      __builtin_amdgcn_sched_barrier(0);
-      if (d == 0) issue_a(c + 1);   // into the buffer of chunk c - 1, released by the last barrier
-      load_w_step((d + kLmRing - 1) % kLmRing, min(s + kLmRing - 1, ksteps - 1));
-      __builtin_amdgcn_sched_barrier(0);
-      bf16x8_t af[4];
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-        af[a] = as_bf16x8(*reinterpret_cast<const uint4 *>(&As[c % 2][(d * 4 + a) * 512 + lane * 8]));
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int t = 0; t < kLmStrips; ++t)
-          acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], as_bf16x8(rw[d % kLmRing][t]), acc[a][t], 0, 0, 0);
-    }
-    // A(c + 1) landed: issued after it, the weights of this chunk's kLmChunk steps
+      for (int t = 0; t < NS; ++t) rw[slot][t] = load_w<true>(wb[t] + (long)step * kWStep);
+    };
     __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm(kLmChunk * kLmStrips));
+    issue_a(0);
+#pragma unroll
+    for (int d = 0; d < kLmRing - 1; ++d) load_w_step(d, d);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((kLmRing - 1) * NS));   // A(0) landed
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-  }
+    for (int c = 0; c < nchunks; ++c) {
+#pragma unroll
+      for (int d = 0; d < kLmChunk; ++d) {
+        const int s = kLmChunk * c + d;
+        __builtin_amdgcn_sched_barrier(0);
+        if (d == 0) issue_a(c + 1);   // into the buffer of chunk c - 1, released by the last barrier
+        load_w_step((d + kLmRing - 1) % kLmRing, min(s + kLmRing - 1, ksteps - 1));
+        __builtin_amdgcn_sched_barrier(0);
+        bf16x8_t af[4];
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+          af[a] = as_bf16x8(*reinterpret_cast<const uint4 *>(&As[c % 2][(d * 4 + a) * 512 + lane * 8]));
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+          for (int t = 0; t < NS; ++t)
+            acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], as_bf16x8(rw[d % kLmRing][t]), acc[a][t], 0, 0, 0);
+      }
+      // A(c + 1) landed: issued after it, the weights of this chunk's kLmChunk steps
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(kLmChunk * NS));
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  if (n == kLmStrips) k_loop(std::integral_constant<int, kLmStrips>{});
+  else k_loop(std::integral_constant<int, kLmStrips - 1>{});
   __builtin_amdgcn_s_waitcnt(kVmcnt0);   // the clamped re-reads past the end, before the waves leave
   if (!active) return;
 

@@ -131,6 +131,22 @@ def test_qwen_layer_bf16_forward_mid_batch(qwen_layer):
     assert rel_err(logits, ref_c) < 1e-2 and rel_err(hidden, ref_hc) < 1e-2
 
 
+def test_qwen_layer_bf16_forward_k7_block(qwen_layer):
+    # a k = 7 block of the 64 sequences: M = 512 verify rows, which take 256 x 224 tiles on the
+    # SwiGLU projection (385..768 rows) and two 256-row M tiles of 224 columns on the LM head
+    need_gpu()
+    wl, shape, W, lens, caches, _ = qwen_layer
+    B, k = wl.batch, 7
+    tokens = synth.token_ids(B * (k + 1), shape.vocab, 1, "k7-block").reshape(B, k + 1)
+    model = gm.DeviceModel(shape, W)
+    cache = device_cache(shape, caches, lens, k + 1)
+    logits, hidden = _gpu_forward(model, cache, tokens)
+    ref_c, ref_hc, _ = oracle.verify_forward(shape, W, caches, tokens, lens, CONTRACT)
+    print("[forward qwen3 layer bf16 k=7] logits rel err vs contract %.3e, hidden %.3e"
+          % (rel_err(logits, ref_c), rel_err(hidden, ref_hc)), flush=True)
+    assert rel_err(logits, ref_c) < 1e-2 and rel_err(hidden, ref_hc) < 1e-2
+
+
 def test_qwen_layer_bf16_block_is_causal(qwen_layer):
     # Changing the last draft d_k leaves every earlier block row's logits and hidden
     # bit-identical (a block position sees only the positions before it, Sec. 3.1's

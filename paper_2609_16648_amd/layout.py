@@ -71,7 +71,7 @@ def tile_weight(w: np.ndarray) -> np.ndarray:
     ((s // 8) * (in / 32) + c // 32) * 8 + s % 8.  Returns a flat array."""
     n, k = w.shape
     if n % 128 or k % 32:
-        raise ValueError("tiled weights need out % 128 == 0 and in % 32 == 0, got %s" % (w.shape,))
+        raise ValueError(f"tiled weights need out % 128 == 0 and in % 32 == 0, got {w.shape}")
     # [group][strip in group][row][kstep][col block][col] -> [group][kstep][strip][col block][row][col]
     return np.ascontiguousarray(w.reshape(n // 128, 8, 16, k // 32, 4, 8).transpose(0, 3, 1, 4, 2, 5)).reshape(-1)
 

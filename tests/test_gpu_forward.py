@@ -292,3 +292,26 @@ def test_target_stats_handoff_qwen_layer(qwen_layer, B):
                        gm.Workspace(), temperature=T)
         torch.cuda.synchronize()
         assert (n_pass.cpu().numpy() == n).mean() >= 0.98
+
+
+def test_strip_ranges_with_idle_waves():
+    # A bf16 model whose vocabulary is 10248 strips of 16 ids (163968 ids): more strips than
+    # 1024 waves hold at ten each, so the LM head at M = 64 rows runs 1025 strip ranges (1023 of
+    # ten strips, two of nine) in 257 workgroups, the last of which holds three waves with no
+    # range (they stage their share of the activations and meet the barriers, then leave).
+    # Both K loops (ten and nine strips) and the idle waves run; logits against the oracle,
+    # statistics against their definition.
+    need_gpu()
+    shape = synth.ModelShape(1, 256, 2, 2, 128, 512, 10248 * 16, dtype="bf16")
+    W = synth.model_weights(shape)
+    B, k = 16, 3
+    lens = 96 + 16 * np.arange(B)
+    caches = synth_caches(shape, lens, shape.n_layers)
+    tokens = synth.token_ids(B * (k + 1), shape.vocab, 1, "idle-waves").reshape(B, k + 1)
+    ref, _, _ = oracle.verify_forward(shape, W, caches, tokens, lens, CONTRACT)
+    model = gm.DeviceModel(shape, W)
+    logits, stats = _forward_with_stats(model, device_cache(shape, caches, lens, k + 1), tokens, 1.0)
+    err = rel_err(logits.cpu().numpy(), ref)
+    print("[strip ranges, 10248 strips] logits rel err vs contract %.3e" % err, flush=True)
+    assert err < 1e-2
+    _check_stats("strip ranges, 10248 strips", stats, logits, 1.0)

@@ -41,10 +41,13 @@ What it computes, and where the paper states it:
 * ``mtp``    -- the recurrent MTP draft head (Sec. 2.2; App. "Models and Draft
   Heads"; Eqs. tf-restart and tf-restart-kv), and the draft-path
   reconstruction that re-runs recorded chains with the recorded drafts as
-  inputs (App. "Draft-Path Reconstruction").  Pinned by the pass-through
-  special cases and by the reconstruction reproducing the drafting's own
-  distributions; beyond them the head's composition is described only in
-  prose, so its parity is "parity unpinned" past those cases.
+  inputs (App. "Draft-Path Reconstruction").  Pinned by pass-through special
+  cases (concat order, shared embedding and head, final norm, the chain's
+  feed), by two special cases in which the decoder layer has a closed form that
+  reads the head's cache (uniform attention; scores fixed by RoPE's
+  relative-position property), which fix the (hidden, token) pair and the
+  rotary position of every extend and chain entry, and by the reconstruction
+  reproducing the drafting's own distributions.
 * ``mixing`` -- the draft construction of the top-1 mixing workloads (an input
   recipe, not part of the method).
 

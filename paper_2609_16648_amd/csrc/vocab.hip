@@ -37,7 +37,7 @@ __device__ __forceinline__ bool in_nucleus(float z, int x, uint32_t key, int idt
 // ------------------------------------------------------------------ 1. row statistics
 // submax (may be null): [row][n_chunks * 64] maxima of the raw logits over runs of
 // kRecSub = 256 ids (one wave's float4 load), for the cycle record's selection.
-__global__ __launch_bounds__(kStatThreads) void row_stats_kernel(const float *__restrict__ logits,
+__global__ __launch_bounds__(kStatThreads) __attribute__((amdgpu_waves_per_eu(5, 8))) void row_stats_kernel(const float *__restrict__ logits,
                                                                  long row_stride, int V, float inv_t,
                                                                  int n_chunks, RowStat *__restrict__ out,
                                                                  float *__restrict__ submax) {
@@ -50,22 +50,32 @@ __global__ __launch_bounds__(kStatThreads) void row_stats_kernel(const float *__
   const int hi = min(V, lo + kStatChunk);
   const bool vec = ((V & 3) == 0) && ((row_stride & 3) == 0);
 
-  float v[kStatVec][4], rmax[kStatVec];
+  // The raw logits stay in registers and z / T is formed where it is used (the same
+  // product each time).  With no second copy, no per-load maxima kept and straight-line
+  // loads for whole chunks the kernel fits five waves per SIMD (87 registers), so the
+  // 2560 workgroups of 256 rows of the 151936-id vocabulary run in two full rounds
+  // rather than two and a half.
+  float f[kStatVec][4];
+  if (vec && hi - lo == kStatChunk) {   // a whole chunk (uniform over the workgroup): plain vector loads
 #pragma unroll
-  for (int j = 0; j < kStatVec; ++j) {
-    const int e = lo + 4 * (tid + kStatThreads * j);
-    float f[4];
-    if (vec && e + 3 < hi) {
-      const float4 g = __builtin_bit_cast(float4, load_nt(row + e));   // each logit is read once here
-      f[0] = g.x; f[1] = g.y; f[2] = g.z; f[3] = g.w;
-    } else {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) f[q] = (e + q < hi) ? row[e + q] : -INFINITY;
+    for (int j = 0; j < kStatVec; ++j) {
+      const float4 g = __builtin_bit_cast(float4, load_nt(row + lo + 4 * (tid + kStatThreads * j)));   // read once
+      f[j][0] = g.x; f[j][1] = g.y; f[j][2] = g.z; f[j][3] = g.w;
     }
+  } else {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) v[j][q] = f[q] * inv_t;
-    rmax[j] = fmaxf(fmaxf(f[0], f[1]), fmaxf(f[2], f[3]));
+    for (int j = 0; j < kStatVec; ++j) {
+      const int e = lo + 4 * (tid + kStatThreads * j);
+      if (vec && e + 3 < hi) {
+        const float4 g = __builtin_bit_cast(float4, load_nt(row + e));
+        f[j][0] = g.x; f[j][1] = g.y; f[j][2] = g.z; f[j][3] = g.w;
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) f[j][q] = (e + q < hi) ? row[e + q] : -INFINITY;
+      }
+    }
   }
+  auto rmax = [&](int j) { return fmaxf(fmaxf(f[j][0], f[j][1]), fmaxf(f[j][2], f[j][3])); };
   if (submax) {
     // maxima of the 16 runs of 256 ids this wave loaded (run j: load j of the wave), by a
     // reduce-scatter over the lanes: after the rounds with masks 32..4 lane L holds run
@@ -75,7 +85,7 @@ __global__ __launch_bounds__(kStatThreads) void row_stats_kernel(const float *__
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       const bool hi_half = lane & 32;
-      const float keep = hi_half ? rmax[8 + q] : rmax[q], send = hi_half ? rmax[q] : rmax[8 + q];
+      const float keep = hi_half ? rmax(8 + q) : rmax(q), send = hi_half ? rmax(q) : rmax(8 + q);
       m8[q] = fmaxf(keep, __shfl_xor(send, 32, kWave));
     }
 #pragma unroll
@@ -103,19 +113,24 @@ __global__ __launch_bounds__(kStatThreads) void row_stats_kernel(const float *__
       submax[(long)blockIdx.x * n_chunks * 64 + (long)c * 64 + 4 * j + w] = m1;
     }
   }
-  // max, then the lowest id attaining it, as two branch-free wave reductions
+  // max, then the lowest id attaining it, as two branch-free wave reductions.  Each
+  // pass takes an opaque copy of 1/T, so the compiler recomputes z / T there instead
+  // of keeping all 64 products live beside the logits.
+  auto opaque_inv_t = [&]() { float t = inv_t; asm volatile("" : "+v"(t)); return t; };
+  const float t1 = opaque_inv_t();
   float m = -INFINITY;
 #pragma unroll
   for (int j = 0; j < kStatVec; ++j)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) m = fmaxf(m, v[j][q]);
+    for (int q = 0; q < 4; ++q) m = fmaxf(m, f[j][q] * t1);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
   int am = 0x7fffffff;
+  const float t2 = opaque_inv_t();
 #pragma unroll
   for (int j = kStatVec - 1; j >= 0; --j)
 #pragma unroll
-    for (int q = 3; q >= 0; --q) am = v[j][q] == m ? lo + 4 * (tid + kStatThreads * j) + q : am;
+    for (int q = 3; q >= 0; --q) am = f[j][q] * t2 == m ? lo + 4 * (tid + kStatThreads * j) + q : am;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) am = min(am, __shfl_xor(am, o, kWave));
   const int lane = tid & 63, wid = tid >> 6;
@@ -128,10 +143,11 @@ __global__ __launch_bounds__(kStatThreads) void row_stats_kernel(const float *__
     if (sm_max[w] > m || (sm_max[w] == m && sm_arg[w] < am)) { m = sm_max[w]; am = sm_arg[w]; }
 
   double s = 0.0;
+  const float t3 = opaque_inv_t();
 #pragma unroll
   for (int j = 0; j < kStatVec; ++j)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) s += (double)expf(v[j][q] - m);
+    for (int q = 0; q < 4; ++q) s += (double)expf(f[j][q] * t3 - m);
   s = wave_sum(s);
   if (lane == 0) sm_sum[wid] = s;
   __syncthreads();

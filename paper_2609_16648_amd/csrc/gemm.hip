@@ -10,8 +10,8 @@
 //    W never touches LDS.
 //  * Activations (small, L2-resident) are staged in LDS in 16 or 32 KiB
 //    chunks, three deep, by one extra wave of direct-to-LDS loads, one barrier
-//    per chunk, shared by the 4 compute waves (7 for wide outputs, two per
-//    SIMD, so that one wave's LDS reads overlap another's MFMAs).
+//    per chunk, shared by the 4 compute waves (5 or 7 for wide outputs, up to
+//    two per SIMD, so that one wave's LDS reads overlap another's MFMAs).
 //  * Small N is split along K (deterministic two-pass reduction: float32
 //    partials, then a reduce kernel that sums the splits in order and applies
 //    the epilogue) so that a launch fills the 256 CUs.
@@ -675,9 +675,13 @@ void launch_stream(const GemmS &g, hipStream_t s) {
 
 template <int EPI>
 void launch_stream_shape(int shape, int cw, const GemmS &g, hipStream_t s) {
-  // four compute waves: 128-column tiles, one tile-statistics block each; seven (no
-  // statistics): 224-column tiles
+  // four compute waves: 128-column tiles, one tile-statistics block each; five or seven
+  // (no statistics): 160- or 224-column tiles
   if constexpr (EPI != EPI_STATS) {
+    if (cw == 5) {
+      launch_stream<8, 2, 1, EPI, 5>(g, s);                   // 128 x 160 tiles
+      return;
+    }
     if (cw == 7) {
       if (shape == 1) launch_stream<8, 2, 1, EPI, 7>(g, s);   // 128 x 224 tiles
       else launch_stream<16, 2, 1, EPI, 7>(g, s);             // 256 x 224 tiles
@@ -752,7 +756,10 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
   // shapes measured fastest on the Qwen3-4B gate/up (19456 weight rows, K 2560), against
   // the rules above: 96 / 128 rows, 128-row tiles: 31 / 34 us against 37 / 40; 256 rows,
   // 128 x 224 tiles: 43 against 53; 512 rows, 256 x 224: 69 against 83; 1024 rows,
-  // 128 x 224: 127 against 138 (160 and 192 rows: 38-39 us either way)
+  // 128 x 224: 127 against 138 (160 and 192 rows: 38-39 us either way).  With two
+  // 128-row M tiles, 160-column tiles (five compute waves) where they still fit one
+  // workgroup per CU: each CU streams fewer weight bytes per activation read (256 rows,
+  // 244 workgroups: 43.9 us against 46.9 with 128 x 224 and 45.1 with 128 x 192).
   if (epi == EPI_SWIGLU && M > 64 && p.n_tiles >= 128 && p.n_tiles < target) {
     const bool tall = M > 384 && M <= 768;
     p.shape = tall ? 2 : 1;
@@ -762,6 +769,11 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
     if (M > 128) {
       p.cw = 7;
       p.n_tiles = (p.Nw + 7 * cols / 4 - 1) / (7 * cols / 4);
+      const int n5 = (p.Nw + 5 * cols / 4 - 1) / (5 * cols / 4);
+      if (p.m_tiles == 2 && 2 * n5 <= target) {
+        p.cw = 5;
+        p.n_tiles = n5;
+      }
     }
   }
   return p;

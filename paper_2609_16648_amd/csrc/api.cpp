@@ -246,7 +246,9 @@ gm_status spec_accept_impl(int B, int k, int V, int mode, float temperature, flo
                        draft_tokens, u_accept, u_final, n_accept, out_tokens, sel, s);
   if (rec)
     launch_record_topk(B, k, V, inv_t, record->topk, target_logits, tstat, submax, record->logp, record->ids, s);
-  if (mode == GM_SAMPLE) launch_residual_draw("accept_residual_chunk", "accept_residual_scan", B, V, inv_t, sel, (double *)(w + p.wsum), (double *)(w + p.psum), s);
+  if (mode == GM_SAMPLE)
+    launch_residual_draw("accept_residual_chunk", "accept_residual_scan", B, V, inv_t, sel, (double *)(w + p.wsum),
+                         (double *)(w + p.psum), top_p_on, s);
   return check_launch("gm_spec_accept");
 }
 }  // namespace gm

@@ -205,7 +205,7 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
                      (unsigned long long *)(ws + p.nucpart), s);
       launch_nucleus_select(B, zl, (long)k * V, nuc, ns, u_draft + j, k, drafts + j, k, sel, s);
       launch_residual_draw("draft_nucleus_chunk", "draft_nucleus_scan", B, V, inv_t, sel, (double *)(ws + p.wsum),
-                           (double *)(ws + p.psum), s);
+                           (double *)(ws + p.psum), true, s);
     } else {
       launch_tile_draw(B, V, mode, inv_t, zl, (long)k * V, geo, tiles, u_draft ? u_draft + j : nullptr, k, drafts + j,
                        k, draft_stats ? draft_stats + j : nullptr, k, s);

@@ -123,8 +123,9 @@ void launch_nucleus(const char *name, int n_rows, int V, double inv_td, double t
 // with the uniform u[b * u_stride], into dst[b * dst_stride]
 void launch_nucleus_select(int B, const float *logits, long row_stride, const NucRow *nuc, int nuc_stride,
                            const float *u, int u_stride, int32_t *dst, int dst_stride, RowSel *sel, hipStream_t s);
-void launch_residual_draw(const char *chunk_name, const char *scan_name, int B, int V, float inv_t, const RowSel *sel, double *wsum,
-                          double *psum, hipStream_t s);
+// nucleus false: every row of sel keeps every id (top-p 1), and the kernels skip the nucleus tests
+void launch_residual_draw(const char *chunk_name, const char *scan_name, int B, int V, float inv_t, const RowSel *sel,
+                          double *wsum, double *psum, bool nucleus, hipStream_t s);
 
 // ---------------------------------------------------------------- KV index
 void launch_kv_commit(int B, int k, int page_size, int max_pages, const int32_t *block_table,

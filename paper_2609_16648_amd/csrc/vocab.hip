@@ -990,8 +990,24 @@ __device__ __forceinline__ void load_run(const float *row, int x0, int V, float 
   }
 }
 
-// the kScanPer draw weights of one thread's run (max(0, p - q), or p alone) and their
-// p; under top-p, ids outside a row's nucleus weigh 0 in it
+// the draw weight of id x (max(0, p - q), or p alone) and its p; under top-p, ids outside
+// a row's nucleus weigh 0 in it.  NUC false (top-p 1, every row keeps every id): the same
+// weights without the nucleus tests, which are about a quarter of the pass's ALU work.
+template <bool NUC>
+__device__ __forceinline__ void id_weight(const RowSel &s, int x, int V, float zp, float zq, bool with_q, float inv_t,
+                                          float mp, float mq, double isp, double isq, double &w, double &px) {
+  const bool kp = x < V && (!NUC || in_nucleus(zp, x, s.pkey, s.pid));
+  px = kp ? (double)expf(zp * inv_t - mp) * isp : 0.0;
+  w = px;
+  if (with_q) {
+    const bool kq = x < V && (!NUC || in_nucleus(zq, x, s.qkey, s.qid));
+    const double qx = kq ? (double)expf(zq * inv_t - mq) * isq : 0.0;
+    w = fmax(px - qx, 0.0);
+  }
+}
+
+// the kScanPer draw weights of one thread's run and the sum of their p
+template <bool NUC>
 __device__ __forceinline__ void run_weights(const RowSel &s, int x0, int V, float inv_t, bool use_p, double isp,
                                             double isq, double (&w)[kScanPer], double &psum) {
   float rp[kScanPer], rq[kScanPer];
@@ -1000,18 +1016,32 @@ __device__ __forceinline__ void run_weights(const RowSel &s, int x0, int V, floa
   if (with_q) load_run(s.q_row, x0, V, rq);
   const float mp = (float)s.mp, mq = (float)s.mq;
   psum = 0.0;
+  double px;
 #pragma unroll
   for (int j = 0; j < kScanPer; ++j) {
-    const int x = x0 + j;
-    const bool kp = x < V && in_nucleus(rp[j], x, s.pkey, s.pid);
-    const double px = kp ? (double)expf(rp[j] * inv_t - mp) * isp : 0.0;
+    id_weight<NUC>(s, x0 + j, V, rp[j], rq[j], with_q, inv_t, mp, mq, isp, isq, w[j], px);
     psum += px;
-    w[j] = px;
-    if (with_q) {
-      const bool kq = x < V && in_nucleus(rq[j], x, s.qkey, s.qid);
-      const double qx = kq ? (double)expf(rq[j] * inv_t - mq) * isq : 0.0;
-      w[j] = fmax(px - qx, 0.0);
-    }
+  }
+}
+
+// the same run summed as it is formed: the sums the scan kernel takes over run_weights'
+// weights, in the same order, without holding the kScanPer weights
+template <bool NUC>
+__device__ __forceinline__ void run_sums(const RowSel &s, int x0, int V, float inv_t, double isp, double isq,
+                                         double &wsum, double &psum) {
+  float rp[kScanPer], rq[kScanPer];
+  load_run(s.p_row, x0, V, rp);
+  const bool with_q = s.q_row != nullptr;
+  if (with_q) load_run(s.q_row, x0, V, rq);
+  const float mp = (float)s.mp, mq = (float)s.mq;
+  psum = 0.0;
+  wsum = 0.0;
+  double w, px;
+#pragma unroll
+  for (int j = 0; j < kScanPer; ++j) {
+    id_weight<NUC>(s, x0 + j, V, rp[j], rq[j], with_q, inv_t, mp, mq, isp, isq, w, px);
+    psum += px;
+    wsum += w;
   }
 }
 
@@ -1033,6 +1063,7 @@ __device__ __forceinline__ double block_incl_scan(double v, double *wsum /* >= 4
 // per-thread sums over kScanPer consecutive ids, then a block-wide inclusive scan
 // over the threads (the same code in both kernels, so a chunk's mass is exactly
 // the last running sum of the scan inside it)
+template <bool NUC>
 __global__ __launch_bounds__(kScanThreads) void residual_chunk_kernel(int V, float inv_t,
                                                                       const RowSel *__restrict__ sel,
                                                                       int nch, double *__restrict__ wsum,
@@ -1043,11 +1074,8 @@ __global__ __launch_bounds__(kScanThreads) void residual_chunk_kernel(int V, flo
   if (!s.active) return;
   const int x0 = c * kScanChunk + tid * kScanPer;
   const double isp = 1.0 / s.sp, isq = 1.0 / s.sq;
-  double wv[kScanPer], p = 0.0;
-  run_weights(s, x0, V, inv_t, false, isp, isq, wv, p);
-  double w = 0.0;
-#pragma unroll
-  for (int j = 0; j < kScanPer; ++j) w += wv[j];
+  double w, p;
+  run_sums<NUC>(s, x0, V, inv_t, isp, isq, w, p);
   const double tw = block_incl_scan(w, sw);
   const double tp = block_incl_scan(p, sp);
   if (tid == kScanThreads - 1) {
@@ -1056,6 +1084,7 @@ __global__ __launch_bounds__(kScanThreads) void residual_chunk_kernel(int V, flo
   }
 }
 
+template <bool NUC>
 __global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, float inv_t,
                                                                      const RowSel *__restrict__ sel, int nch,
                                                                      const double *__restrict__ wsum,
@@ -1110,7 +1139,7 @@ __global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, floa
   const double isp = 1.0 / s.sp, isq = 1.0 / s.sq;
   const int x0 = cs * kScanChunk + tid * kScanPer;
   double wv[kScanPer], pdummy;
-  run_weights(s, x0, V, inv_t, use_p, isp, isq, wv, pdummy);
+  run_weights<NUC>(s, x0, V, inv_t, use_p, isp, isq, wv, pdummy);
   double w = 0.0;
 #pragma unroll
   for (int j = 0; j < kScanPer; ++j) w += wv[j];
@@ -1142,18 +1171,26 @@ __global__ __launch_bounds__(kScanThreads) void residual_scan_kernel(int V, floa
   }
 }
 
-void launch_residual_draw(const char *chunk_name, const char *scan_name, int B, int V, float inv_t, const RowSel *sel, double *wsum, double *psum,
-                          hipStream_t s) {
+void launch_residual_draw(const char *chunk_name, const char *scan_name, int B, int V, float inv_t, const RowSel *sel,
+                          double *wsum, double *psum, bool nucleus, hipStream_t s) {
   const int nch = scan_chunks(V);
   {
     TraceScope ts(chunk_name, s);
-    hipLaunchKernelGGL(residual_chunk_kernel, dim3(B, nch), dim3(kScanThreads), 0, s, V, inv_t, sel, nch,
-                       wsum, psum);
+    if (nucleus)
+      hipLaunchKernelGGL(residual_chunk_kernel<true>, dim3(B, nch), dim3(kScanThreads), 0, s, V, inv_t, sel, nch,
+                         wsum, psum);
+    else
+      hipLaunchKernelGGL(residual_chunk_kernel<false>, dim3(B, nch), dim3(kScanThreads), 0, s, V, inv_t, sel, nch,
+                         wsum, psum);
   }
   {
     TraceScope ts(scan_name, s);
-    hipLaunchKernelGGL(residual_scan_kernel, dim3(B), dim3(kScanThreads), 2 * nch * sizeof(double), s, V, inv_t,
-                       sel, nch, wsum, psum);
+    if (nucleus)
+      hipLaunchKernelGGL(residual_scan_kernel<true>, dim3(B), dim3(kScanThreads), 2 * nch * sizeof(double), s, V,
+                         inv_t, sel, nch, wsum, psum);
+    else
+      hipLaunchKernelGGL(residual_scan_kernel<false>, dim3(B), dim3(kScanThreads), 2 * nch * sizeof(double), s, V,
+                         inv_t, sel, nch, wsum, psum);
   }
 }
 

@@ -207,8 +207,11 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
       launch_residual_draw("draft_nucleus_chunk", "draft_nucleus_scan", B, V, inv_t, sel, (double *)(ws + p.wsum),
                            (double *)(ws + p.psum), true, s);
     } else {
+      // below the last depth the draw also builds the next chain step's input row (the
+      // drawn id with the layer output x1), in place of a separate input launch
+      const DrawNextInput next{dt, H, cfg.rms_eps, x1, shared.embed, mtp.norm_h, mtp.norm_e, u, dev_err};
       launch_tile_draw(B, V, mode, inv_t, zl, (long)k * V, geo, tiles, u_draft ? u_draft + j : nullptr, k, drafts + j,
-                       k, draft_stats ? draft_stats + j : nullptr, k, s);
+                       k, draft_stats ? draft_stats + j : nullptr, k, s, j + 1 < k ? &next : nullptr);
     }
   };
 
@@ -237,8 +240,9 @@ void run_mtp_draft(const gm_model_config &cfg, const gm_mtp_weights &mtp, const 
 
   // ---- chain: step j feeds (g_{j-1}, d_{j-1}) at slot boundary + j - 1
   for (int j = 1; j < k; ++j) {
-    launch_mtp_input(dt, B, H, V, cfg.rms_eps, xg, drafts + (j - 1), k, shared.embed, mtp.norm_h, mtp.norm_e, u,
-                     dev_err, s);
+    if (top_p < 1.0)   // (at top-p 1 the draw of depth j - 1 has built this input)
+      launch_mtp_input(dt, B, H, V, cfg.rms_eps, xg, drafts + (j - 1), k, shared.embed, mtp.norm_h, mtp.norm_e, u,
+                       dev_err, s);
     gemm_norm("mtp_gemm_proj", dt, EPI_STORE_F32, B, H, 2 * H, u, 2 * H, mtp.w_proj, xg, part, L.attn_norm, eps, nbuf,
               s);
     sq = launch_gemm("mtp_gemm_qkv", dt, EPI_STORE_F32, B, qw, H, nbuf, H, L.w_qkv, qkv, qw, part, s, nullptr, 1.f,

@@ -770,7 +770,7 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K) {
       p.cw = 7;
       p.n_tiles = (p.Nw + 7 * cols / 4 - 1) / (7 * cols / 4);
       const int n5 = (p.Nw + 5 * cols / 4 - 1) / (5 * cols / 4);
-      if (p.m_tiles == 2 && 2 * n5 <= target) {
+      if (p.shape == 1 && p.m_tiles == 2 && 2 * n5 <= target) {   // the five-wave tiles are 128 rows tall
         p.cw = 5;
         p.n_tiles = n5;
       }

@@ -88,9 +88,19 @@ void launch_tile_stats(const float *logits, long row_stride, int n_rows, int V, 
 // one draw per row from softmax(z / T) given its tile statistics: argmax (greedy) or the
 // inverse-CDF draw with u[b * u_stride]; writes dst[b * dst_stride]
 // row_out (may be null): the row's combined statistics at row_out[b * row_stride_out]
+// next (may be null): the same launch also writes the next chain step's MTP input row b
+// (mtp_input_row with h + b * H and the drawn id) into out + b * 2 * H
+struct DrawNextInput {
+  int dtype, H;
+  float eps;
+  const float *h;
+  const void *E, *norm_h, *norm_e;
+  void *out;
+  int32_t *dev_err;
+};
 void launch_tile_draw(int B, int V, int mode, float inv_t, const float *logits, long row_stride, TileGeom geo,
                       const RowStat *tiles, const float *u, int u_stride, int32_t *dst, int dst_stride,
-                      RowStat *row_out, int row_stride_out, hipStream_t s);
+                      RowStat *row_out, int row_stride_out, hipStream_t s, const DrawNextInput *next = nullptr);
 
 // submax (may be null): also the raw-logit maxima of every run of kRecSub ids, [row][stat_chunks(V) * 64]
 void launch_row_stats(const char *name, const float *logits, long row_stride, int n_rows, int V, float inv_t,

@@ -7,6 +7,7 @@
 // angle is off by ~2e-3 rad); outputs rounded once to the model dtype.
 #include "common.h"
 #include "forward.h"
+#include "mtp_row.h"
 
 namespace gm {
 
@@ -76,16 +77,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(int M, int H, float eps, c
   }
 }
 
-// four consecutive elements of a row (16-byte or 8-byte aligned) as float
-__device__ __forceinline__ float4 load4(const float *p, long i) { return *reinterpret_cast<const float4 *>(p + i); }
-__device__ __forceinline__ float4 load4(const bf16 *p, long i) {
-  const uint2 v = *reinterpret_cast<const uint2 *>(p + i);
-  return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u), __uint_as_float(v.y << 16),
-                     __uint_as_float(v.y & 0xffff0000u));
-}
-
-// MTP input row r: [RMSNorm(h_r) * norm_h, RMSNorm(E[tok_r]) * norm_e] (model dtype, 2H wide);
-// four channels per thread and step, both sums of squares reduced together
+// MTP input row r (mtp_input_row): one block of mtp_input_threads(H) threads per row
 template <typename T>
 __global__ __launch_bounds__(1024) void mtp_input_kernel(int H, int V, float eps, const float *__restrict__ h,
                                                          const int32_t *__restrict__ tok, int tok_stride,
@@ -94,47 +86,8 @@ __global__ __launch_bounds__(1024) void mtp_input_kernel(int H, int V, float eps
                                                          int32_t *dev_err) {
   __shared__ float2 red[16];
   const int r = blockIdx.x;
-  const int t = tok[(long)r * tok_stride];
-  T *o = out + (long)r * 2 * H;
-  if (t < 0 || t >= V) {     // -1 pads a row with no token
-    if (t >= V && threadIdx.x == 0) raise_dev_err(dev_err, GM_DEVERR_TOKEN);
-    for (int c = threadIdx.x; c < 2 * H; c += blockDim.x) Elem<T>::store(o, c, 0.f);
-    return;
-  }
-  const float *hr = h + (long)r * H;
-  const T *er = E + (long)t * H;
-  float sh = 0.f, se = 0.f;
-  for (int c = threadIdx.x * 4; c < H; c += blockDim.x * 4) {
-    const float4 a = load4(hr, c), e = load4(er, c);
-    sh += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
-    se += e.x * e.x + e.y * e.y + e.z * e.z + e.w * e.w;
-  }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    sh += __shfl_xor(sh, off, kWave);
-    se += __shfl_xor(se, off, kWave);
-  }
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  if (lane == 0) red[wid] = make_float2(sh, se);
-  __syncthreads();
-  sh = 0.f;
-  se = 0.f;
-  for (int i = 0; i < nw; ++i) {
-    sh += red[i].x;
-    se += red[i].y;
-  }
-  const float ih = 1.0f / sqrtf(sh / (float)H + eps), ie = 1.0f / sqrtf(se / (float)H + eps);
-  for (int c = threadIdx.x * 4; c < H; c += blockDim.x * 4) {
-    const float4 a = load4(hr, c), e = load4(er, c), wh = load4(nh, c), we = load4(ne, c);
-    Elem<T>::store(o, c, a.x * ih * wh.x);
-    Elem<T>::store(o, c + 1, a.y * ih * wh.y);
-    Elem<T>::store(o, c + 2, a.z * ih * wh.z);
-    Elem<T>::store(o, c + 3, a.w * ih * wh.w);
-    Elem<T>::store(o, H + c, e.x * ie * we.x);
-    Elem<T>::store(o, H + c + 1, e.y * ie * we.y);
-    Elem<T>::store(o, H + c + 2, e.z * ie * we.z);
-    Elem<T>::store(o, H + c + 3, e.w * ie * we.w);
-  }
+  mtp_input_row<T>(blockDim.x, H, V, eps, h + (long)r * H, tok[(long)r * tok_stride], E, nh, ne, out + (long)r * 2 * H,
+                   dev_err, red);
 }
 
 // One wave per (row, kRopeHeads consecutive heads): block (row, y) holds 4 such
@@ -372,8 +325,7 @@ void launch_mtp_input(int dtype, int M, int H, int V, float eps, const float *h,
                       hipStream_t s) {
   if (M <= 0) return;
   TraceScope ts("mtp_input", s);
-  int threads = ((H / 4 + 63) / 64) * 64;   // one four-channel group per thread when H <= 4096
-  if (threads > 1024) threads = 1024;
+  const int threads = mtp_input_threads(H);
   if (dtype == GM_BF16)
     hipLaunchKernelGGL(mtp_input_kernel<bf16>, dim3(M), dim3(threads), 0, s, H, V, eps, h, tok, tok_stride,
                        (const bf16 *)E, (const bf16 *)norm_h, (const bf16 *)norm_e, (bf16 *)out, dev_err);

@@ -20,6 +20,7 @@
 
 #include "common.h"
 #include "launch.h"
+#include "mtp_row.h"
 
 namespace gm {
 
@@ -1276,20 +1277,25 @@ void launch_tile_stats(const float *logits, long row_stride, int n_rows, int V, 
 // that tile's ids (at most kMaxDrawTileIds, kDrawRun consecutive ids per lane; the
 // same per-id terms exp(z / T - m_t) the tile sums were made of, scaled in float64)
 // for the first running sum above u * S.
-__global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float inv_t, const float *__restrict__ logits,
-                                                        long row_stride, const RowStat *__restrict__ tiles,
-                                                        TileGeom geo, const float *__restrict__ u, int u_stride,
-                                                        int32_t *__restrict__ dst, int dst_stride,
-                                                        RowStat *__restrict__ row_out, int row_stride_out) {
+// The draw of row b by one block of 256 threads; the drawn id goes to dst[b * dst_stride]
+// and to *tok_sh.  Waves other than the first may leave before the last phase.
+__device__ __forceinline__ void tile_draw_row(int V, int mode, float inv_t, const float *__restrict__ logits,
+                                              long row_stride, const RowStat *__restrict__ tiles, TileGeom geo,
+                                              const float *__restrict__ u, int u_stride, int32_t *__restrict__ dst,
+                                              int dst_stride, RowStat *__restrict__ row_out, int row_stride_out,
+                                              RowStat *st, int *tok_sh) {
   const int n_tiles = geo.tiles;
-  extern __shared__ uint4 st_raw[];   // [n_tiles] RowStat
-  RowStat *st = reinterpret_cast<RowStat *>(st_raw);
+  uint4 *st_raw = reinterpret_cast<uint4 *>(st);
   __shared__ float red_m[4];
   __shared__ int red_a[4];
   __shared__ double wsum[4];
   __shared__ double sh_base, sh_t;
   __shared__ int sh_tile, sh_hit, sh_last;
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  auto put = [&](int x) {
+    dst[(long)b * dst_stride] = x;
+    *tok_sh = x;
+  };
   const uint4 *src = reinterpret_cast<const uint4 *>(tiles + (long)b * n_tiles);
   float m = -INFINITY;
   int a = 0x7fffffff;
@@ -1325,7 +1331,7 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
   for (int w = 1; w < 4; ++w)
     if (red_m[w] > m || (red_m[w] == m && red_a[w] < a)) { m = red_m[w]; a = red_a[w]; }
   if (mode == GM_GREEDY && !row_out) {
-    if (tid == 0) dst[(long)b * dst_stride] = a;
+    if (tid == 0) put(a);
     return;
   }
   const double M = (double)m;
@@ -1342,7 +1348,7 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
     row_out[(long)b * row_stride_out] = o;
   }
   if (mode == GM_GREEDY) {
-    if (tid == 0) dst[(long)b * dst_stride] = a;
+    if (tid == 0) put(a);
     return;
   }
   const double target = (double)u[(long)b * u_stride] * S;
@@ -1400,18 +1406,66 @@ __global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float i
   // running sums grow along lanes: the first hit lane holds the drawn id
   const int first = hitm ? __ffsll((long long)hitm) - 1 : -1;
   const int lastnz = nz ? 63 - __clzll((long long)nz) : -1;
-  if (first >= 0 && lane == first) dst[(long)b * dst_stride] = x0 + pick;
-  if (first < 0 && lastnz >= 0 && lane == lastnz) dst[(long)b * dst_stride] = x0 + lastq;
-  if (first < 0 && lastnz < 0 && lane == 0) dst[(long)b * dst_stride] = a;
+  if (first >= 0 && lane == first) put(x0 + pick);
+  if (first < 0 && lastnz >= 0 && lane == lastnz) put(x0 + lastq);
+  if (first < 0 && lastnz < 0 && lane == 0) put(a);
+}
+
+// Optional second half of the draw launch: the next chain step's MTP input row
+// (mtp_input_row) from the id just drawn and the layer output h, in place of a
+// separate input launch.  out == nullptr: draw only.
+template <typename T>
+struct DrawInput {
+  int H, VT;
+  float eps;
+  const float *h;
+  const T *E, *nh, *ne;
+  T *out;
+  int32_t *dev_err;
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void tile_draw_kernel(int V, int mode, float inv_t, const float *__restrict__ logits,
+                                                        long row_stride, const RowStat *__restrict__ tiles,
+                                                        TileGeom geo, const float *__restrict__ u, int u_stride,
+                                                        int32_t *__restrict__ dst, int dst_stride,
+                                                        RowStat *__restrict__ row_out, int row_stride_out,
+                                                        DrawInput<T> in) {
+  extern __shared__ uint4 st_raw[];   // [n_tiles] RowStat
+  __shared__ int tok_sh;
+  __shared__ float2 red[16];
+  tile_draw_row(V, mode, inv_t, logits, row_stride, tiles, geo, u, u_stride, dst, dst_stride, row_out,
+                row_stride_out, reinterpret_cast<RowStat *>(st_raw), &tok_sh);
+  if (in.out == nullptr) return;
+  __syncthreads();
+  const int b = blockIdx.x;
+  mtp_input_row<T>(in.VT, in.H, V, in.eps, in.h + (long)b * in.H, tok_sh, in.E, in.nh, in.ne,
+                   in.out + (long)b * 2 * in.H, in.dev_err, red);
 }
 
 void launch_tile_draw(int B, int V, int mode, float inv_t, const float *logits, long row_stride, TileGeom geo,
                       const RowStat *tiles, const float *u, int u_stride, int32_t *dst, int dst_stride,
-                      RowStat *row_out, int row_stride_out, hipStream_t s) {
+                      RowStat *row_out, int row_stride_out, hipStream_t s, const DrawNextInput *next) {
   if (B <= 0) return;
   TraceScope ts("draft_draw", s);
-  hipLaunchKernelGGL(tile_draw_kernel, dim3(B), dim3(256), (size_t)geo.tiles * sizeof(RowStat), s, V, mode, inv_t,
-                     logits, row_stride, tiles, geo, u, u_stride, dst, dst_stride, row_out, row_stride_out);
+  const size_t lds = (size_t)geo.tiles * sizeof(RowStat);
+  if (next && next->dtype == GM_BF16) {
+    const DrawInput<bf16> in{next->H,       mtp_input_threads(next->H), next->eps, next->h,
+                             (const bf16 *)next->E, (const bf16 *)next->norm_h, (const bf16 *)next->norm_e,
+                             (bf16 *)next->out, next->dev_err};
+    hipLaunchKernelGGL(tile_draw_kernel<bf16>, dim3(B), dim3(256), lds, s, V, mode, inv_t, logits, row_stride, tiles,
+                       geo, u, u_stride, dst, dst_stride, row_out, row_stride_out, in);
+  } else if (next) {
+    const DrawInput<float> in{next->H,       mtp_input_threads(next->H), next->eps, next->h,
+                              (const float *)next->E, (const float *)next->norm_h, (const float *)next->norm_e,
+                              (float *)next->out, next->dev_err};
+    hipLaunchKernelGGL(tile_draw_kernel<float>, dim3(B), dim3(256), lds, s, V, mode, inv_t, logits, row_stride,
+                       tiles, geo, u, u_stride, dst, dst_stride, row_out, row_stride_out, in);
+  } else {
+    const DrawInput<float> none{};
+    hipLaunchKernelGGL(tile_draw_kernel<float>, dim3(B), dim3(256), lds, s, V, mode, inv_t, logits, row_stride,
+                       tiles, geo, u, u_stride, dst, dst_stride, row_out, row_stride_out, none);
+  }
 }
 
 }  // namespace gm

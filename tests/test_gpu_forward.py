@@ -294,6 +294,25 @@ def test_target_stats_handoff_qwen_layer(qwen_layer, B):
         assert (n_pass.cpu().numpy() == n).mean() >= 0.98
 
 
+def test_qwen_layer_bf16_forward_200_rows(qwen_layer):
+    # 50 of the sequences with k = 3: M = 200 verify rows, so the SwiGLU projection takes two
+    # 128-row M tiles (the second holds 72 rows) of 160 columns with five compute waves, the
+    # last column tile ragged (9728 features in 122 tiles of 80), and the LM head one 256-row
+    # tile of 224 columns
+    need_gpu()
+    wl, shape, W, lens, caches, tokens = qwen_layer
+    B = 50
+    lens_b = lens[:B]
+    caches_b = [(ks[:B], vs[:B]) for ks, vs in caches]
+    tok_b = tokens[:B]
+    model = gm.DeviceModel(shape, W)
+    logits, hidden = _gpu_forward(model, device_cache(shape, caches_b, lens_b, wl.k + 1), tok_b)
+    ref_c, ref_hc, _ = oracle.verify_forward(shape, W, caches_b, tok_b, lens_b, CONTRACT)
+    print("[forward qwen3 layer bf16, 200 rows] logits rel err vs contract %.3e, hidden %.3e"
+          % (rel_err(logits, ref_c), rel_err(hidden, ref_hc)), flush=True)
+    assert rel_err(logits, ref_c) < 1e-2 and rel_err(hidden, ref_hc) < 1e-2
+
+
 def test_strip_ranges_with_idle_waves():
     # A bf16 model whose vocabulary is 10248 strips of 16 ids (163968 ids): more strips than
     # 1024 waves hold at ten each, so the LM head at M = 64 rows runs 1025 strip ranges (1023 of

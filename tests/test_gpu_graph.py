@@ -6,7 +6,9 @@ commit -> draft once and replay it.  The graph is replayed several times, with
 the caches' lengths restored and the outputs cleared by eager work between the
 replays and an eager step run in between; every replay and every eager step
 must reproduce the first eager step bit for bit (the kernels are
-deterministic: fixed reduction orders, integer atomics only)."""
+deterministic: fixed reduction orders, integer atomics only).  The
+no-allocation accept, meant for such callers, is captured and replayed the
+same way."""
 import numpy as np
 import pytest
 import torch
@@ -98,3 +100,55 @@ def test_step_graph_replays_match_eager(top_p):
     assert int(err.item()) == 0
     print("[graph top_p=%.1f] 3 replays and 3 eager steps identical to the first eager step (n_accept %s)"
           % (top_p, ref[2].cpu().numpy().tolist()), flush=True)
+
+
+@pytest.mark.parametrize("top_p", [1.0, 0.7])
+def test_noalloc_accept_graph_replays_match_eager(top_p):
+    # the no-allocation accept is meant for callers under graph capture: captured once, its
+    # replays (with the workspace accept run eagerly between them, on its own scratch) give
+    # the eager call's decisions and tokens bit for bit
+    need_gpu()
+    import oracle
+    B, k, V = 32, 3, 32768
+    zt = t32(synth.normal_logits((B, k + 1, V), 3, "graph-noalloc-t"))
+    zq_np = synth.normal_logits((B, k, V), 3, "graph-noalloc-q")
+    ua, uf, ud = synth.uniforms(B, k, 4, "graph-noalloc")
+    q = oracle.softmax(zq_np.astype(np.float64))
+    drafts = i32(np.stack([oracle.inverse_cdf_rows(q[:, i], ud[:, i])[0] for i in range(k)], 1))
+    zq, ua, uf = t32(zq_np), t32(ua), t32(uf)
+    n = torch.zeros(B, dtype=torch.int32, device="cuda")
+    out = torch.zeros((B, k + 1), dtype=torch.int32, device="cuda")
+    n2, out2 = torch.zeros_like(n), torch.zeros_like(out)
+    ws = gm.Workspace()
+
+    def reset():
+        for t in (n, out, n2, out2):
+            t.fill_(-7)
+
+    def call():
+        gm.spec_accept_noalloc(zt, zq, drafts, ua, uf, n, out, gm.GM_SAMPLE, top_p=top_p)
+
+    reset()
+    call()
+    torch.cuda.synchronize()
+    ref_n, ref_out = n.clone(), out.clone()
+    assert int((ref_n >= 0).sum()) == B
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        call()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call()
+    for r in range(3):
+        reset()
+        g.replay()
+        gm.spec_accept(zt, zq, drafts, ua, uf, n2, out2, gm.GM_SAMPLE, ws, top_p=top_p)   # eager, between replays
+        torch.cuda.synchronize()
+        assert torch.equal(n, ref_n) and torch.equal(out, ref_out), "replay %d differs from the eager call" % r
+        assert torch.equal(n2, ref_n) and torch.equal(out2, ref_out), "workspace accept after replay %d differs" % r
+    print("[graph no-alloc accept top_p=%.1f] 3 replays identical to the eager call (mean accepted %.2f)"
+          % (top_p, float(ref_n.float().mean())), flush=True)

@@ -444,9 +444,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF g) {
 // Persistent strip ranges: as many waves as the chip holds, each owning a
 // contiguous range of 16-column weight strips (at most kLmStrips, balanced to
 // within one strip over all waves) over the whole K.  A wave streams its weight
-// tiles through a kLmRing-step register ring with unconditional loads (every
-// wave loads kLmStrips strips, the last one again where its range is shorter,
-// so the four waves of a workgroup keep pace).  The activation fragments (64
+// tiles through a kLmRing-step register ring with unconditional loads (kLmStrips
+// or kLmStrips - 1 strips, the last one again where its range is shorter, so
+// the four waves of a workgroup keep pace).  The activation fragments (64
 // rows) are shared by the workgroup's four waves: each stages a quarter of every
 // kLmChunk-step chunk in LDS, in the A-operand order, with direct-to-LDS loads one
 // chunk ahead, and one barrier per chunk hands the chunk over (measured at 64

@@ -74,9 +74,10 @@ __device__ __forceinline__ int xcd_remap(int bid, int T) {
 
 // MT: 16-row tiles per compute wave; NT: 16-column strips per compute wave;
 // WM: compute waves along M (1 or 2); SW: weights loaded non-temporally (one M
-// tile); CW: compute waves (4, or 7 for wide outputs: two per SIMD on three of
-// the SIMDs, 224-column tiles, the last tile of a launch clamped to the
-// output).  Waves 0 .. CW - 1 compute; wave CW only stages the A chunks in LDS.
+// tile); CW: compute waves (4; for wide outputs 7, two per SIMD on three of
+// the SIMDs with 224-column tiles, or 5 with 160-column tiles; the last tile of
+// a launch clamped to the output).  Waves 0 .. CW - 1 compute; wave CW only
+// stages the A chunks in LDS.
 // The wait counter of loads is per wave, so the loader's waits for A never
 // drain the compute waves' weight ring.
 template <int MT, int NT, int WM, int EPI, bool SW, int CW>
@@ -170,7 +171,7 @@ __global__ __launch_bounds__(gemm_threads<CW>()) void gemm_stream_kernel(GemmS g
     const int kt_total = g.K / 32;
     const uint16_t *wbase[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t)   // strips past the weight (the last 224-column tile) re-read the last one
+    for (int t = 0; t < NT; ++t)   // strips past the weight (the last wide tile) re-read the last one
       wbase[t] = g.W + w_tile(CW == 4 ? strip[t] : min(strip[t], g.Nw / 16 - 1), k_begin / 32, kt_total) + lane * 8;
     // Slot d of the ring holds step d mod D.  Each step first refills the slot
     // consumed by the step before (its registers are dead), then consumes its

@@ -57,7 +57,7 @@ enum GemmEpi {
 };
 struct GemmPlan {
   int shape, Nw, n_tiles, m_tiles, k_iters, splits;
-  int cw;              // compute waves per workgroup (4: 128-column tiles, 7: 224-column tiles)
+  int cw;              // compute waves per workgroup (4, 5, 7: 128-, 160-, 224-column tiles)
   size_t part_bytes;   // float32 K-split partials
 };
 GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K);

@@ -590,14 +590,41 @@ constexpr int kNucBins = 4096;
 constexpr int kNucQueue = 12288;     // logits and ids of the boundary's 12-bit bin kept in LDS (96 KiB)
 constexpr int kNucTieRank = 2048;    // ties at the boundary ranked in LDS (more: a pass over the row)
 
+// exp(y) for -32 <= y <= 0 by Tang's table-driven reduction (ACM TOMS 15(2), 1989):
+// y = (64 q + j) ln2 / 64 + r with |r| <= ln2 / 128, exp(y) = 2^q 2^(j/64) exp(r), and
+// exp(r) by its Taylor polynomial to r^6 (truncation below 2^-64 at |r| <= ln2 / 128).
+// ln2 / 64 is split into a 32-bit head (k times it is exact for |k| < 2^21) and a tail;
+// tab[j] = 2^(j/64), filled per block (nuc_exp_table).  A few ulps in all, far below
+// the 2^-44 units the masses are rounded to.
+__device__ __forceinline__ double nuc_exp(double y, const double *tab) {
+  constexpr double kLn2Hi = 0x1.62e42feep-1 / 64.0, kLn2Lo = 0x1.a39ef35793c76p-33 / 64.0;
+  const double kd = rint(y * (64.0 / 0x1.62e42fefa39efp-1));
+  double r = fma(-kd, kLn2Hi, y);
+  r = fma(-kd, kLn2Lo, r);
+  double p = 1.0 / 720.0;
+  p = fma(p, r, 1.0 / 120.0);
+  p = fma(p, r, 1.0 / 24.0);
+  p = fma(p, r, 1.0 / 6.0);
+  p = fma(p, r, 0.5);
+  p = fma(p, r, 1.0);
+  p = fma(p, r, 1.0);
+  const int k = (int)kd;
+  return ldexp(tab[k & 63] * p, k >> 6);
+}
+
+// the block's table of 2^(j/64), j = 0..63 (before the block's first barrier)
+__device__ __forceinline__ void nuc_exp_table(double *tab) {
+  if (threadIdx.x < 64) tab[threadIdx.x] = exp2((double)threadIdx.x / 64.0);
+}
+
 // mass of one id in 2^-44 units (the same operations at every call: no contraction)
-__device__ __forceinline__ unsigned long long nuc_mass(float v, double inv_td, double m) {
+__device__ __forceinline__ unsigned long long nuc_mass(float v, double inv_td, double m, const double *tab) {
 #pragma clang fp contract(off)
   const double y = (double)v * inv_td - m;
   if (!(y >= -32.0)) return 0ull;          // exp(-32) 2^44 < 0.5: rounds to 0 (and -inf, NaN)
   // exp(y) 2^44 < 2^52: adding 2^52 leaves its nearest integer (ties to even) in the
   // low mantissa bits
-  const double t = exp(y) * 0x1p44 + 0x1p52;
+  const double t = nuc_exp(y, tab) * 0x1p44 + 0x1p52;
   return (unsigned long long)(__double_as_longlong(t) - 0x4330000000000000ll);
 }
 
@@ -740,14 +767,16 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_hist_kernel(int V, double
   __shared__ unsigned long long hist[kNucBins];
   __shared__ float red_m[kNucThreads / 64];
   __shared__ int red_a[kNucThreads / 64];
+  __shared__ double etab[64];
   const int r = blockIdx.x / S, sg = blockIdx.x % S, tid = threadIdx.x;
   const float *row = logits + (long)r * row_stride;
+  nuc_exp_table(etab);
   for (int b = tid; b < kNucBins; b += kNucThreads) hist[b] = 0ull;
   const double m = nuc_reference(row, st + (long)r * nch, nch, V, inv_td, red_m, red_a);
   const int lo = (int)(((long)V * sg / S) & ~3l), hi = sg + 1 == S ? V : (int)(((long)V * (sg + 1) / S) & ~3l);
   const bool vec = (V & 3) == 0 && (row_stride & 3) == 0 && (reinterpret_cast<uintptr_t>(logits) & 15) == 0;
   nuc_visit(row + lo, hi - lo, vec, [&](float v, int) {
-    const unsigned long long e = nuc_mass(v, inv_td, m);
+    const unsigned long long e = nuc_mass(v, inv_td, m, etab);
     if (e) atomicAdd(&hist[order_key(v) >> 20], e);
   });
   __syncthreads();
@@ -769,9 +798,11 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
   __shared__ int red_a[kNucThreads / 64];
   __shared__ int sh_bin, sh_idt;
   __shared__ unsigned long long sh_above;
+  __shared__ double etab[64];
   const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const float *row = logits + (long)r * row_stride;
 
+  nuc_exp_table(etab);
   for (int b = tid; b < kNucBins; b += kNucThreads) hist[b] = 0ull;
   const double m = nuc_reference(row, st + (long)r * nch, nch, V, inv_td, red_m, red_a);
 
@@ -786,7 +817,7 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
     }
   } else {
     nuc_visit(row, V, vec, [&](float v, int) {
-      const unsigned long long e = nuc_mass(v, inv_td, m);
+      const unsigned long long e = nuc_mass(v, inv_td, m, etab);
       if (e) atomicAdd(&hist[order_key(v) >> 20], e);
     });
   }
@@ -833,12 +864,12 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
   if (queued) {
     for (unsigned i = tid; i < qn; i += kNucThreads) {
       const float v = qv[i];
-      atomicAdd(&hist[(order_key(v) >> 8) & 0xfffu], nuc_mass(v, inv_td, m));
+      atomicAdd(&hist[(order_key(v) >> 8) & 0xfffu], nuc_mass(v, inv_td, m, etab));
     }
   } else {
     nuc_visit(row, V, vec, [&](float v, int) {
       const uint32_t k = order_key(v);
-      if ((k >> 20) == b1) atomicAdd(&hist[(k >> 8) & 0xfffu], nuc_mass(v, inv_td, m));
+      if ((k >> 20) == b1) atomicAdd(&hist[(k >> 8) & 0xfffu], nuc_mass(v, inv_td, m, etab));
     });
   }
   __syncthreads();
@@ -853,12 +884,12 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
     for (unsigned i = tid; i < qn; i += kNucThreads) {
       const float v = qv[i];
       const uint32_t k = order_key(v);
-      if ((k >> 8) == pre) atomicAdd(&hist[k & 0xffu], nuc_mass(v, inv_td, m));
+      if ((k >> 8) == pre) atomicAdd(&hist[k & 0xffu], nuc_mass(v, inv_td, m, etab));
     }
   } else {
     nuc_visit(row, V, vec, [&](float v, int) {
       const uint32_t k = order_key(v);
-      if ((k >> 8) == pre) atomicAdd(&hist[k & 0xffu], nuc_mass(v, inv_td, m));
+      if ((k >> 8) == pre) atomicAdd(&hist[k & 0xffu], nuc_mass(v, inv_td, m, etab));
     });
   }
   __syncthreads();
@@ -866,7 +897,7 @@ __global__ __launch_bounds__(kNucThreads) void nucleus_kernel(int V, double inv_
   const uint32_t key = (pre << 8) | (uint32_t)sh_bin;
   above = sh_above;
   const unsigned long long hk = hist[sh_bin];          // cnt ids of equal mass et
-  const unsigned long long et = nuc_mass(key_value(key), inv_td, m);
+  const unsigned long long et = nuc_mass(key_value(key), inv_td, m, etab);
   const long long cnt = et ? (long long)(hk / et) : 1;
   // the fewest of them that reach thr (at least one, at most all)
   long long j = (long long)ceil((thr - (double)above) / (double)et);
